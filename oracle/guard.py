@@ -1,0 +1,126 @@
+"""Guard-banded parity cases -- TEST INFRASTRUCTURE ONLY.
+
+Builds one verification step's inputs from the seeded generator and runs the
+oracle on them, redrawing inputs until every discrete decision the oracle
+takes sits at least a stated distance from a tie:
+
+* scheduler: every throughput comparison made satisfies
+  |Theta - Theta_best| >= SCHED_GUARD * Theta_best.  The GPU sums the
+  survival probabilities in a different order than the oracle's sequential
+  loop; for at most 4608 fp64 terms in [0, 1] the two sums differ by at most
+  about 1.1e-12 relative, so a 1e-9 band makes equal decisions certain.  (A
+  1e-4 band is unreachable here: the greedy stop happens exactly where the
+  marginal throughput gain crosses zero, typically 1e-6..1e-9 from a tie.)
+* acceptance test: |u - min(1, p_t(x) / p_d(x))| >= ACCEPT_GUARD;
+* final draw: u * mass at least ACCEPT_GUARD (in units of the total mass)
+  from both edges of the chosen token's bucket.
+
+Redraws use fresh sub-streams of the generator (confidences as a whole,
+uniforms per request), at most ``max_tries`` times; requests still inside the
+band are listed in ``unguarded`` and left out of exact comparisons.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import List, Optional
+
+import numpy as np
+
+import oracle
+from paper_2607_05147_amd import synth
+
+SCHED_GUARD = 1e-9
+ACCEPT_GUARD = 1e-4
+
+
+@dataclass
+class StepCase:
+    w: synth.Workload
+    seed: int
+    conf: np.ndarray
+    sps: np.ndarray
+    len: np.ndarray  # oracle schedule
+    cu_q: np.ndarray
+    sched_margin: float
+    sched_guarded: bool
+    kv: Optional[synth.PagedKV] = None
+    q: Optional[np.ndarray] = None  # [total_q, Hq, Dqk]
+    logits: Optional[np.ndarray] = None  # [total_q, V]
+    drafts: Optional[synth.Drafts] = None
+    accepted_len: Optional[np.ndarray] = None  # oracle acceptance
+    next_tok: Optional[np.ndarray] = None
+    accept_margin: Optional[np.ndarray] = None
+    unguarded: List[int] = field(default_factory=list)
+
+    @property
+    def total_q(self) -> int:
+        return int(self.cu_q[-1])
+
+    @property
+    def q_len(self) -> np.ndarray:
+        return np.diff(self.cu_q)
+
+
+def schedule_case(w: synth.Workload, seed: int, mode: int = 0, max_tries: int = 64,
+                  guard: float = SCHED_GUARD) -> StepCase:
+    sps = synth.sps_table(w)
+    best = None
+    for attempt in range(max_tries):
+        conf = synth.confidences(w, seed, attempt)
+        ln, _, _, mm = oracle.schedule(conf, sps, mode)
+        if best is None or mm > best[3]:
+            best = (conf, ln, attempt, mm)
+        if mm >= guard:
+            break
+    conf, ln, _, mm = best
+    return StepCase(w=w, seed=seed, conf=conf, sps=sps, len=ln, cu_q=oracle.cu_from_len(ln),
+                    sched_margin=mm, sched_guarded=mm >= guard)
+
+
+def _accept_subset(case: StepCase, reqs: List[int], u: np.ndarray):
+    """Oracle acceptance for a subset of requests (rows gathered)."""
+    w = case.w
+    cu = case.cu_q
+    rows = np.concatenate([np.arange(cu[r], cu[r + 1]) for r in reqs])
+    sub_cu = oracle.cu_from_len(case.len[reqs])
+    dr = case.drafts
+    acc, nxt, mg, _ = oracle.accept(
+        dr.draft_tok[reqs], None if dr.draft_p is None else dr.draft_p[reqs],
+        case.logits[rows], w.logit_dtype, sub_cu, w.K, w.V,
+        u=None if u is None else u[reqs])
+    return acc, nxt, mg
+
+
+def build_case(w: synth.Workload, seed: int, mode: int = 0, with_kv: bool = True,
+               with_accept: bool = True, max_tries: int = 64,
+               guard: float = ACCEPT_GUARD) -> StepCase:
+    """Schedule (guarded), then KV/queries and logits/drafts (guarded)."""
+    case = schedule_case(w, seed, mode=mode, max_tries=max_tries)
+    keys = synth.flat_keys(case.q_len)
+    if with_kv:
+        case.kv = synth.paged_kv(w, seed)
+        case.q = synth.query_rows(w, seed, keys)
+    if not with_accept:
+        return case
+    case.logits = synth.logit_rows(w, seed, keys)
+    needed = np.arange(w.K)[None, :] < case.len[:, None]
+    attempts = np.zeros(w.R, dtype=np.int64)
+    case.drafts = synth.drafts(w, seed, case.conf, needed=needed, u_attempts=attempts)
+    R = w.R
+    acc = np.zeros(R, np.int32)
+    nxt = np.zeros(R, np.int32)
+    mg = np.full(R, np.inf)
+    todo = list(range(R))
+    u = case.drafts.u
+    for _ in range(max_tries):
+        a, n, m = _accept_subset(case, todo, u)
+        acc[todo], nxt[todo], mg[todo] = a, n, m
+        todo = [r for r in todo if mg[r] < guard]
+        if not todo or w.greedy:
+            break
+        for r in todo:
+            attempts[r] += 1
+            u[r] = synth.uniforms(w, seed, r, int(attempts[r]))
+    case.accepted_len, case.next_tok, case.accept_margin = acc, nxt, mg
+    case.unguarded = [] if w.greedy else [r for r in range(R) if mg[r] < guard]
+    return case

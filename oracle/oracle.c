@@ -1,0 +1,426 @@
+/*
+ * Plain fp64 CPU oracle for DSpark's batched verification step.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path links, loads or
+ * calls this file: only the test suite, the smoke check and the CPU-baseline
+ * leg of the benchmark do.  It shares no code, header, table or constant with
+ * the GPU library.
+ *
+ * It is deliberately slow and literal:
+ *   - scheduling follows the hardware-aware prefix scheduler (Algorithm 1 of
+ *     the section on confidence-scheduled verification) step by step;
+ *   - attention is the textbook masked softmax attention, written out;
+ *   - acceptance is the left-to-right speculative acceptance rule of the
+ *     background section on speculative decoding, with the conventions listed
+ *     at each function.
+ * All arithmetic is fp64; bf16 inputs are widened exactly.  OpenMP only runs
+ * independent rows side by side; no row's arithmetic is reordered.
+ *
+ * Parity pins: every function here is pinned by tests against values printed
+ * in the paper's appendix counterexample, closed forms, library routines and
+ * brute force on tiny inputs.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define ORACLE_OK 0
+#define ORACLE_EINVAL 1
+
+/* ----------------------------------------------------------------- helpers */
+
+static double bf16_to_f64(uint16_t b) {
+    uint32_t u = ((uint32_t)b) << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+/* dtype 0 = fp32, 1 = bf16 (uint16 bit patterns) */
+static double elem(const void* base, int64_t i, int dtype) {
+    if (dtype == 0) return (double)((const float*)base)[i];
+    return bf16_to_f64(((const uint16_t*)base)[i]);
+}
+
+/* Confidence as used in the survival product.  The paper takes c in (0,1);
+   a value that is not > 0 (zero, negative, NaN) ends the request's candidate
+   list, a value above 1 is read as 1. */
+static double conf_value(float c) {
+    if (!(c > 0.0f)) return 0.0;
+    if (c > 1.0f) return 1.0;
+    return (double)c;
+}
+
+/* ------------------------------------------------------- prefix survival */
+
+/* Prefix survival probabilities a[r, j-1] = prod_{i<=j} c[r, i]
+   (Algorithm 1, first loop; "Hardware-Aware Prefix Scheduler" section).
+   Sequential fp64 multiplication in increasing j. */
+int oracle_survival(const float* conf, int R, int K, double* a) {
+    if (!conf || !a || R < 0 || K < 0) return ORACLE_EINVAL;
+    for (int r = 0; r < R; ++r) {
+        double p = 1.0;
+        for (int j = 0; j < K; ++j) {
+            double c = conf_value(conf[(int64_t)r * K + j]);
+            p = p * c;
+            a[(int64_t)r * K + j] = p;
+        }
+    }
+    return ORACLE_OK;
+}
+
+/* -------------------------------------------------- Algorithm 1 scheduler */
+
+typedef struct {
+    double a;
+    int32_t r;
+    int32_t j; /* 1-based draft position */
+} cand_t;
+
+/* Descending survival; ties by request, then position, ascending. */
+static int cand_order(const void* x, const void* y) {
+    const cand_t* p = (const cand_t*)x;
+    const cand_t* q = (const cand_t*)y;
+    if (p->a > q->a) return -1;
+    if (p->a < q->a) return 1;
+    if (p->r != q->r) return p->r < q->r ? -1 : 1;
+    if (p->j != q->j) return p->j < q->j ? -1 : 1;
+    return 0;
+}
+
+/*
+ * Algorithm 1 ("Hardware-Aware Prefix Scheduler").
+ *   conf [R, K] fp32, sps [sps_len] fp64 with sps[B] = steps/s at B verify
+ *   tokens (B = sum_r (1 + l_r)); sps_len must exceed R*(K+1).
+ *   mode 0: causal greedy with early stop (the algorithm as printed);
+ *   mode 1: no break -- the same greedy path, keeping the best prefix of it
+ *           (the production variant of the "scheduler in practice" section).
+ * Outputs: len[R] = l*_r; *theta_best; *n_admitted = number of admitted
+ * candidates; *min_margin = min over the throughput comparisons made of
+ * |Theta - Theta_best| / Theta_best (how far the decisions are from a tie).
+ * theta_trace (nullable, room for R*K+1 values) receives Theta_0, Theta_1, ...
+ * for every step evaluated, and *n_trace their count.
+ */
+int oracle_schedule(const float* conf, int R, int K, const double* sps, int64_t sps_len,
+                    int mode, int32_t* len, double* theta_best_out, int32_t* n_admitted_out,
+                    double* min_margin_out, double* theta_trace, int64_t* n_trace) {
+    if (!conf || !sps || !len || R <= 0 || K < 0) return ORACLE_EINVAL;
+    if (mode != 0 && mode != 1) return ORACLE_EINVAL;
+    if (sps_len <= (int64_t)R * (K + 1)) return ORACLE_EINVAL;
+
+    double* a = (double*)malloc(sizeof(double) * ((size_t)R * K + 1));
+    cand_t* E = (cand_t*)malloc(sizeof(cand_t) * ((size_t)R * K + 1));
+    int32_t* l = (int32_t*)calloc((size_t)R, sizeof(int32_t));
+    if (!a || !E || !l) { free(a); free(E); free(l); return ORACLE_EINVAL; }
+
+    /* survival probabilities */
+    oracle_survival(conf, R, K, a);
+
+    /* candidate space {(r, j) : a_{r,j} > 0}, sorted descending by a */
+    int64_t n = 0;
+    for (int r = 0; r < R; ++r)
+        for (int j = 1; j <= K; ++j) {
+            double v = a[(int64_t)r * K + (j - 1)];
+            if (v > 0.0) { E[n].a = v; E[n].r = r; E[n].j = j; ++n; }
+        }
+    qsort(E, (size_t)n, sizeof(cand_t), cand_order);
+
+    /* initial state */
+    for (int r = 0; r < R; ++r) { l[r] = 0; len[r] = 0; }
+    int64_t B = R;
+    double tau = (double)R;
+    double theta_best = (double)R * sps[R];
+    double min_margin = INFINITY;
+    int32_t admitted = 0;
+    int64_t nt = 0;
+    if (theta_trace) theta_trace[nt] = theta_best;
+    ++nt;
+
+    for (int64_t i = 0; i < n; ++i) {
+        l[E[i].r] = E[i].j;
+        B = B + 1;
+        tau = tau + E[i].a;
+        double theta = tau * sps[B];
+        if (theta_trace) theta_trace[nt] = theta;
+        ++nt;
+        double m = fabs(theta - theta_best) / theta_best;
+        if (m < min_margin) min_margin = m;
+        if (theta > theta_best) {
+            theta_best = theta;
+            for (int r = 0; r < R; ++r) len[r] = l[r]; /* snapshot l* <- l */
+            admitted = (int32_t)(i + 1);
+        } else if (mode == 0) {
+            break;
+        }
+    }
+    if (theta_best_out) *theta_best_out = theta_best;
+    if (n_admitted_out) *n_admitted_out = admitted;
+    if (min_margin_out) *min_margin_out = min_margin;
+    if (n_trace) *n_trace = nt;
+    free(a); free(E); free(l);
+    return ORACLE_OK;
+}
+
+/* -------------------------------------------------------- verify attention */
+
+/*
+ * Ragged causal verify attention over a paged KV cache.
+ *   Request r owns q_len_r = cu_q[r+1] - cu_q[r] consecutive query tokens of
+ *   q [total_q, Hq, Dqk]; its context holds kv_len_r tokens, the last q_len_r
+ *   of which are the verify tokens themselves, so query t (0-based) sees keys
+ *   0 .. kv_len_r - q_len_r + t.  Key token j lives in page
+ *   block_table[r, j / page_size], slot j % page_size; element (page, head,
+ *   slot, d) is at page*s[0] + head*s[1] + slot*s[2] + d.  Query head h reads
+ *   KV head h / (Hq / Hkv).
+ *   o = sum_j softmax_j(scale * <q, k_j>) v_j ;  lse = log sum_j exp(scale <q,k_j>).
+ * If rows != NULL only the n_rows listed (token, head) pairs are computed and
+ * written, packed in list order; otherwise all total_q * Hq rows are written
+ * in [token, head] order.  out: fp64 [.., Dv], lse: fp64 [..] (nullable).
+ */
+int oracle_verify_attn(const void* q, const void* k_cache, const void* v_cache,
+                       const int64_t* ks, const int64_t* vs, const int32_t* block_table,
+                       int max_pages, const int32_t* kv_len, const int32_t* cu_q, int R,
+                       int Hq, int Hkv, int Dqk, int Dv, int page_size, double scale,
+                       int dtype, const int32_t* rows, int64_t n_rows, double* out,
+                       double* lse) {
+    if (!q || !k_cache || !v_cache || !ks || !vs || !block_table || !kv_len || !cu_q || !out)
+        return ORACLE_EINVAL;
+    if (R <= 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv || Dqk <= 0 || Dv <= 0 || page_size <= 0)
+        return ORACLE_EINVAL;
+    for (int r = 0; r < R; ++r) {
+        int ql = cu_q[r + 1] - cu_q[r];
+        if (ql < 0 || kv_len[r] < ql || kv_len[r] > (int64_t)max_pages * page_size)
+            return ORACLE_EINVAL;
+    }
+    const int64_t total_q = cu_q[R];
+    const int64_t count = rows ? n_rows : total_q * Hq;
+    const int group = Hq / Hkv;
+
+    /* token -> request */
+    int32_t* req_of = (int32_t*)malloc(sizeof(int32_t) * (size_t)(total_q + 1));
+    if (!req_of) return ORACLE_EINVAL;
+    for (int r = 0; r < R; ++r)
+        for (int t = cu_q[r]; t < cu_q[r + 1]; ++t) req_of[t] = r;
+    if (rows)
+        for (int64_t i = 0; i < count; ++i)
+            if (rows[2 * i] < 0 || rows[2 * i] >= total_q || rows[2 * i + 1] < 0 ||
+                rows[2 * i + 1] >= Hq) { free(req_of); return ORACLE_EINVAL; }
+
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 4) reduction(| : bad)
+    for (int64_t i = 0; i < count; ++i) {
+        int64_t tok = rows ? rows[2 * i] : i / Hq;
+        int h = rows ? rows[2 * i + 1] : (int)(i % Hq);
+        int r = req_of[tok];
+        int ql = cu_q[r + 1] - cu_q[r];
+        int t = (int)(tok - cu_q[r]);
+        int64_t visible = (int64_t)kv_len[r] - ql + t + 1;
+        int g = h / group;
+        double* s = (double*)malloc(sizeof(double) * (size_t)(visible > 0 ? visible : 1));
+        if (!s) { bad = 1; continue; }
+        const int64_t qoff = (tok * Hq + h) * (int64_t)Dqk;
+        for (int64_t j = 0; j < visible; ++j) {
+            int64_t page = block_table[(int64_t)r * max_pages + j / page_size];
+            int64_t base = page * ks[0] + g * ks[1] + (j % page_size) * ks[2];
+            double dot = 0.0;
+            for (int d = 0; d < Dqk; ++d)
+                dot += elem(q, qoff + d, dtype) * elem(k_cache, base + d, dtype);
+            s[j] = scale * dot;
+        }
+        double m = -INFINITY;
+        for (int64_t j = 0; j < visible; ++j) if (s[j] > m) m = s[j];
+        double den = 0.0;
+        for (int64_t j = 0; j < visible; ++j) { s[j] = exp(s[j] - m); den += s[j]; }
+        double* o = out + i * (int64_t)Dv;
+        for (int d = 0; d < Dv; ++d) o[d] = 0.0;
+        for (int64_t j = 0; j < visible; ++j) {
+            int64_t page = block_table[(int64_t)r * max_pages + j / page_size];
+            int64_t base = page * vs[0] + g * vs[1] + (j % page_size) * vs[2];
+            double w = s[j] / den;
+            for (int d = 0; d < Dv; ++d) o[d] += w * elem(v_cache, base + d, dtype);
+        }
+        if (lse) lse[i] = m + log(den);
+        free(s);
+    }
+    free(req_of);
+    return bad ? ORACLE_EINVAL : ORACLE_OK;
+}
+
+/* ------------------------------------------------------------- acceptance */
+
+/* Target distribution p = softmax(inv_temp * z) of one logit row, fp64. */
+static void target_dist(const void* row, int dtype, int V, double inv_temp, double* p) {
+    double m = -INFINITY;
+    for (int v = 0; v < V; ++v) {
+        p[v] = inv_temp * elem(row, v, dtype);
+        if (p[v] > m) m = p[v];
+    }
+    double S = 0.0;
+    for (int v = 0; v < V; ++v) { p[v] = exp(p[v] - m); S += p[v]; }
+    for (int v = 0; v < V; ++v) p[v] = p[v] / S;
+}
+
+/* Index of the largest raw logit; the lowest index among equals. */
+static int argmax_row(const void* row, int dtype, int V) {
+    int best = 0;
+    double bv = elem(row, 0, dtype);
+    for (int v = 1; v < V; ++v) {
+        double x = elem(row, v, dtype);
+        if (x > bv) { bv = x; best = v; }
+    }
+    return best;
+}
+
+/* Inverse-CDF draw from unnormalised non-negative masses with one uniform:
+   the smallest v (ascending vocabulary order) whose running mass exceeds
+   u * total.  *margin = distance of u*total from the chosen bucket's edges,
+   in units of the total mass. */
+static int inverse_cdf(const double* mass, int V, double u, double* margin) {
+    double total = 0.0;
+    for (int v = 0; v < V; ++v) total += mass[v];
+    double thr = u * total;
+    double cum = 0.0;
+    int last_pos = 0;
+    for (int v = 0; v < V; ++v) {
+        double prev = cum;
+        cum += mass[v];
+        if (mass[v] > 0.0) last_pos = v;
+        if (cum > thr) {
+            double m1 = (thr - prev) / total, m2 = (cum - thr) / total;
+            *margin = m1 < m2 ? m1 : m2;
+            return v;
+        }
+    }
+    *margin = 0.0;
+    return last_pos;
+}
+
+/*
+ * Speculative acceptance for every request.
+ *   Rows: logits row cu_q[r] + t (row stride ld elements) is the target's
+ *   distribution for the token after verify slot t; slot t < l_r tests draft
+ *   token draft_tok[r, t] (the paper's x_{t+1}), slot l_r supplies the bonus
+ *   token.  l_r = q_len_r - 1 must not exceed K.
+ *   Greedy (draft_p == NULL and u == NULL): x_{t+1} is accepted iff it equals
+ *     the argmax of the raw logits (lowest index on ties); the emitted token is
+ *     the argmax of the first rejected row, or of row l_r if all are accepted.
+ *   Stochastic: p_t = softmax(inv_temp * z_t); x_{t+1} is accepted iff
+ *     u[r, t] < p_t(x) / p_d(x) (p_d(x) = 0 accepts), i.e. with probability
+ *     min(1, p_t/p_d); left to right, the first rejection at t* ends the
+ *     request and the corrected token is drawn from max(0, p_t - p_d) (p_t if
+ *     that has no mass); with no rejection the bonus token is drawn from
+ *     p_{l_r}.  Draws use the inverse CDF at u[r, K].
+ * Outputs accepted_len[R], next_tok[R]; margin[R] (nullable) = the smallest
+ * distance of any stochastic decision taken from its tie (|u - min(1,ratio)|
+ * for tests, CDF units for the draw), +inf for greedy requests.
+ * accept_rate (nullable, [total_q]) = sum_v min(p_t(v), p_d(v)) for every
+ * row t < l_r that carries a draft, whether or not an earlier draft was
+ * rejected (the analytic per-step acceptance rate of the confidence-head
+ * section: one minus the total variation distance); -1 for bonus rows and in
+ * greedy mode.
+ */
+int oracle_accept(const int32_t* draft_tok, const float* draft_p, const void* logits,
+                  int logit_dtype, int64_t ld, const float* u, const int32_t* cu_q, int R,
+                  int K, int V, double inv_temp, int32_t* accepted_len, int32_t* next_tok,
+                  double* margin, double* accept_rate) {
+    if (!draft_tok || !logits || !cu_q || !accepted_len || !next_tok) return ORACLE_EINVAL;
+    if (R <= 0 || K < 0 || V <= 0 || ld < V || !(inv_temp > 0.0)) return ORACLE_EINVAL;
+    const int greedy = (draft_p == NULL && u == NULL);
+    if (!greedy && (draft_p == NULL || u == NULL)) return ORACLE_EINVAL;
+    const size_t esz = logit_dtype == 0 ? 4 : 2;
+    for (int r = 0; r < R; ++r) {
+        int ql = cu_q[r + 1] - cu_q[r];
+        if (ql < 1 || ql > K + 1) return ORACLE_EINVAL;
+        for (int t = 0; t < ql - 1; ++t) {
+            int32_t x = draft_tok[(int64_t)r * K + t];
+            if (x < 0 || x >= V) return ORACLE_EINVAL;
+        }
+    }
+    if (accept_rate)
+        for (int64_t i = 0; i < cu_q[R]; ++i) accept_rate[i] = -1.0;
+
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : bad)
+    for (int r = 0; r < R; ++r) {
+        const int l = cu_q[r + 1] - cu_q[r] - 1;
+        const char* base = (const char*)logits;
+        double mg = INFINITY;
+        int acc = l, tok = -1;
+        if (greedy) {
+            for (int t = 0; t < l; ++t) {
+                const void* row = base + (size_t)(cu_q[r] + t) * (size_t)ld * esz;
+                int am = argmax_row(row, logit_dtype, V);
+                if (draft_tok[(int64_t)r * K + t] != am) { acc = t; tok = am; break; }
+            }
+            if (tok < 0)
+                tok = argmax_row(base + (size_t)(cu_q[r] + l) * (size_t)ld * esz, logit_dtype, V);
+        } else {
+            double* p = (double*)malloc(sizeof(double) * (size_t)V);
+            double* m = (double*)malloc(sizeof(double) * (size_t)V);
+            if (!p || !m) { free(p); free(m); bad = 1; continue; }
+            if (accept_rate)
+                for (int t = 0; t < l; ++t) {
+                    const void* row = base + (size_t)(cu_q[r] + t) * (size_t)ld * esz;
+                    const float* pd = draft_p + ((int64_t)r * K + t) * (int64_t)V;
+                    target_dist(row, logit_dtype, V, inv_temp, p);
+                    double ar = 0.0;
+                    for (int v = 0; v < V; ++v) ar += p[v] < (double)pd[v] ? p[v] : (double)pd[v];
+                    accept_rate[cu_q[r] + t] = ar;
+                }
+            for (int t = 0; t < l; ++t) {
+                const void* row = base + (size_t)(cu_q[r] + t) * (size_t)ld * esz;
+                const float* pd = draft_p + ((int64_t)r * K + t) * (int64_t)V;
+                target_dist(row, logit_dtype, V, inv_temp, p);
+                int32_t x = draft_tok[(int64_t)r * K + t];
+                double pdx = (double)pd[x];
+                double ratio = pdx > 0.0 ? p[x] / pdx : INFINITY;
+                double uu = (double)u[(int64_t)r * (K + 1) + t];
+                double d = fabs(uu - (ratio < 1.0 ? ratio : 1.0));
+                if (d < mg) mg = d;
+                if (!(uu < ratio)) {
+                    acc = t;
+                    double tot = 0.0;
+                    for (int v = 0; v < V; ++v) {
+                        double e = p[v] - (double)pd[v];
+                        m[v] = e > 0.0 ? e : 0.0;
+                        tot += m[v];
+                    }
+                    if (!(tot > 0.0)) memcpy(m, p, sizeof(double) * (size_t)V);
+                    double cm;
+                    tok = inverse_cdf(m, V, (double)u[(int64_t)r * (K + 1) + K], &cm);
+                    if (cm < mg) mg = cm;
+                    break;
+                }
+            }
+            if (tok < 0) {
+                const void* row = base + (size_t)(cu_q[r] + l) * (size_t)ld * esz;
+                target_dist(row, logit_dtype, V, inv_temp, p);
+                double cm;
+                tok = inverse_cdf(p, V, (double)u[(int64_t)r * (K + 1) + K], &cm);
+                if (cm < mg) mg = cm;
+            }
+            free(p); free(m);
+        }
+        accepted_len[r] = acc;
+        next_tok[r] = tok;
+        if (margin) margin[r] = mg;
+    }
+    return bad ? ORACLE_EINVAL : ORACLE_OK;
+}
+
+/* Reports how many OpenMP threads a parallel region of the oracle uses. */
+int oracle_threads(void) {
+    int n = 1;
+#ifdef _OPENMP
+#pragma omp parallel
+    {
+#pragma omp single
+        n = omp_get_num_threads();
+    }
+#endif
+    return n;
+}

@@ -1,0 +1,21 @@
+"""MI355X-native batched verification step of confidence-scheduled speculative decoding.
+
+Three stages, each a hand-written HIP kernel for gfx950 behind the C ABI in
+``include/dspark.h``: the hardware-aware prefix scheduler, ragged paged verify
+attention and speculative acceptance.  The binding (``paper_2607_05147_amd.dspark``)
+is loaded on first use so that the input generator (``synth``) can be imported
+without the GPU library.
+"""
+
+_BINDING_NAMES = (
+    "dspark_abi_version", "dspark_last_error", "dspark_schedule", "dspark_verify_attn",
+    "dspark_accept", "dspark_schedule_workspace_size", "dspark_verify_attn_workspace_size",
+    "dspark_accept_workspace_size", "DSparkError",
+)
+
+
+def __getattr__(name):
+    if name in _BINDING_NAMES:
+        from . import dspark
+        return getattr(dspark, name)
+    raise AttributeError(name)

@@ -1,0 +1,265 @@
+"""Pins for the oracle's speculative acceptance.
+
+References outside the oracle: the appendix counterexample's printed
+probabilities (acceptance 0.8, min(1, 0.7/0.5) = 1, the biased first-token
+law (0.85, 0.15) under the retrospective scheduler versus (0.7, 0.3) with the
+early stop); losslessness of rejection sampling (the emitted token follows the
+target law) checked by exhaustive integration over the uniforms on tiny
+vocabularies and by a chi-square test; the per-step acceptance probability
+sum_v min(p_t, p_d) = 1 - TV(p_t, p_d); numpy's argmax, cumsum and
+searchsorted for the greedy and inverse-CDF conventions.
+"""
+import numpy as np
+import pytest
+from scipy import stats
+from scipy.special import softmax
+
+import oracle
+
+
+def _tile_case(logit_rows, draft_p_rows, draft_tok, u):
+    """N identical requests (one logit block each) with per-request uniforms."""
+    N = u.shape[0]
+    L = logit_rows.shape[0] - 1
+    V = logit_rows.shape[1]
+    logits = np.ascontiguousarray(np.broadcast_to(logit_rows, (N,) + logit_rows.shape)
+                                  .reshape(N * (L + 1), V), dtype=np.float32)
+    K = draft_tok.shape[-1]
+    dp = None
+    if draft_p_rows is not None:
+        dp = np.ascontiguousarray(np.broadcast_to(draft_p_rows, (N, K, V)), dtype=np.float32)
+    tok = np.ascontiguousarray(np.broadcast_to(draft_tok, (N, K)), dtype=np.int32)
+    cu = np.arange(N + 1, dtype=np.int32) * (L + 1)
+    return logits, dp, tok, cu
+
+
+def _midpoints(n):
+    return ((np.arange(n) + 0.5) / n).astype(np.float32)
+
+
+def _first_token_law(p_t_logits, p_d, V, n=20000):
+    """Exact-by-grid law of the first emitted token with one verified draft.
+
+    Given x, acceptance depends only on u[0] and the corrected token only on
+    u[K]; integrate each over an n-point midpoint grid."""
+    law = np.zeros(V)
+    acc_prob = 0.0
+    grid = _midpoints(n)
+    for x in range(V):
+        rows = np.stack([p_t_logits, p_t_logits])  # row 0 tests x, row 1 = bonus
+        # acceptance probability given x: u[0] on the grid, u[K] anything
+        u = np.stack([grid, np.full(n, 0.5, np.float32)], axis=1)
+        logits, dp, tok, cu = _tile_case(rows, p_d[None, :], np.array([x]), u)
+        acc, nxt, _, _ = oracle.accept(tok, dp, logits, "f32", cu, 1, V, u=u)
+        pa = acc.mean()
+        acc_prob += p_d[x] * pa
+        law[x] += p_d[x] * pa
+        if pa < 1.0:
+            # corrected token given rejection: force u[0] -> 1, sweep u[K]
+            u = np.stack([np.full(n, np.float32(1.0 - 2 ** -24)), grid], axis=1)
+            acc, nxt, _, _ = oracle.accept(tok, dp, logits, "f32", cu, 1, V, u=u)
+            assert (acc == 0).all()
+            law += p_d[x] * (1 - pa) * np.bincount(nxt, minlength=V) / n
+    return law, acc_prob
+
+
+def test_appendix_acceptance_probabilities(appendix):
+    p_t = np.array(appendix["p_target"])
+    p_d = np.array(appendix["p_draft"], dtype=np.float32)
+    z = np.log(p_t).astype(np.float32)
+    law, acc = _first_token_law(z, p_d, 2)
+    assert acc == pytest.approx(appendix["accept_prob"], abs=2e-4)
+    # x_1 = A is always accepted: min(1, 0.7 / 0.5) = 1
+    n = 1000
+    u = np.stack([_midpoints(n), np.full(n, 0.5, np.float32)], axis=1)
+    logits, dp, tok, cu = _tile_case(np.stack([z, z]), p_d[None, :], np.array([0]), u)
+    a, _, _, _ = oracle.accept(tok, dp, logits, "f32", cu, 1, 2, u=u)
+    assert a.mean() == appendix["accept_prob_A"]
+    np.testing.assert_allclose(law, appendix["lossless_output"], atol=2e-4)
+
+
+def test_appendix_selection_bias(appendix):
+    """Scheduler + sampler: no-break selection biases the first token to
+    (0.85, 0.15); the early stop keeps the target law (0.7, 0.3)."""
+    sps = np.array([0.0, appendix["sps_1"], appendix["sps_2"], appendix["sps_3"]])
+    p_t = np.array(appendix["p_target"])
+    p_d = np.array(appendix["p_draft"], dtype=np.float32)
+    z = np.log(p_t).astype(np.float32)
+    c2_of = {0: appendix["case1_c2"], 1: appendix["case2_c2"]}  # x_1 = A -> high c_2
+    n = 20000
+    grid = _midpoints(n)
+    for mode, expect in ((1, appendix["biased_output"]), (0, appendix["lossless_output"])):
+        law = np.zeros(2)
+        for x in (0, 1):
+            conf = np.array([[appendix["a_1"], c2_of[x]]], dtype=np.float32)
+            ln, _, _, _ = oracle.schedule(conf, sps, mode)
+            L = int(ln[0])
+            rows = np.stack([z] * (L + 1))
+            # second draft token and its distribution are irrelevant to the first output
+            tok = np.array([x, 0])
+            u = np.stack([grid, grid, grid[::-1]], axis=1)
+            logits, dp, tk, cu = _tile_case(rows, np.stack([p_d, p_d]), tok, u)
+            acc, nxt, _, _ = oracle.accept(tk, dp, logits, "f32", cu, 2, 2, u=u)
+            first = np.where(acc >= 1, x, nxt)
+            law += p_d[x] * np.bincount(first, minlength=2) / n
+        np.testing.assert_allclose(law, expect, atol=5e-4)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_lossless_by_enumeration(seed):
+    rng = np.random.default_rng(seed)
+    V = 3 if seed < 3 else 5
+    z = (rng.normal(size=V) * 1.5).astype(np.float32)
+    p_d = rng.dirichlet(np.ones(V) * 0.7).astype(np.float32)
+    p_d = (p_d / p_d.sum()).astype(np.float32)
+    p_t = softmax(z.astype(np.float64))
+    law, acc = _first_token_law(z, p_d, V)
+    # grid error: one boundary per decision piece -> O(V / n)
+    np.testing.assert_allclose(law, p_t, atol=V * 1e-4)
+    assert acc == pytest.approx(np.minimum(p_t, p_d).sum(), abs=V * 1e-4)
+
+
+def test_accept_rate_is_one_minus_tv():
+    rng = np.random.default_rng(7)
+    V, L = 64, 4
+    z = (rng.normal(size=(L + 1, V)) * 3).astype(np.float32)
+    p_d = rng.dirichlet(np.ones(V) * 0.3, size=L).astype(np.float32)
+    tok = rng.integers(0, V, size=(1, L)).astype(np.int32)
+    u = rng.random((1, L + 1)).astype(np.float32)
+    cu = np.array([0, L + 1], np.int32)
+    _, _, _, rate = oracle.accept(tok, p_d[None], z, "f32", cu, L, V, u=u, want_rate=True)
+    p_t = softmax(z.astype(np.float64), axis=1)
+    tv = 0.5 * np.abs(p_t[:L] - p_d.astype(np.float64)).sum(1)
+    mass_gap = 0.5 * (1.0 - p_d.astype(np.float64).sum(1))  # fp32 draft rows sum to 1 +- eps
+    np.testing.assert_allclose(rate[:L], 1.0 - tv - mass_gap, atol=1e-12)
+    assert rate[L] == -1.0
+
+
+def test_chi_square_two_positions():
+    rng = np.random.default_rng(11)
+    V, L, N = 16, 3, 100000
+    z = (rng.normal(size=(L + 1, V)) * 2).astype(np.float32)
+    p_d = rng.dirichlet(np.ones(V), size=L).astype(np.float32)
+    logits = np.ascontiguousarray(np.tile(z, (N, 1)))
+    dp = np.ascontiguousarray(np.broadcast_to(p_d, (N, L, V)))
+    tok = np.stack([np.array([rng.choice(V, p=p_d[t] / p_d[t].sum()) for t in range(L)])
+                    for _ in range(N)]).astype(np.int32)
+    u = rng.random((N, L + 1)).astype(np.float32)
+    cu = np.arange(N + 1, dtype=np.int32) * (L + 1)
+    acc, nxt, _, _ = oracle.accept(tok, dp, logits, "f32", cu, L, V, u=u)
+    p_t = softmax(z.astype(np.float64), axis=1)
+    y1 = np.where(acc >= 1, tok[:, 0], nxt)
+    sel = acc >= 1
+    y2 = np.where(acc[sel] >= 2, tok[sel, 1], nxt[sel])
+    for y, p in ((y1, p_t[0]), (y2, p_t[1])):
+        obs = np.bincount(y, minlength=V)
+        exp = p * len(y)
+        keep = exp > 5
+        chi = ((obs[keep] - exp[keep]) ** 2 / exp[keep]).sum() + \
+            ((obs[~keep].sum() - exp[~keep].sum()) ** 2 / max(exp[~keep].sum(), 1e-9))
+        dof = keep.sum()
+        assert stats.chi2.sf(chi, dof) > 1e-4, (chi, dof)
+
+
+def test_identical_distributions_accept_everything():
+    rng = np.random.default_rng(3)
+    V, L, N = 257, 5, 64
+    z = (rng.normal(size=(N * (L + 1), V)) * 4).astype(np.float32)
+    p = softmax(z.astype(np.float64), axis=1).astype(np.float32)
+    cu = np.arange(N + 1, dtype=np.int32) * (L + 1)
+    dp = np.stack([p[cu[r]: cu[r] + L] for r in range(N)])
+    tok = rng.integers(0, V, size=(N, L)).astype(np.int32)
+    u = (rng.random((N, L + 1)) * 0.999).astype(np.float32)
+    acc, _, _, _ = oracle.accept(tok, dp, z, "f32", cu, L, V, u=u)
+    assert (acc == L).all()
+
+
+def test_bonus_draw_is_numpy_inverse_cdf():
+    rng = np.random.default_rng(4)
+    V, N = 1000, 300
+    z = (rng.normal(size=(N, V)) * 4).astype(np.float32)
+    u = rng.random((N, 1)).astype(np.float32)
+    cu = np.arange(N + 1, dtype=np.int32)
+    dp = np.zeros((N, 0, V), np.float32)
+    tok = np.zeros((N, 0), np.int32)
+    _, nxt, mg, _ = oracle.accept(tok, dp, z, "f32", cu, 0, V, u=u)
+    p = softmax(z.astype(np.float64), axis=1)
+    c = np.cumsum(p, axis=1)
+    ref = np.array([np.searchsorted(c[i], u[i, 0] * c[i, -1], side="right") for i in range(N)])
+    ok = mg > 1e-9
+    assert ok.mean() > 0.99
+    assert np.array_equal(nxt[ok], ref[ok])
+
+
+def test_residual_without_mass_falls_back_to_target():
+    rng = np.random.default_rng(5)
+    V, N = 50, 200
+    z = (rng.normal(size=(2 * N, V)) * 2).astype(np.float32)
+    dp = np.ones((N, 1, V), np.float32)  # p_t <= p_d everywhere: empty residual
+    tok = np.zeros((N, 1), np.int32)
+    u = np.stack([np.full(N, 0.9999, np.float32), rng.random(N).astype(np.float32)], axis=1)
+    cu = np.arange(N + 1, dtype=np.int32) * 2
+    acc, nxt, mg, _ = oracle.accept(tok, dp, z, "f32", cu, 1, V, u=u)
+    p = softmax(z[0::2].astype(np.float64), axis=1)
+    c = np.cumsum(p, axis=1)
+    ref = np.array([np.searchsorted(c[i], u[i, 1] * c[i, -1], side="right") for i in range(N)])
+    assert (acc == 0).all()
+    ok = mg > 1e-9
+    assert np.array_equal(nxt[ok], ref[ok])
+
+
+def test_inverse_temperature_scales_logits():
+    rng = np.random.default_rng(6)
+    V, L, N = 300, 3, 40
+    z = (rng.normal(size=(N * (L + 1), V)) * 4).astype(np.float32)
+    dp = rng.dirichlet(np.ones(V), size=(N, L)).astype(np.float32)
+    tok = rng.integers(0, V, size=(N, L)).astype(np.int32)
+    u = rng.random((N, L + 1)).astype(np.float32)
+    cu = np.arange(N + 1, dtype=np.int32) * (L + 1)
+    a1, n1, _, _ = oracle.accept(tok, dp, z, "f32", cu, L, V, u=u, inv_temperature=0.5)
+    a2, n2, _, _ = oracle.accept(tok, dp, z * np.float32(0.5), "f32", cu, L, V, u=u)
+    assert np.array_equal(a1, a2) and np.array_equal(n1, n2)
+
+
+def test_greedy_matches_numpy_argmax_with_ties():
+    rng = np.random.default_rng(8)
+    V, L, N = 100, 4, 50
+    z = np.round(rng.normal(size=(N * (L + 1), V)) * 2).astype(np.float32)  # many ties
+    cu = np.arange(N + 1, dtype=np.int32) * (L + 1)
+    am = np.argmax(z, axis=1)  # lowest index among maxima
+    tok = np.zeros((N, L), np.int32)
+    expect_acc = np.zeros(N, np.int32)
+    expect_tok = np.zeros(N, np.int32)
+    for r in range(N):
+        cut = r % (L + 1)  # first mismatching position (L = none)
+        for t in range(L):
+            row = cu[r] + t
+            tok[r, t] = am[row] if t < cut else (am[row] + 1 + (r % (V - 1))) % V
+        expect_acc[r] = cut
+        expect_tok[r] = am[cu[r] + cut]
+    acc, nxt, _, _ = oracle.accept(tok, None, z, "f32", cu, L, V)
+    assert np.array_equal(acc, expect_acc)
+    assert np.array_equal(nxt, expect_tok)
+    # tie: the draft equal to the later of two maxima is rejected
+    row = np.zeros((1, V), np.float32)
+    row[0, 3] = row[0, 7] = 5.0
+    logits = np.concatenate([row, row])
+    acc, nxt, _, _ = oracle.accept(np.array([[7]], np.int32), None, logits, "f32",
+                                   np.array([0, 2], np.int32), 1, V)
+    assert acc.tolist() == [0] and nxt.tolist() == [3]
+
+
+def test_bf16_logits_widen_exactly():
+    rng = np.random.default_rng(9)
+    from paper_2607_05147_amd import synth
+    V, L, N = 200, 2, 30
+    zf = (rng.normal(size=(N * (L + 1), V)) * 4).astype(np.float32)
+    zb = synth.f32_to_bf16_bits(zf)
+    zw = synth.bf16_bits_to_f32(zb)
+    dp = rng.dirichlet(np.ones(V), size=(N, L)).astype(np.float32)
+    tok = rng.integers(0, V, size=(N, L)).astype(np.int32)
+    u = rng.random((N, L + 1)).astype(np.float32)
+    cu = np.arange(N + 1, dtype=np.int32) * (L + 1)
+    r1 = oracle.accept(tok, dp, zb, "bf16", cu, L, V, u=u)
+    r2 = oracle.accept(tok, dp, zw, "f32", cu, L, V, u=u)
+    assert all(np.array_equal(a, b) for a, b in zip(r1[:3], r2[:3]))
