@@ -1,0 +1,186 @@
+/*
+ * dspark.h -- C ABI of the MI355X (gfx950) batched verification step of
+ * confidence-scheduled speculative decoding (DSpark).
+ *
+ * Three stages, each a hand-written HIP kernel family:
+ *   1. dspark_schedule    -- the hardware-aware prefix scheduler (Algorithm 1):
+ *                            per-request verification lengths from draft
+ *                            confidences and an engine throughput table;
+ *   2. dspark_verify_attn -- ragged causal verify attention over a paged KV
+ *                            cache (all verify tokens of all requests flattened
+ *                            into one batch, as in the section on serving with
+ *                            variable-length verification);
+ *   3. dspark_accept      -- speculative acceptance (the speculative-decoding
+ *                            background section): greedy match or stochastic
+ *                            rejection sampling, emitting the accepted length
+ *                            and the corrected / bonus token per request.
+ *
+ * Conventions shared by every entry point
+ *   - All array arguments are DEVICE pointers unless marked "host".  Arrays are
+ *     dense row-major unless strides are given.  The caller allocates and owns
+ *     every buffer, including the workspace, sized with the matching
+ *     *_workspace_size() call.  The library never allocates, frees or
+ *     synchronises; it keeps no global state and is re-entrant.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream).
+ *   - Arguments are validated on the host before anything touches the GPU;
+ *     a failed check returns a non-zero dspark_status and enqueues nothing.
+ *     dspark_last_error() then describes it (thread-local).  Values that live
+ *     in device memory (lengths, tokens) cannot be checked on the host; the
+ *     kernels clamp them into range as documented per call, so no access
+ *     leaves the buffers described here.
+ *   - A workspace must not be shared by two calls that may run concurrently.
+ */
+#ifndef DSPARK_H
+#define DSPARK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DSPARK_ABI_VERSION 1
+
+typedef enum {
+    DSPARK_OK = 0,
+    DSPARK_EINVAL = 1,       /* null pointer / non-positive size / bad enum   */
+    DSPARK_ESHAPE = 2,       /* sizes inconsistent with each other            */
+    DSPARK_EDTYPE = 3,       /* unsupported element type                      */
+    DSPARK_EUNSUPPORTED = 4, /* valid but outside what the kernels implement  */
+    DSPARK_EWORKSPACE = 5,   /* workspace missing, too small or misaligned    */
+    DSPARK_EHIP = 6          /* a HIP launch failed                           */
+} dspark_status;
+
+typedef enum { DSPARK_F32 = 0, DSPARK_BF16 = 1 } dspark_dtype;
+
+/* A hipStream_t, passed opaquely. */
+typedef void* dspark_stream;
+
+/* Version of this ABI (DSPARK_ABI_VERSION of the built library). */
+int dspark_abi_version(void);
+
+/* Message for the last failed call on this thread ("" if none). */
+const char* dspark_last_error(void);
+
+/* ------------------------------------------------------------------------
+ * Stage 1: hardware-aware prefix scheduler (Algorithm 1 of the section on
+ * confidence-scheduled verification; the "scheduler in practice" section for
+ * mode 1).
+ *
+ *   conf     [R, K] fp32   conditional confidence c_{r,j} of draft position
+ *                          j+1 (confidence-head section).  The survival
+ *                          probability a_{r,j} is the running product of
+ *                          c_{r,1..j} in fp64, multiplied in increasing j.
+ *                          A value that is not > 0 (0, negative, NaN) ends
+ *                          request r's candidates; a value above 1 reads as 1.
+ *   sps      [sps_len] fp64 engine throughput in steps/s at B verify tokens,
+ *                          B = sum_r (1 + len_r); sps_len must be
+ *                          > R*(K+1).  Entries below R are not read.
+ *   mode     0 = the causal greedy with early stop (stop at the first
+ *                admission that does not strictly raise Theta = tau * SPS(B));
+ *            1 = no early stop: the best prefix of the same greedy path.
+ *   len      [R] int32 out  selected verification length l*_r in 0..K.
+ *   cu_q     [R+1] int32 out (nullable) exclusive prefix sum of 1 + len_r:
+ *                          request r's verify tokens are rows
+ *                          cu_q[r] .. cu_q[r+1]-1 of the flattened batch.
+ *   tok_req  [R*(K+1)] int32 out (nullable) request id of every flattened
+ *                          verify token; slots >= cu_q[R] are set to -1.
+ *   The candidates (r, j) with a_{r,j} > 0 are admitted in descending a,
+ *   ties by r then j.  Limits: 1 <= R, 0 <= K <= 64, R*K <= 8192.
+ * ---------------------------------------------------------------------- */
+size_t dspark_schedule_workspace_size(int R, int K);
+
+dspark_status dspark_schedule(const float* conf, int R, int K, const double* sps,
+                              int64_t sps_len, int mode, int32_t* len, int32_t* cu_q,
+                              int32_t* tok_req, void* ws, size_t ws_bytes,
+                              dspark_stream stream);
+
+/* ------------------------------------------------------------------------
+ * Stage 2: ragged causal verify attention over a paged KV cache (the target
+ * model's verification forward pass over the flattened verify tokens).
+ *
+ *   q         [total_q, Hq, Dqk]  queries, total_q = cu_q[R].
+ *   k_cache   paged keys:   element (page, head, slot, d) at
+ *             page*k_strides[0] + head*k_strides[1] + slot*k_strides[2] + d.
+ *   v_cache   paged values, likewise with v_strides; it may alias k_cache
+ *             (latent attention: values are the first Dv <= Dqk dims).
+ *   k_strides, v_strides  host int64[3], in elements.
+ *   block_table [R, max_pages] int32: physical page of request r's logical
+ *             page i (token j sits in page j / page_size, slot j % page_size).
+ *   kv_len    [R] int32: context length of request r, INCLUDING its q_len_r
+ *             verify tokens, which are its last q_len_r keys.  Query t of
+ *             request r (0-based) attends keys 0 .. kv_len_r - q_len_r + t.
+ *   cu_q      [R+1] int32: as produced by dspark_schedule.
+ *   max_q     host bound on every q_len_r = cu_q[r+1] - cu_q[r] (K+1 after
+ *             scheduling).  Rows with q_len_r > max_q or kv_len_r outside
+ *             [q_len_r, max_pages*page_size] are skipped (left unwritten).
+ *   Head h reads KV head h / (Hq / Hkv).
+ *   out       [total_q, Hq, Dv] softmax(scale * q k^T) v in dtype `dt`
+ *             (fp32 accumulation, rounded to nearest-even on store).
+ *   lse       [total_q, Hq] fp32 (nullable): natural-log sum of exp of the
+ *             scaled scores.
+ *   dt        element type of q, k_cache, v_cache and out.
+ *   Supported: Hq % Hkv == 0; Dqk, Dv multiples of 8 up to 576;
+ *   page_size multiple of 16.  bf16 with Dqk == Dv == 128 and page_size a
+ *   multiple of 32 runs on MFMA tiles; other shapes run on vector ALUs.
+ * ---------------------------------------------------------------------- */
+size_t dspark_verify_attn_workspace_size(int R, int max_q, int Hq, int Hkv, int Dqk, int Dv,
+                                         int max_pages, int page_size, dspark_dtype dt);
+
+dspark_status dspark_verify_attn(const void* q, const void* k_cache, const void* v_cache,
+                                 const int64_t* k_strides, const int64_t* v_strides,
+                                 const int32_t* block_table, int max_pages,
+                                 const int32_t* kv_len, const int32_t* cu_q, int R, int max_q,
+                                 int Hq, int Hkv, int Dqk, int Dv, int page_size, float scale,
+                                 dspark_dtype dt, void* out, float* lse, void* ws,
+                                 size_t ws_bytes, dspark_stream stream);
+
+/* ------------------------------------------------------------------------
+ * Stage 3: speculative acceptance (the background section on speculative
+ * decoding: left-to-right test, first rejection discards the suffix, one
+ * corrected or bonus token per round).
+ *
+ *   draft_tok [R, K] int32: draft token for verify slot t+1 (the paper's
+ *             x_{t+1}); values outside [0, V) are read as rejected.
+ *   draft_p   [R, K, V] fp32 (nullable): draft distribution p_d for slot t+1,
+ *             used as given (not renormalised).
+ *   logits    target logits, row cu_q[r] + t (row stride `ld` elements) is the
+ *             target distribution for the token after verify slot t:
+ *             rows t < len_r test draft_tok[r, t]; row len_r gives the bonus.
+ *   logit_dt  element type of logits.
+ *   u         [R, K+1] fp32 uniforms in [0,1) (nullable): u[r,t] (t < K) tests
+ *             draft t+1, u[r,K] draws the emitted token.
+ *   cu_q      [R+1] int32 as produced by dspark_schedule; len_r = q_len_r - 1
+ *             must lie in 0..K (requests outside it get accepted_len = -1,
+ *             next_tok = -1).
+ *   draft_p == NULL and u == NULL: greedy -- draft t+1 is accepted iff it is
+ *             the argmax of the raw logits of row t (lowest index on ties);
+ *             the emitted token is the argmax of row accepted_len.
+ *   otherwise stochastic -- p_t = softmax(inv_temperature * z); draft x is
+ *             accepted iff u[r,t] < p_t(x) / p_d(x) (p_d(x) = 0 accepts); at
+ *             the first rejection t* the emitted token is drawn from
+ *             max(0, p_t - p_d) of row t* (p_t if that has no mass); with no
+ *             rejection it is drawn from p_t of row len_r.  A draw is the
+ *             smallest token v whose running mass (ascending v) exceeds
+ *             u[r,K] times the total mass.
+ *   accepted_len [R] int32 out, next_tok [R] int32 out.
+ *   accept_rate  [total_q] fp32 out (nullable, stochastic only): for rows
+ *             t < len_r the analytic acceptance probability
+ *             sum_v min(p_t(v), p_d(v)) (one minus the total variation
+ *             distance, the confidence head's training label); -1 for bonus
+ *             rows.
+ *   Limits: 1 <= V, ld >= V, 0 <= K <= 64, inv_temperature > 0.
+ * ---------------------------------------------------------------------- */
+size_t dspark_accept_workspace_size(int R, int K, int V);
+
+dspark_status dspark_accept(const int32_t* draft_tok, const float* draft_p, const void* logits,
+                            dspark_dtype logit_dt, int64_t ld, const float* u,
+                            const int32_t* cu_q, int R, int K, int V, float inv_temperature,
+                            int32_t* accepted_len, int32_t* next_tok, float* accept_rate,
+                            void* ws, size_t ws_bytes, dspark_stream stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DSPARK_H */

@@ -1,0 +1,60 @@
+// Host-side launchers of the gfx950 kernels (defined in the .hip files).
+// Arguments are already validated by the C ABI layer.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace dspark {
+
+// ---- scheduler --------------------------------------------------------------
+size_t schedule_lds_bytes(int R, int K);
+hipError_t launch_schedule(const float* conf, int R, int K, const double* sps, int mode,
+                           int32_t* len, int32_t* cu_q, int32_t* tok_req, hipStream_t s);
+
+// ---- verify attention ---------------------------------------------------------
+struct AttnArgs {
+    const void* q;
+    const void* k;
+    const void* v;
+    int64_t ks[3];
+    int64_t vs[3];
+    const int32_t* block_table;
+    int max_pages;
+    const int32_t* kv_len;
+    const int32_t* cu_q;
+    int R, max_q, Hq, Hkv, Dqk, Dv, page;
+    float scale;
+    int bf16;  // 0 = fp32, 1 = bf16
+    void* out;
+    float* lse;
+};
+
+// The MFMA path handles bf16, Dqk == Dv == 128, page % 32 == 0.
+bool attn_mfma_supported(const AttnArgs& a);
+size_t attn_mfma_workspace(const AttnArgs& a);
+hipError_t launch_attn_mfma(const AttnArgs& a, void* ws, hipStream_t s);
+
+size_t attn_generic_workspace(const AttnArgs& a);
+hipError_t launch_attn_generic(const AttnArgs& a, void* ws, hipStream_t s);
+
+// ---- acceptance ------------------------------------------------------------------
+struct AcceptArgs {
+    const int32_t* draft_tok;
+    const float* draft_p;
+    const void* logits;
+    int logit_bf16;
+    int64_t ld;
+    const float* u;
+    const int32_t* cu_q;
+    int R, K, V;
+    float inv_temp;
+    int32_t* accepted_len;
+    int32_t* next_tok;
+    float* accept_rate;
+};
+
+size_t accept_workspace(int R, int K, int V);
+hipError_t launch_accept(const AcceptArgs& a, void* ws, hipStream_t s);
+
+}  // namespace dspark

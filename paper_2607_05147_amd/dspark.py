@@ -1,0 +1,242 @@
+"""Python binding of the C ABI in include/dspark.h (argument marshalling only).
+
+Every function takes torch tensors that live on a ROCm device, checks their
+dtype/shape/contiguity, passes raw pointers to ``libdspark.so`` and raises
+``DSparkError`` with the library's message when a call fails.  Outputs that are
+not supplied are allocated with torch (device memory plumbing); all
+computation happens in the library's HIP kernels, enqueued on the current
+torch stream unless ``stream`` is given.  There is no fallback: without the
+built library every call raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional, Sequence, Tuple
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdspark.so")
+
+DSPARK_F32 = 0
+DSPARK_BF16 = 1
+STATUS = {0: "OK", 1: "EINVAL", 2: "ESHAPE", 3: "EDTYPE", 4: "EUNSUPPORTED", 5: "EWORKSPACE",
+          6: "EHIP"}
+
+
+class DSparkError(RuntimeError):
+    def __init__(self, msg: str, status: int = -1):
+        super().__init__(msg)
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """The loaded C library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise DSparkError(f"{LIB_PATH} is missing: build it with "
+                              "`python -m paper_2607_05147_amd.build` (no fallback path exists)")
+        L = C.CDLL(LIB_PATH)
+        p, i32, i64, sz, f32 = C.c_void_p, C.c_int, C.c_int64, C.c_size_t, C.c_float
+        L.dspark_abi_version.restype = i32
+        L.dspark_abi_version.argtypes = []
+        L.dspark_last_error.restype = C.c_char_p
+        L.dspark_last_error.argtypes = []
+        L.dspark_schedule_workspace_size.restype = sz
+        L.dspark_schedule_workspace_size.argtypes = [i32, i32]
+        L.dspark_schedule.restype = i32
+        L.dspark_schedule.argtypes = [p, i32, i32, p, i64, i32, p, p, p, p, sz, p]
+        L.dspark_verify_attn_workspace_size.restype = sz
+        L.dspark_verify_attn_workspace_size.argtypes = [i32] * 8 + [i32]
+        L.dspark_verify_attn.restype = i32
+        L.dspark_verify_attn.argtypes = [p, p, p, p, p, p, i32, p, p, i32, i32, i32, i32, i32, i32,
+                                         i32, f32, i32, p, p, p, sz, p]
+        L.dspark_accept_workspace_size.restype = sz
+        L.dspark_accept_workspace_size.argtypes = [i32, i32, i32]
+        L.dspark_accept.restype = i32
+        L.dspark_accept.argtypes = [p, p, p, i32, i64, p, p, i32, i32, i32, f32, p, p, p, p, sz, p]
+        _lib = L
+    return _lib
+
+
+def dspark_abi_version() -> int:
+    return int(lib().dspark_abi_version())
+
+
+def dspark_last_error() -> str:
+    return lib().dspark_last_error().decode()
+
+
+def _raise(st: int, what: str) -> None:
+    if st != 0:
+        raise DSparkError(f"{what}: {STATUS.get(st, st)}: {dspark_last_error()}", st)
+
+
+def _dev(t: Optional[torch.Tensor], name: str, dtype=None, shape=None, optional=False):
+    if t is None:
+        if optional:
+            return None
+        raise DSparkError(f"{name} is required")
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise DSparkError(f"{name} must be a torch tensor on a ROCm device")
+    if dtype is not None and t.dtype != dtype:
+        raise DSparkError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise DSparkError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise DSparkError(f"{name} must be contiguous")
+    return t
+
+
+def _p(t: Optional[torch.Tensor]):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> C.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return C.c_void_p(stream.cuda_stream)
+
+
+def _workspace(nbytes: int, device, ws: Optional[torch.Tensor]) -> Tuple[Optional[torch.Tensor], int]:
+    if nbytes == 0:
+        return ws, 0 if ws is None else ws.numel() * ws.element_size()
+    if ws is None:
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    return ws, ws.numel() * ws.element_size()
+
+
+_DT = {torch.float32: DSPARK_F32, torch.bfloat16: DSPARK_BF16}
+
+
+# ------------------------------------------------------------------ stage 1
+
+def dspark_schedule_workspace_size(R: int, K: int) -> int:
+    return int(lib().dspark_schedule_workspace_size(R, K))
+
+
+def dspark_schedule(conf: torch.Tensor, sps: torch.Tensor, mode: int = 0,
+                    len_out: Optional[torch.Tensor] = None, cu_q: Optional[torch.Tensor] = None,
+                    tok_req: Optional[torch.Tensor] = None, want_tok_req: bool = False,
+                    stream=None):
+    """conf fp32 [R, K], sps fp64 [> R*(K+1)] -> (len int32 [R], cu_q int32 [R+1], tok_req|None)."""
+    _dev(conf, "conf", torch.float32)
+    if conf.dim() != 2:
+        raise DSparkError("conf must be [R, K]")
+    R, K = conf.shape
+    _dev(sps, "sps", torch.float64)
+    dev = conf.device
+    if len_out is None:
+        len_out = torch.empty(R, dtype=torch.int32, device=dev)
+    if cu_q is None:
+        cu_q = torch.empty(R + 1, dtype=torch.int32, device=dev)
+    if tok_req is None and want_tok_req:
+        tok_req = torch.empty(R * (K + 1), dtype=torch.int32, device=dev)
+    _dev(len_out, "len", torch.int32, (R,))
+    _dev(cu_q, "cu_q", torch.int32, (R + 1,))
+    _dev(tok_req, "tok_req", torch.int32, (R * (K + 1),), optional=True)
+    st = lib().dspark_schedule(_p(conf), R, K, _p(sps), sps.numel(), mode, _p(len_out), _p(cu_q),
+                               _p(tok_req), None, 0, _stream(stream))
+    _raise(st, "dspark_schedule")
+    return len_out, cu_q, tok_req
+
+
+# ------------------------------------------------------------------ stage 2
+
+def dspark_verify_attn_workspace_size(R: int, max_q: int, Hq: int, Hkv: int, Dqk: int, Dv: int,
+                                      max_pages: int, page_size: int, dtype: torch.dtype) -> int:
+    return int(lib().dspark_verify_attn_workspace_size(R, max_q, Hq, Hkv, Dqk, Dv, max_pages,
+                                                       page_size, _DT[dtype]))
+
+
+def dspark_verify_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+                       k_strides: Sequence[int], v_strides: Sequence[int],
+                       block_table: torch.Tensor, kv_len: torch.Tensor, cu_q: torch.Tensor,
+                       max_q: int, Hkv: int, Dv: int, page_size: int, scale: float,
+                       out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                       want_lse: bool = False, ws: Optional[torch.Tensor] = None, stream=None):
+    """q [total_q(or more rows), Hq, Dqk]; caches flat or shaped, addressed by element strides.
+    Returns (out [rows of q, Hq, Dv], lse|None)."""
+    if q.dtype not in _DT:
+        raise DSparkError("q must be float32 or bfloat16")
+    _dev(q, "q")
+    if q.dim() != 3:
+        raise DSparkError("q must be [tokens, Hq, Dqk]")
+    rows, Hq, Dqk = q.shape
+    _dev(k_cache, "k_cache", q.dtype)
+    _dev(v_cache, "v_cache", q.dtype)
+    _dev(block_table, "block_table", torch.int32)
+    if block_table.dim() != 2:
+        raise DSparkError("block_table must be [R, max_pages]")
+    R, max_pages = block_table.shape
+    _dev(kv_len, "kv_len", torch.int32, (R,))
+    _dev(cu_q, "cu_q", torch.int32, (R + 1,))
+    if out is None:
+        out = torch.empty((rows, Hq, Dv), dtype=q.dtype, device=q.device)
+    _dev(out, "out", q.dtype, (rows, Hq, Dv))
+    if lse is None and want_lse:
+        lse = torch.empty((rows, Hq), dtype=torch.float32, device=q.device)
+    _dev(lse, "lse", torch.float32, (rows, Hq), optional=True)
+    need = dspark_verify_attn_workspace_size(R, max_q, Hq, Hkv, Dqk, Dv, max_pages, page_size,
+                                             q.dtype)
+    ws, ws_bytes = _workspace(need, q.device, ws)
+    ks = (C.c_int64 * 3)(*[int(x) for x in k_strides])
+    vs = (C.c_int64 * 3)(*[int(x) for x in v_strides])
+    st = lib().dspark_verify_attn(_p(q), _p(k_cache), _p(v_cache), ks, vs, _p(block_table),
+                                  max_pages, _p(kv_len), _p(cu_q), R, max_q, Hq, Hkv, Dqk, Dv,
+                                  page_size, float(scale), _DT[q.dtype], _p(out), _p(lse), _p(ws),
+                                  ws_bytes, _stream(stream))
+    _raise(st, "dspark_verify_attn")
+    return out, lse
+
+
+# ------------------------------------------------------------------ stage 3
+
+def dspark_accept_workspace_size(R: int, K: int, V: int) -> int:
+    return int(lib().dspark_accept_workspace_size(R, K, V))
+
+
+def dspark_accept(draft_tok: torch.Tensor, logits: torch.Tensor, cu_q: torch.Tensor,
+                  draft_p: Optional[torch.Tensor] = None, u: Optional[torch.Tensor] = None,
+                  inv_temperature: float = 1.0, accepted_len: Optional[torch.Tensor] = None,
+                  next_tok: Optional[torch.Tensor] = None, accept_rate: Optional[torch.Tensor] = None,
+                  want_rate: bool = False, ws: Optional[torch.Tensor] = None, stream=None):
+    """draft_tok int32 [R, K]; logits [rows, V] (fp32/bf16, row stride = stride(0));
+    draft_p fp32 [R, K, V] and u fp32 [R, K+1] for stochastic acceptance (both None: greedy).
+    Returns (accepted_len int32 [R], next_tok int32 [R], accept_rate|None)."""
+    _dev(draft_tok, "draft_tok", torch.int32)
+    if draft_tok.dim() != 2:
+        raise DSparkError("draft_tok must be [R, K]")
+    R, K = draft_tok.shape
+    if logits.dtype not in _DT or logits.dim() != 2 or logits.device.type != "cuda":
+        raise DSparkError("logits must be a 2-D float32/bfloat16 ROCm tensor")
+    if logits.stride(1) != 1:
+        raise DSparkError("logits rows must be contiguous")
+    V = logits.shape[1]
+    ld = logits.stride(0)
+    _dev(cu_q, "cu_q", torch.int32, (R + 1,))
+    _dev(draft_p, "draft_p", torch.float32, (R, K, V), optional=True)
+    _dev(u, "u", torch.float32, (R, K + 1), optional=True)
+    dev = draft_tok.device
+    if accepted_len is None:
+        accepted_len = torch.empty(R, dtype=torch.int32, device=dev)
+    if next_tok is None:
+        next_tok = torch.empty(R, dtype=torch.int32, device=dev)
+    if accept_rate is None and want_rate:
+        accept_rate = torch.empty(R * (K + 1), dtype=torch.float32, device=dev)
+    _dev(accepted_len, "accepted_len", torch.int32, (R,))
+    _dev(next_tok, "next_tok", torch.int32, (R,))
+    _dev(accept_rate, "accept_rate", torch.float32, optional=True)
+    need = dspark_accept_workspace_size(R, K, V)
+    ws, ws_bytes = _workspace(need, dev, ws)
+    st = lib().dspark_accept(_p(draft_tok), _p(draft_p), C.c_void_p(logits.data_ptr()),
+                             _DT[logits.dtype], ld, _p(u), _p(cu_q), R, K, V,
+                             float(inv_temperature), _p(accepted_len), _p(next_tok),
+                             _p(accept_rate), _p(ws), ws_bytes, _stream(stream))
+    _raise(st, "dspark_accept")
+    return accepted_len, next_tok, accept_rate

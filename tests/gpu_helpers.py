@@ -1,0 +1,76 @@
+"""Helpers for GPU tests: move generator/oracle cases to the device and run the
+three stages through the Python binding of the C ABI."""
+import sys
+
+import numpy as np
+import torch
+
+from paper_2607_05147_amd import dspark, synth
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def dev():
+    return torch.device("cuda:0")
+
+
+def to_dev(a: np.ndarray, bf16: bool = False) -> torch.Tensor:
+    a = np.ascontiguousarray(a)
+    if bf16 or a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).to(dev()).view(torch.bfloat16)
+    return torch.from_numpy(a).to(dev())
+
+
+def to_f64(t: torch.Tensor) -> np.ndarray:
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def gpu_schedule(conf: np.ndarray, sps: np.ndarray, mode: int = 0):
+    ln, cu, tok = dspark.dspark_schedule(to_dev(conf), to_dev(sps), mode, want_tok_req=True)
+    torch.cuda.synchronize()
+    return ln.cpu().numpy(), cu.cpu().numpy(), tok.cpu().numpy()
+
+
+class DevKV:
+    """Device copy of a synth.PagedKV."""
+
+    def __init__(self, kv: synth.PagedKV, bf16: bool):
+        self.k = to_dev(kv.k.reshape(-1), bf16)
+        self.v = self.k if kv.v is kv.k else to_dev(kv.v.reshape(-1), bf16)
+        self.bt = to_dev(kv.block_table)
+        self.kv_len = to_dev(kv.kv_len)
+        self.ks = kv.k_strides
+        self.vs = kv.v_strides
+
+
+def gpu_attention(w: synth.Workload, dkv: DevKV, q: np.ndarray, cu_q: np.ndarray, want_lse=True):
+    bf16 = w.dtype == "bf16"
+    qd = to_dev(q, bf16)
+    out, lse = dspark.dspark_verify_attn(qd, dkv.k, dkv.v, dkv.ks, dkv.vs, dkv.bt, dkv.kv_len,
+                                         to_dev(cu_q), w.max_q, w.Hkv, w.Dv, w.page, w.scale,
+                                         want_lse=want_lse)
+    torch.cuda.synchronize()
+    return out, lse
+
+
+def row_rel_err(out: np.ndarray, ref: np.ndarray) -> np.ndarray:
+    """Per (token, head) row: ||o - ref||_2 / ||ref||_2."""
+    num = np.linalg.norm((out - ref).reshape(-1, ref.shape[-1]), axis=1)
+    den = np.linalg.norm(ref.reshape(-1, ref.shape[-1]), axis=1)
+    return num / np.maximum(den, 1e-300)
+
+
+def gpu_accept(w: synth.Workload, drafts: synth.Drafts, logits: np.ndarray, cu_q: np.ndarray,
+               want_rate: bool = False):
+    bf16 = w.logit_dtype == "bf16"
+    lg = to_dev(logits, bf16)
+    dp = None if drafts.draft_p is None else to_dev(drafts.draft_p)
+    u = None if drafts.u is None else to_dev(drafts.u)
+    acc, nxt, rate = dspark.dspark_accept(to_dev(drafts.draft_tok), lg, to_dev(cu_q), draft_p=dp,
+                                          u=u, want_rate=want_rate)
+    torch.cuda.synchronize()
+    return (acc.cpu().numpy(), nxt.cpu().numpy(),
+            None if rate is None else rate.cpu().numpy())

@@ -1,0 +1,146 @@
+"""C ABI checks that need no GPU.
+
+The library must load on a host without a GPU, export every function that
+include/dspark.h declares, and reject bad arguments with the documented
+status before it touches HIP (every call here fails validation, so nothing is
+launched).
+"""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2607_05147_amd import dspark
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dspark.h")
+
+EINVAL, ESHAPE, EDTYPE, EUNSUPPORTED, EWORKSPACE = 1, 2, 3, 4, 5
+FAKE = C.c_void_p(1 << 20)  # aligned, never dereferenced: validation fails first
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(dspark.LIB_PATH):
+        from paper_2607_05147_amd import build
+        build.build()
+    return dspark.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dspark_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_three_stages():
+    names = declared_functions()
+    for n in ("dspark_schedule", "dspark_verify_attn", "dspark_accept", "dspark_abi_version",
+              "dspark_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(L):
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+def test_abi_version_matches_header(L):
+    m = re.search(r"#define DSPARK_ABI_VERSION (\d+)", open(HEADER).read())
+    assert L.dspark_abi_version() == int(m.group(1))
+
+
+def _sched(L, conf=FAKE, R=4, K=8, sps=FAKE, sps_len=100, mode=0, ln=FAKE):
+    return L.dspark_schedule(conf, R, K, sps, sps_len, mode, ln, None, None, None, 0, None)
+
+
+def test_schedule_validation(L):
+    assert _sched(L, conf=None) == EINVAL
+    assert _sched(L, sps=None) == EINVAL
+    assert _sched(L, ln=None) == EINVAL
+    assert _sched(L, R=0) == EINVAL
+    assert _sched(L, K=65) == EINVAL
+    assert _sched(L, K=-1) == EINVAL
+    assert _sched(L, mode=2) == EINVAL
+    assert _sched(L, sps_len=36) == ESHAPE  # must exceed R*(K+1) = 36
+    assert _sched(L, R=8192, K=2, sps_len=10**6) == EUNSUPPORTED
+    assert _sched(L, conf=C.c_void_p((1 << 20) + 2)) == EINVAL  # misaligned
+
+
+def test_last_error_describes_failure(L):
+    assert _sched(L, sps_len=36) == ESHAPE
+    assert "sps_len" in L.dspark_last_error().decode()
+
+
+def _attn(L, **kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, ks=(C.c_int64 * 3)(8 * 64 * 128, 64 * 128, 128),
+             vs=(C.c_int64 * 3)(8 * 64 * 128, 64 * 128, 128), bt=FAKE, max_pages=4, kv=FAKE,
+             cu=FAKE, R=4, max_q=9, Hq=32, Hkv=8, Dqk=128, Dv=128, page=64, scale=0.1, dt=1,
+             out=FAKE, lse=None, ws=FAKE, ws_bytes=0)
+    a.update(kw)
+    return L.dspark_verify_attn(a["q"], a["k"], a["v"], a["ks"], a["vs"], a["bt"], a["max_pages"],
+                                a["kv"], a["cu"], a["R"], a["max_q"], a["Hq"], a["Hkv"], a["Dqk"],
+                                a["Dv"], a["page"], a["scale"], a["dt"], a["out"], a["lse"],
+                                a["ws"], a["ws_bytes"], None)
+
+
+def test_verify_attn_validation(L):
+    assert _attn(L, q=None) == EINVAL
+    assert _attn(L, bt=None) == EINVAL
+    assert _attn(L, ks=None) == EINVAL
+    assert _attn(L, dt=7) == EDTYPE
+    assert _attn(L, Hq=30) == ESHAPE  # not a multiple of Hkv
+    assert _attn(L, Dqk=100) == EUNSUPPORTED
+    assert _attn(L, Dv=1024) == EUNSUPPORTED
+    assert _attn(L, page=24) == EUNSUPPORTED
+    assert _attn(L, max_q=0) == EINVAL
+    assert _attn(L, R=0) == EINVAL
+    assert _attn(L, ks=(C.c_int64 * 3)(1, 1, 64)) == ESHAPE  # token stride < Dqk
+    assert _attn(L, scale=float("nan")) == EINVAL
+    assert _attn(L, q=C.c_void_p((1 << 20) + 1)) == EINVAL
+    assert _attn(L, ws_bytes=16) == EWORKSPACE  # far too small
+
+
+def test_verify_attn_workspace_sizes(L):
+    f = L.dspark_verify_attn_workspace_size
+    mfma = f(128, 17, 64, 8, 128, 128, 256, 64, 1)
+    assert mfma > 0
+    assert f(4, 9, 8, 2, 64, 64, 8, 16, 0) > 0  # fp32 vector path
+    assert f(0, 9, 8, 2, 64, 64, 8, 16, 0) == 0  # invalid shape -> 0
+
+
+def _acc(L, **kw):
+    a = dict(tok=FAKE, dp=FAKE, logits=FAKE, dt=1, ld=1024, u=FAKE, cu=FAKE, R=4, K=8, V=1024,
+             it=1.0, acc=FAKE, nxt=FAKE, rate=None, ws=FAKE, ws_bytes=0)
+    a.update(kw)
+    return L.dspark_accept(a["tok"], a["dp"], a["logits"], a["dt"], a["ld"], a["u"], a["cu"],
+                           a["R"], a["K"], a["V"], a["it"], a["acc"], a["nxt"], a["rate"], a["ws"],
+                           a["ws_bytes"], None)
+
+
+def test_accept_validation(L):
+    assert _acc(L, dt=5) == EDTYPE
+    assert _acc(L, ld=1000) == ESHAPE
+    assert _acc(L, it=0.0) == EINVAL
+    assert _acc(L, it=float("inf")) == EINVAL
+    assert _acc(L, dp=None) == EINVAL  # u without draft_p
+    assert _acc(L, u=None) == EINVAL
+    assert _acc(L, dp=None, u=None, rate=FAKE) == EINVAL  # rate needs stochastic mode
+    assert _acc(L, logits=None) == EINVAL
+    assert _acc(L, K=65) == EINVAL
+    assert _acc(L, V=0) == EINVAL
+    assert _acc(L, R=0) == EINVAL
+    assert _acc(L, ws_bytes=8) == EWORKSPACE
+    assert _acc(L, logits=C.c_void_p((1 << 20) + 1)) == EINVAL
+
+
+def test_accept_workspace_size(L):
+    assert L.dspark_accept_workspace_size(128, 16, 129280) > 0
+    assert L.dspark_accept_workspace_size(0, 16, 129280) == 0
+
+
+def test_binding_rejects_host_tensors():
+    import torch
+    with pytest.raises(dspark.DSparkError):
+        dspark.dspark_schedule(torch.zeros(2, 3), torch.ones(20, dtype=torch.float64))

@@ -1,0 +1,136 @@
+"""GPU parity of speculative acceptance against the oracle: accepted lengths and
+emitted tokens bit-exact (greedy, and stochastic on guard-banded inputs), the
+analytic acceptance rate within fp32 rounding, the sampler's output law by a
+chi-square test, and edge cases."""
+import numpy as np
+import pytest
+from scipy import stats
+from scipy.special import softmax
+
+import oracle
+from oracle import guard
+from paper_2607_05147_amd import synth
+
+from gpu_helpers import gpu_accept, log, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _compare(case, label):
+    acc, nxt, _ = gpu_accept(case.w, case.drafts, case.logits, case.cu_q)
+    ok = np.ones(case.w.R, bool)
+    ok[case.unguarded] = False
+    log(f"[accept] {label}: R={case.w.R} total_q={case.total_q} unguarded={len(case.unguarded)} "
+        f"mean accepted={case.accepted_len.mean():.2f}")
+    assert ok.mean() > 0.9
+    bad = np.nonzero(ok & ((acc != case.accepted_len) | (nxt != case.next_tok)))[0]
+    assert bad.size == 0, (label, bad[:10], acc[bad[:10]], case.accepted_len[bad[:10]],
+                           nxt[bad[:10]], case.next_tok[bad[:10]])
+
+
+@pytest.mark.parametrize("name", synth.WORKLOAD_ORDER)
+def test_workloads_full_size(name):
+    w = synth.WORKLOADS[name]
+    case = guard.build_case(w, 1, with_kv=False)
+    _compare(case, name)
+
+
+@pytest.mark.parametrize("name", ["tiny", "mid", "highconc"])
+def test_reduced_sizes(name):
+    # vocabularies that are not a multiple of the 8192-token chunk, several chunks
+    w = synth.scaled(synth.WORKLOADS[name], R=24, V=20000 + 37)
+    for seed in (2, 3):
+        case = guard.build_case(w, seed, with_kv=False)
+        _compare(case, f"{name}/V{w.V}/seed{seed}")
+
+
+def test_accept_rate_matches_oracle():
+    w = synth.scaled(synth.WORKLOADS["mid"], R=12, V=17000)
+    case = guard.build_case(w, 4, with_kv=False)
+    _, _, _, rate_o = oracle.accept(case.drafts.draft_tok, case.drafts.draft_p, case.logits,
+                                    w.logit_dtype, case.cu_q, w.K, w.V, u=case.drafts.u,
+                                    want_rate=True)
+    acc, nxt, rate = gpu_accept(w, case.drafts, case.logits, case.cu_q, want_rate=True)
+    total = case.total_q
+    tested = rate_o[:total] >= 0
+    assert np.array_equal(rate[:total] < 0, ~tested)
+    np.testing.assert_allclose(rate[:total][tested], rate_o[:total][tested], atol=2e-5)
+
+
+def test_identical_distributions_accept_all():
+    rng = np.random.default_rng(3)
+    R, K, V = 16, 6, 3000
+    z = (rng.normal(size=(R * (K + 1), V)) * 4).astype(np.float32)
+    cu = np.arange(R + 1, dtype=np.int32) * (K + 1)
+    p = softmax(z.astype(np.float64), axis=1).astype(np.float32)
+    dp = np.stack([p[cu[r]: cu[r] + K] for r in range(R)])
+    tok = rng.integers(0, V, size=(R, K)).astype(np.int32)
+    u = (rng.random((R, K + 1)) * 0.999).astype(np.float32)
+    w = synth.scaled(synth.WORKLOADS["mid"], R=R, K=K, V=V)
+    acc, nxt, _ = gpu_accept(w, synth.Drafts(tok, dp, u), z, cu)
+    assert (acc == K).all()
+
+
+def test_greedy_ties_and_rejections():
+    rng = np.random.default_rng(8)
+    R, K, V = 40, 4, 9000
+    z = np.round(rng.normal(size=(R * (K + 1), V)) * 2).astype(np.float32)  # many ties
+    cu = np.arange(R + 1, dtype=np.int32) * (K + 1)
+    am = np.argmax(z, axis=1)
+    tok = np.zeros((R, K), np.int32)
+    for r in range(R):
+        cut = r % (K + 1)
+        for t in range(K):
+            tok[r, t] = am[cu[r] + t] if t < cut else (am[cu[r] + t] + 1) % V
+    w = synth.scaled(synth.WORKLOADS["tiny"], R=R, K=K, V=V)
+    acc, nxt, _ = gpu_accept(w, synth.Drafts(tok, None, None), z, cu)
+    acc_o, nxt_o, _, _ = oracle.accept(tok, None, z, "f32", cu, K, V)
+    assert np.array_equal(acc, acc_o) and np.array_equal(nxt, nxt_o)
+
+
+def test_zero_length_requests_and_bonus_only():
+    """len = 0 for every request: only the bonus draw happens."""
+    w = synth.scaled(synth.WORKLOADS["mid"], R=10, V=9000)
+    case = guard.build_case(w, 5, with_kv=False)
+    cu = np.arange(w.R + 1, dtype=np.int32)
+    keys = [(r, 0) for r in range(w.R)]
+    logits = synth.logit_rows(w, 5, keys)
+    acc, nxt, _ = gpu_accept(w, case.drafts, logits, cu)
+    acc_o, nxt_o, mg, _ = oracle.accept(case.drafts.draft_tok, case.drafts.draft_p, logits,
+                                        w.logit_dtype, cu, w.K, w.V, u=case.drafts.u)
+    ok = mg >= guard.ACCEPT_GUARD
+    assert (acc == 0).all()
+    assert np.array_equal(nxt[ok], nxt_o[ok])
+
+
+def test_sampler_law_chi_square():
+    """Emitted first token ~ target law (losslessness) on the GPU sampler."""
+    rng = np.random.default_rng(11)
+    V, L, N = 16, 2, 8192
+    zrow = (rng.normal(size=(L + 1, V)) * 2).astype(np.float32)
+    p_d = rng.dirichlet(np.ones(V), size=L).astype(np.float32)
+    logits = np.tile(zrow, (N, 1))
+    dp = np.ascontiguousarray(np.broadcast_to(p_d, (N, L, V)))
+    tok = np.stack([[rng.choice(V, p=p_d[t] / p_d[t].sum()) for t in range(L)]
+                    for _ in range(N)]).astype(np.int32)
+    cu = np.arange(N + 1, dtype=np.int32) * (L + 1)
+    p_t = softmax(zrow.astype(np.float64), axis=1)
+    y = []
+    for rep in range(6):
+        u = rng.random((N, L + 1)).astype(np.float32)
+        w = synth.scaled(synth.WORKLOADS["mid"], R=N, K=L, V=V)
+        acc, nxt, _ = gpu_accept(w, synth.Drafts(tok, dp, u), logits, cu)
+        y.append(np.where(acc >= 1, tok[:, 0], nxt))
+    y = np.concatenate(y)
+    obs = np.bincount(y, minlength=V)
+    exp = p_t[0] * len(y)
+    chi = ((obs - exp) ** 2 / exp).sum()
+    assert stats.chi2.sf(chi, V - 1) > 1e-4, chi
+
+
+def test_repeatable():
+    w = synth.WORKLOADS["serving"]
+    case = guard.build_case(synth.scaled(w, R=32), 6, with_kv=False)
+    a1 = gpu_accept(case.w, case.drafts, case.logits, case.cu_q)
+    a2 = gpu_accept(case.w, case.drafts, case.logits, case.cu_q)
+    assert all(np.array_equal(x, y) for x, y in zip(a1[:2], a2[:2]))

@@ -1,0 +1,84 @@
+"""GPU parity of the scheduler kernel against the oracle (bit-exact lengths,
+cu_q and token -> request marker) on every workload and on edge cases."""
+import numpy as np
+import pytest
+
+import oracle
+from oracle import guard
+from paper_2607_05147_amd import synth
+
+from gpu_helpers import gpu_schedule, log
+
+pytestmark = pytest.mark.gpu
+
+
+def _check(conf, sps, mode, label):
+    ln_o, _, _, mm = oracle.schedule(conf, sps, mode)
+    R, K = conf.shape
+    log(f"[schedule] {label} R={R} K={K} mode={mode} margin={mm:.3g}")
+    ln_g, cu_g, tok_g = gpu_schedule(conf, sps, mode)
+    assert np.array_equal(ln_g, ln_o), (label, np.nonzero(ln_g != ln_o))
+    cu_o = oracle.cu_from_len(ln_o)
+    assert np.array_equal(cu_g, cu_o)
+    tok_o = np.full(R * (K + 1), -1, np.int32)
+    for r in range(R):
+        tok_o[cu_o[r]:cu_o[r + 1]] = r
+    assert np.array_equal(tok_g, tok_o)
+    return mm
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+@pytest.mark.parametrize("name", synth.WORKLOAD_ORDER)
+def test_workloads(name, mode):
+    w = synth.WORKLOADS[name]
+    for seed in range(3):
+        case = guard.schedule_case(w, seed, mode=mode)
+        assert case.sched_guarded
+        _check(case.conf, case.sps, mode, f"{name}/seed{seed}")
+
+
+def test_appendix_counterexample(appendix):
+    sps = np.array([0.0, appendix["sps_1"], appendix["sps_2"], appendix["sps_3"]])
+    for c2, mode, expect in ((0.9, 0, 0), (0.0, 0, 0), (0.9, 1, 2), (0.0, 1, 0)):
+        conf = np.array([[appendix["a_1"], c2]], np.float32)
+        ln, _, _ = gpu_schedule(conf, sps, mode)
+        assert ln.tolist() == [expect]
+
+
+def test_edge_cases():
+    rng = np.random.default_rng(0)
+    # K = 0: nothing to schedule
+    conf = np.zeros((5, 0), np.float32)
+    _check(conf, np.ones(6), 0, "K=0")
+    # a single request
+    conf = rng.uniform(0.3, 1, (1, 16)).astype(np.float32)
+    _check(conf, 1.0 / (1 + 0.05 * np.arange(18)), 0, "R=1")
+    # all-zero / NaN / negative / >1 confidences
+    conf = rng.uniform(0.2, 1, (6, 8)).astype(np.float32)
+    conf[0] = 0.0
+    conf[1, 3] = np.nan
+    conf[2, 0] = -0.5
+    conf[3, 2] = 1.7
+    sps = 1.0 / (1 + 0.02 * np.maximum(0, np.arange(6 * 9 + 1) - 10))
+    _check(conf, sps, 0, "invalid conf")
+    _check(conf, sps, 1, "invalid conf")
+    # flat profile admits every positive candidate
+    conf = rng.uniform(0.05, 1, (7, 5)).astype(np.float32)
+    ln, _, _ = gpu_schedule(conf, np.ones(7 * 6 + 1), 0)
+    assert ln.tolist() == [5] * 7
+    # equal confidences everywhere: ties broken by request, then position
+    conf = np.full((64, 8), 0.75, np.float32)
+    sps = 1.0 / (1 + np.maximum(0, np.arange(64 * 9 + 1) - 100) / 128.0)
+    _check(conf, sps, 0, "ties")
+    _check(conf, sps, 1, "ties")
+
+
+@pytest.mark.parametrize("R,K", [(512, 16), (8192, 1), (1024, 8), (33, 7)])
+def test_sizes(R, K):
+    """Largest candidate counts (R*K = 8192) and ragged, non-power-of-two sizes."""
+    w = synth.scaled(synth.WORKLOADS["highconc"], R=R, K=K, knee=R + R // 2)
+    for mode in (0, 1):
+        case = guard.schedule_case(w, 7, mode=mode)
+        if not case.sched_guarded:
+            pytest.skip("no guarded draw")
+        _check(case.conf, case.sps, mode, f"R{R}K{K}")
