@@ -1,0 +1,267 @@
+#!/usr/bin/env python3
+"""Benchmark of the batched verification step on one MI355X.
+
+One step = the whole hot path on one batch: hardware-aware prefix scheduling
+(dspark_schedule) -> ragged paged verify attention for one attention layer
+(dspark_verify_attn) -> speculative acceptance over the vocabulary
+(dspark_accept), all enqueued on one stream with inputs resident in HBM.
+
+The default workload is the 128-request serving shape (64 query / 8 KV heads,
+head dim 128, log-normal contexts 2048..16384, draft block 16, vocabulary
+129280, bf16, stochastic acceptance).  Inputs are seeded and synthetic.
+Three copies of every input are rotated so that no step finds its inputs in
+the 256 MB last-level cache from the step before.
+
+Prints ONE JSON line on stdout: verified tokens/s (sum of q_len over the step
+time), the per-stage times measured with HIP events on the launch stream, the
+achieved HBM bandwidth of attention + acceptance, a roofline entry for the
+dominant kernel (verify attention) and the oracle timed on the host cores on a
+bounded sample of the same workload.  Progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E
+NCOPY = 3
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="serving")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target CPU time of the oracle baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def attention_bytes(w, kv_len: np.ndarray, q_len: np.ndarray) -> int:
+    """Algorithmic HBM bytes of one verify-attention launch."""
+    s = w.kv_elem_bytes
+    per_tok = w.Hkv * (w.Dqk if w.mla else (w.Dqk + w.Dv)) * s
+    kv = int(kv_len.astype(np.int64).sum()) * per_tok
+    qo = int(q_len.sum()) * w.Hq * (w.Dqk + w.Dv) * s
+    bt = int(((kv_len + w.page - 1) // w.page).sum()) * 4
+    return kv + qo + bt
+
+
+def accept_bytes(w, q_len: np.ndarray, accepted: np.ndarray) -> int:
+    """Algorithmic HBM bytes of one acceptance call: every verified logit row
+    once, plus the draft row at the first rejection (stochastic)."""
+    rows = int(q_len.sum()) * w.V * w.logit_elem_bytes
+    if w.greedy:
+        return rows
+    rejected = int((accepted < (q_len - 1)).sum())
+    return rows + rejected * w.V * 4
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only (--gpus {args.gpus} requested); "
+              "the multi-GPU layout is described in DESIGN.md", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_05147_amd import dspark, synth
+
+    if not torch.cuda.is_available():
+        print("bench.py: no ROCm GPU visible", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    w = synth.WORKLOADS[args.workload]
+    seed = args.seed
+    bf16 = w.dtype == "bf16"
+
+    def to_dev(a, as_bf16=False):
+        a = np.ascontiguousarray(a)
+        if as_bf16 or a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(a).to(dev)
+
+    t0 = time.time()
+    conf = synth.confidences(w, seed)
+    sps = synth.sps_table(w)
+    conf_d, sps_d = to_dev(conf), to_dev(sps)
+    # schedule once (untimed) to lay out the flattened verify rows
+    ln_d, cu_d, _ = dspark.dspark_schedule(conf_d, sps_d, 0)
+    torch.cuda.synchronize()
+    ln = ln_d.cpu().numpy()
+    q_len = 1 + ln.astype(np.int64)
+    keys = synth.flat_keys(q_len)
+    total_q = len(keys)
+    log(f"workload {w.name}: R={w.R} total_q={total_q} mean q_len={q_len.mean():.2f}")
+    kv = synth.paged_kv(w, seed)
+    q = synth.query_rows(w, seed, keys)
+    logits = synth.logit_rows(w, seed, keys)
+    needed = np.arange(w.K)[None, :] < ln[:, None]
+    dr = synth.drafts(w, seed, conf, needed=needed)
+    log(f"inputs generated in {time.time() - t0:.1f}s: KV {kv.k.nbytes * (1 if w.mla else 2) / 1e9:.2f} GB, "
+        f"logits {logits.nbytes / 1e6:.0f} MB")
+
+    # device copies (rotated)
+    copies = []
+    k0 = to_dev(kv.k.reshape(-1), bf16)
+    v0 = k0 if w.mla else to_dev(kv.v.reshape(-1), bf16)
+    base = dict(conf=conf_d, sps=sps_d, k=k0, v=v0, bt=to_dev(kv.block_table),
+                kv_len=to_dev(kv.kv_len), q=to_dev(q, bf16),
+                logits=to_dev(logits, w.logit_dtype == "bf16"), tok=to_dev(dr.draft_tok),
+                dp=None if dr.draft_p is None else to_dev(dr.draft_p),
+                u=None if dr.u is None else to_dev(dr.u))
+    del kv.k, kv.v
+    for c in range(NCOPY):
+        d = {k: (None if v is None else (v if c == 0 else v.clone())) for k, v in base.items()}
+        if w.mla:
+            d["v"] = d["k"]
+        d["len"] = torch.empty(w.R, dtype=torch.int32, device=dev)
+        d["cu"] = torch.empty(w.R + 1, dtype=torch.int32, device=dev)
+        d["out"] = torch.empty((total_q, w.Hq, w.Dv), dtype=base["q"].dtype, device=dev)
+        d["acc"] = torch.empty(w.R, dtype=torch.int32, device=dev)
+        d["nxt"] = torch.empty(w.R, dtype=torch.int32, device=dev)
+        copies.append(d)
+    ws_attn = torch.empty(dspark.dspark_verify_attn_workspace_size(
+        w.R, w.max_q, w.Hq, w.Hkv, w.Dqk, w.Dv, kv.max_pages, w.page, base["q"].dtype),
+        dtype=torch.uint8, device=dev)
+    ws_acc = torch.empty(dspark.dspark_accept_workspace_size(w.R, w.K, w.V), dtype=torch.uint8,
+                         device=dev)
+    torch.cuda.synchronize()
+    log(f"device inputs ready ({NCOPY} copies), {time.time() - t0:.1f}s")
+
+    stream = torch.cuda.current_stream()
+
+    def step(d, ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        dspark.dspark_schedule(d["conf"], d["sps"], 0, len_out=d["len"], cu_q=d["cu"])
+        if ev is not None:
+            ev[1].record(stream)
+        dspark.dspark_verify_attn(d["q"], d["k"], d["v"], kv.k_strides, kv.v_strides, d["bt"],
+                                  d["kv_len"], d["cu"], w.max_q, w.Hkv, w.Dv, w.page, w.scale,
+                                  out=d["out"], ws=ws_attn)
+        if ev is not None:
+            ev[2].record(stream)
+        dspark.dspark_accept(d["tok"], d["logits"], d["cu"], draft_p=d["dp"], u=d["u"],
+                             accepted_len=d["acc"], next_tok=d["nxt"], ws=ws_acc)
+        if ev is not None:
+            ev[3].record(stream)
+
+    for i in range(args.warmup):
+        step(copies[i % NCOPY])
+    torch.cuda.synchronize()
+    accepted = copies[0]["acc"].cpu().numpy()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        step(copies[i % NCOPY], evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    sched_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    attn_ms = np.array([e[1].elapsed_time(e[2]) for e in evs])
+    acc_ms = np.array([e[2].elapsed_time(e[3]) for e in evs])
+    ms_per_step = wall * 1e3 / args.steps
+
+    ab = attention_bytes(w, kv.kv_len, q_len)
+    cb = accept_bytes(w, q_len, accepted)
+    attn_s = attn_ms.mean() / 1e3
+    acc_s = acc_ms.mean() / 1e3
+    attn_gbps = ab / attn_s / 1e9
+    both_gbps = (ab + cb) / (attn_s + acc_s) / 1e9
+    log(f"per step: schedule {sched_ms.mean() * 1e3:.1f} us, attention {attn_ms.mean() * 1e3:.1f} us "
+        f"({attn_gbps:.0f} GB/s), accept {acc_ms.mean() * 1e3:.1f} us; "
+        f"attention+accept {both_gbps:.0f} GB/s = {both_gbps / HBM_PEAK_GBPS:.1%} of peak")
+
+    result = {
+        "metric": "verified tokens/s and achieved HBM GB/s (% of peak), verify step on 1 MI355X",
+        "value": total_q / (ms_per_step / 1e3),
+        "unit": "verified tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if bf16 else "f32",
+        "data": "synthetic (seeded; shapes and distributions of the workload)",
+        "config": {
+            "workload": f"{w.name}: R={w.R} requests, Hq={w.Hq}/Hkv={w.Hkv}, head dim {w.Dqk}/{w.Dv}, "
+                        f"page {w.page}, K={w.K}, V={w.V}, "
+                        f"{'greedy' if w.greedy else 'stochastic'} acceptance, one attention layer",
+            "seed": seed,
+            "total_q": total_q,
+            "mean_q_len": float(q_len.mean()),
+            "kv_tokens": int(kv.kv_len.sum()),
+        },
+        "stages_us": {"schedule": float(sched_ms.mean() * 1e3),
+                      "verify_attn": float(attn_ms.mean() * 1e3),
+                      "accept": float(acc_ms.mean() * 1e3)},
+        "attn_accept_hbm": {"bytes": ab + cb, "achieved_gbps": both_gbps,
+                            "frac_of_peak": both_gbps / HBM_PEAK_GBPS},
+        "emitted_tokens_per_s": float((accepted + 1).sum()) / (ms_per_step / 1e3),
+        "roofline": {"kernel": "attn_mfma_kernel" if (bf16 and w.Dqk == 128) else "attn_generic_kernel",
+                     "bound": "hbm", "achieved": attn_gbps, "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": attn_gbps / HBM_PEAK_GBPS,
+                     "bytes_per_launch": ab, "traffic": None},
+    }
+
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, seed, conf, sps, ln, kv, q, logits, dr,
+                                              args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(w, seed, conf, sps, ln, kv, q, logits, dr, target_s):
+    """The oracle on a bounded sample of the same step: the schedule over all
+    requests, then attention and acceptance for the first n requests (all of
+    their verify tokens); n grows until the sample costs about target_s."""
+    import oracle
+    from paper_2607_05147_amd import synth
+
+    cu = oracle.cu_from_len(ln)
+    kvk = synth.paged_kv(w, seed)  # the device copy freed the host arrays
+
+    def run(n):
+        t = time.perf_counter()
+        oracle.schedule(conf, sps, 0)
+        sub_cu = cu[: n + 1]
+        rows = int(sub_cu[-1])
+        oracle.verify_attn(q[:rows], kvk.k, kvk.v, kvk.k_strides, kvk.v_strides,
+                           kvk.block_table[:n], kvk.kv_len[:n], sub_cu, w.Hq, w.Hkv, w.Dqk, w.Dv,
+                           w.page, w.scale, w.dtype)
+        oracle.accept(dr.draft_tok[:n], None if dr.draft_p is None else dr.draft_p[:n],
+                      logits[:rows], w.logit_dtype, sub_cu, w.K, w.V,
+                      u=None if dr.u is None else dr.u[:n])
+        return time.perf_counter() - t, rows
+
+    n = 1
+    el, rows = run(n)
+    while el < target_s / 4 and n < w.R:
+        n = min(w.R, max(n + 1, int(n * min(8.0, target_s / max(el, 1e-3)))))
+        el, rows = run(n)
+    log(f"oracle baseline: {n} requests, {rows} verify tokens in {el:.1f}s "
+        f"on {oracle.threads()} threads")
+    return {"value": rows / el, "unit": "verified tokens/s", "cores": oracle.threads(),
+            "kind": "oracle",
+            "sample": f"schedule over all {w.R} requests; attention + acceptance for requests "
+                      f"0..{n - 1} ({rows} verify tokens, {int(kvk.kv_len[:n].sum())} context tokens)",
+            "seconds": el}
+
+
+if __name__ == "__main__":
+    main()

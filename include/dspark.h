@@ -123,7 +123,7 @@ dspark_status dspark_schedule(const float* conf, int R, int K, const double* sps
  *   dt        element type of q, k_cache, v_cache and out.
  *   Supported: Hq % Hkv == 0; Dqk, Dv multiples of 8 up to 576;
  *   page_size multiple of 16.  bf16 with Dqk == Dv == 128 and page_size a
- *   multiple of 32 runs on MFMA tiles; other shapes run on vector ALUs.
+ *   power of two >= 64 runs on MFMA tiles; other shapes run on vector ALUs.
  * ---------------------------------------------------------------------- */
 size_t dspark_verify_attn_workspace_size(int R, int max_q, int Hq, int Hkv, int Dqk, int Dv,
                                          int max_pages, int page_size, dspark_dtype dt);
@@ -170,7 +170,7 @@ dspark_status dspark_verify_attn(const void* q, const void* k_cache, const void*
  *             sum_v min(p_t(v), p_d(v)) (one minus the total variation
  *             distance, the confidence head's training label); -1 for bonus
  *             rows.
- *   Limits: 1 <= V, ld >= V, 0 <= K <= 64, inv_temperature > 0.
+ *   Limits: 1 <= V <= 2^20, ld >= V, 0 <= K <= 64, inv_temperature > 0.
  * ---------------------------------------------------------------------- */
 size_t dspark_accept_workspace_size(int R, int K, int V);
 

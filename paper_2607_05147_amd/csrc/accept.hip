@@ -27,6 +27,7 @@ constexpr int kAccThreads = 256;
 constexpr int kChunk = 8192;                        // vocabulary entries per chunk
 constexpr int kPerThread = kChunk / kAccThreads;    // 32
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kMaxChunks = 128;                     // V <= 2^20
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -96,37 +97,76 @@ __device__ __forceinline__ float load_logit(const void* base, int64_t i) {
     return ((const float*)base)[i];
 }
 
-// Loads this thread's kPerThread consecutive logits of [v0, v1) into x[]
-// (positions past v1 get -inf).  Vector path: 16-byte loads.
+// Element e of this thread within a chunk starting at v0, in the
+// lane-interleaved layout used by the reductions: every 16-byte group of
+// consecutive elements belongs to one thread and consecutive threads read
+// consecutive groups, so each load instruction covers one contiguous span.
+template <bool BF16>
+__device__ __forceinline__ int ilv_index(int v0, int e) {
+    constexpr int G = BF16 ? 8 : 4;  // elements per 16 bytes
+    return v0 + (e / G) * (kAccThreads * G) + threadIdx.x * G + (e % G);
+}
+
+// Loads this thread's kPerThread logits of [v0, v1) (interleaved layout) into
+// x[]; positions past v1 get -inf.  VEC: 16-byte loads for full chunks.
 template <bool BF16, bool VEC>
 __device__ __forceinline__ void load_chunk(const void* row, int v0, int v1, float* x) {
-    const int first = v0 + threadIdx.x * kPerThread;
-    if (VEC && first + kPerThread <= v1) {
+    constexpr int G = BF16 ? 8 : 4;
+    if (VEC && v0 + kChunk <= v1) {
         if (BF16) {
-            const u32x4* p = (const u32x4*)((const uint16_t*)row + first);
+            const u32x4* p = (const u32x4*)((const uint16_t*)row + v0) + threadIdx.x;
 #pragma unroll
-            for (int q = 0; q < kPerThread / 8; ++q) {
-                const u32x4 w = __builtin_nontemporal_load(p + q);
-                const uint32_t ww[4] = {w[0], w[1], w[2], w[3]};
+            for (int q = 0; q < kPerThread / G; ++q) {
+                const u32x4 w = __builtin_nontemporal_load(p + q * kAccThreads);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    x[q * 8 + 2 * e] = __uint_as_float(ww[e] << 16);
-                    x[q * 8 + 2 * e + 1] = __uint_as_float(ww[e] & 0xffff0000u);
+                    x[q * 8 + 2 * e] = __uint_as_float(w[e] << 16);
+                    x[q * 8 + 2 * e + 1] = __uint_as_float(w[e] & 0xffff0000u);
                 }
             }
         } else {
-            const f32x4* p = (const f32x4*)((const float*)row + first);
+            const f32x4* p = (const f32x4*)((const float*)row + v0) + threadIdx.x;
 #pragma unroll
-            for (int q = 0; q < kPerThread / 4; ++q) {
-                const f32x4 w = __builtin_nontemporal_load(p + q);
+            for (int q = 0; q < kPerThread / G; ++q) {
+                const f32x4 w = __builtin_nontemporal_load(p + q * kAccThreads);
                 x[q * 4 + 0] = w[0]; x[q * 4 + 1] = w[1]; x[q * 4 + 2] = w[2]; x[q * 4 + 3] = w[3];
+            }
+        }
+    } else {
+        // partial chunk: unconditional loads of a clamped index (all in flight at
+        // once), then mask; a conditional load per element would serialize
+#pragma unroll
+        for (int e = 0; e < kPerThread; ++e) {
+            const int v = ilv_index<BF16>(v0, e);
+            const float xv = load_logit<BF16>(row, min(v, v1 - 1));
+            x[e] = v < v1 ? xv : -__builtin_huge_valf();
+        }
+    }
+}
+
+// Draft probabilities of the same interleaved positions.
+template <bool BF16, bool VEC>
+__device__ __forceinline__ void load_draft(const float* pd, int v0, int v1, float* x) {
+    if (VEC && v0 + kChunk <= v1) {
+        constexpr int G = BF16 ? 8 : 4;
+        const f32x4* p = (const f32x4*)(pd + v0);
+#pragma unroll
+        for (int q = 0; q < kPerThread / G; ++q) {
+#pragma unroll
+            for (int h = 0; h < G / 4; ++h) {
+                // elements q*G*256 + tid*G + 4h .. +4
+                const f32x4 w = __builtin_nontemporal_load(
+                    p + (q * kAccThreads * G + threadIdx.x * G) / 4 + h);
+                x[q * G + 4 * h + 0] = w[0]; x[q * G + 4 * h + 1] = w[1];
+                x[q * G + 4 * h + 2] = w[2]; x[q * G + 4 * h + 3] = w[3];
             }
         }
     } else {
 #pragma unroll
         for (int e = 0; e < kPerThread; ++e) {
-            const int v = first + e;
-            x[e] = v < v1 ? load_logit<BF16>(row, v) : -__builtin_huge_valf();
+            const int v = ilv_index<BF16>(v0, e);
+            const float qv = pd[min(v, v1 - 1)];
+            x[e] = v < v1 ? qv : 0.0f;
         }
     }
 }
@@ -153,15 +193,15 @@ __global__ __launch_bounds__(kAccThreads) void acc_rowpass(
         const void* rp = (const char*)logits + (size_t)row * (size_t)ld * esz;
         float x[kPerThread];
         load_chunk<BF16, VEC>(rp, v0, v1, x);
-        const int first = v0 + threadIdx.x * kPerThread;
         if (GREEDY) {
-            // thread-local max/argmax; the thread's first in-range element seeds it
-            float best = x[0];
-            int arg = first < v1 ? first : 0x7fffffff;
+            // thread-local max/argmax, lowest index among equal values
+            float best = -__builtin_huge_valf();
+            int arg = 0x7fffffff;
 #pragma unroll
-            for (int e = 1; e < kPerThread; ++e)
-                if (x[e] > best) { best = x[e]; arg = first + e; }
-            if (first >= v1) best = -__builtin_huge_valf();
+            for (int e = 0; e < kPerThread; ++e) {
+                const int v = ilv_index<BF16>(v0, e);
+                if (v < v1 && (x[e] > best || (x[e] == best && v < arg))) { best = x[e]; arg = v; }
+            }
 #pragma unroll
             for (int o = 32; o > 0; o >>= 1) {
                 const float ob = __shfl_xor(best, o, DSPARK_WAVE);
@@ -207,6 +247,43 @@ __global__ __launch_bounds__(kAccThreads) void acc_rowpass(
 
 // ---------------------------------------------------------------- resolve
 
+// Row statistics from the chunk statistics: one wave per row, lanes over chunks.
+template <bool GREEDY>
+__device__ __forceinline__ void row_stats(const ChunkStat* st, int nch, float& A, float& B,
+                                          int& arg) {
+    const int lane = threadIdx.x & (DSPARK_WAVE - 1);
+    float a = -__builtin_huge_valf(), b = 0.0f;
+    int i = 0x7fffffff;
+    for (int c = lane; c < nch; c += DSPARK_WAVE) {
+        const ChunkStat x = st[c];
+        if (GREEDY) {
+            if (x.a > a || (x.a == a && x.arg < i)) { a = x.a; i = x.arg; }
+        } else if (x.a > -__builtin_huge_valf()) {
+            if (x.a > a) { b = b * exp2f(a - x.a) + x.b; a = x.a; }
+            else b += x.b * exp2f(x.a - a);
+        }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const float oa = __shfl_xor(a, o, DSPARK_WAVE);
+        const float ob = __shfl_xor(b, o, DSPARK_WAVE);
+        const int oi = __shfl_xor(i, o, DSPARK_WAVE);
+        if (GREEDY) {
+            if (oa > a || (oa == a && oi < i)) { a = oa; i = oi; }
+        } else {
+            const float m = fmaxf(a, oa);
+            float nb = 0.0f;
+            if (a > -__builtin_huge_valf()) nb += b * exp2f(a - m);
+            if (oa > -__builtin_huge_valf()) nb += ob * exp2f(oa - m);
+            a = m;
+            b = nb;
+        }
+    }
+    A = a;
+    B = b;
+    arg = i;
+}
+
 template <bool BF16, bool GREEDY>
 __global__ __launch_bounds__(kAccThreads) void acc_resolve(
     const int32_t* __restrict__ draft_tok, const float* __restrict__ draft_p,
@@ -216,10 +293,10 @@ __global__ __launch_bounds__(kAccThreads) void acc_resolve(
     int32_t* __restrict__ accepted_len, int32_t* __restrict__ next_tok) {
     __shared__ int s_rej[65];
     __shared__ int s_arg[65];
-    __shared__ float s_M[65];
-    __shared__ float s_S[65];
     const int r = blockIdx.x;
     const int tid = threadIdx.x;
+    const int lane = tid & (DSPARK_WAVE - 1);
+    const int wave = tid / DSPARK_WAVE;
     const int nch = n_chunks(V);
     const int row0 = cu_q[r];
     const int l = cu_q[r + 1] - row0 - 1;
@@ -232,41 +309,34 @@ __global__ __launch_bounds__(kAccThreads) void acc_resolve(
         return;
     }
     const size_t esz = BF16 ? 2 : 4;
-    if (tid <= l) {
-        const int64_t row = row0 + tid;
-        const ChunkStat* st = stats + row * nch;
-        int rej = 0;
-        if (GREEDY) {
-            float best = st[0].a;
-            int arg = st[0].arg;
-            for (int c = 1; c < nch; ++c)
-                if (st[c].a > best) { best = st[c].a; arg = st[c].arg; }
-            if (tid < l) rej = draft_tok[(int64_t)r * K + tid] != arg;
-            s_arg[tid] = arg;
-        } else {
-            float M = st[0].a;
-            for (int c = 1; c < nch; ++c) M = fmaxf(M, st[c].a);
-            float S = 0.0f;
-            for (int c = 0; c < nch; ++c)
-                if (st[c].a > -__builtin_huge_valf()) S += st[c].b * exp2f(st[c].a - M);
-            rows[row] = RowInfo{M, S, r, tid};
-            if (tid < l) {
-                const int x = draft_tok[(int64_t)r * K + tid];
-                if (x < 0 || x >= V) {
-                    rej = 1;
-                } else {
-                    const void* rp = (const char*)logits + (size_t)row * (size_t)ld * esz;
-                    const float y = load_logit<BF16>(rp, x) * scale2;
-                    const float pt = exp2f(y - M) / S;
-                    const float pd = draft_p[((int64_t)r * K + tid) * V + x];
-                    const float ratio = pd > 0.0f ? pt / pd : __builtin_huge_valf();
-                    rej = !(u[(int64_t)r * (K + 1) + tid] < ratio);
+    for (int t = wave; t <= l; t += kAccThreads / DSPARK_WAVE) {
+        const int64_t row = row0 + t;
+        float A, B;
+        int arg;
+        row_stats<GREEDY>(stats + row * nch, nch, A, B, arg);
+        if (lane == 0) {
+            int rej = 0;
+            if (GREEDY) {
+                if (t < l) rej = draft_tok[(int64_t)r * K + t] != arg;
+                s_arg[t] = arg;
+            } else {
+                rows[row] = RowInfo{A, B, r, t};
+                if (t < l) {
+                    const int x = draft_tok[(int64_t)r * K + t];
+                    if (x < 0 || x >= V) {
+                        rej = 1;
+                    } else {
+                        const void* rp = (const char*)logits + (size_t)row * (size_t)ld * esz;
+                        const float y = load_logit<BF16>(rp, x) * scale2;
+                        const float pt = exp2f(y - A) / B;
+                        const float pd = draft_p[((int64_t)r * K + t) * V + x];
+                        const float ratio = pd > 0.0f ? pt / pd : __builtin_huge_valf();
+                        rej = !(u[(int64_t)r * (K + 1) + t] < ratio);
+                    }
                 }
             }
-            s_M[tid] = M;
-            s_S[tid] = S;
+            s_rej[t] = rej;
         }
-        s_rej[tid] = rej;
     }
     __syncthreads();
     if (tid == 0) {
@@ -274,18 +344,15 @@ __global__ __launch_bounds__(kAccThreads) void acc_resolve(
         for (int t = 0; t < l; ++t)
             if (s_rej[t]) { acc = t; break; }
         accepted_len[r] = acc;
-        if (GREEDY) {
-            next_tok[r] = s_arg[acc];
-        } else {
-            draw[r] = DrawInfo{acc < l ? 2 : 1, row0 + acc, acc, 0};
-        }
+        if (GREEDY) next_tok[r] = s_arg[acc];
+        else draw[r] = DrawInfo{acc < l ? 2 : 1, row0 + acc, acc, 0};
     }
 }
 
 // ---------------------------------------------------------------- residual masses
 
 // mass of max(0, p_t - p_d) per (request, chunk) for requests that rejected
-template <bool BF16, bool VEC>
+template <bool BF16, bool VEC, bool PDVEC>
 __global__ __launch_bounds__(kAccThreads) void acc_resid(
     const float* __restrict__ draft_p, const void* __restrict__ logits, int64_t ld, int R, int K,
     int V, float scale2, const RowInfo* __restrict__ rows, const DrawInfo* __restrict__ draw,
@@ -306,18 +373,16 @@ __global__ __launch_bounds__(kAccThreads) void acc_resid(
         const int v1 = min(V, v0 + kChunk);
         const void* rp = (const char*)logits + (size_t)d.row * (size_t)ld * esz;
         const float* pd = draft_p + ((int64_t)r * K + d.t) * V;
-        float x[kPerThread];
+        float x[kPerThread], q[kPerThread];
         load_chunk<BF16, VEC>(rp, v0, v1, x);
-        const int first = v0 + threadIdx.x * kPerThread;
+        load_draft<BF16, VEC && PDVEC>(pd, v0, v1, q);
         const float invS = 1.0f / ri.S;
         float acc = 0.0f;
 #pragma unroll
         for (int e = 0; e < kPerThread; ++e) {
-            const int v = first + e;
-            if (v < v1) {
-                const float pt = exp2f(x[e] * scale2 - ri.M) * invS;
-                acc += fmaxf(pt - pd[v], 0.0f);
-            }
+            // positions past v1 have x = -inf: exp2 gives 0 and the term vanishes
+            const float pt = exp2f(x[e] * scale2 - ri.M) * invS;
+            acc += fmaxf(pt - q[e], 0.0f);
         }
         double w = wave_sum_f64((double)acc);
         if (lane == 0) s_w[wave] = w;
@@ -340,6 +405,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_draw(
     const ChunkStat* __restrict__ stats, const RowInfo* __restrict__ rows,
     const DrawInfo* __restrict__ draw, const double* __restrict__ mass,
     int32_t* __restrict__ next_tok) {
+    __shared__ double s_w[kMaxChunks];
     __shared__ int s_chunk;
     __shared__ double s_thr;
     __shared__ int s_kind;
@@ -356,39 +422,41 @@ __global__ __launch_bounds__(kAccThreads) void acc_draw(
     const RowInfo ri = rows[d.row];
     const ChunkStat* st = stats + (int64_t)d.row * nch;
     const double uu = (double)u[(int64_t)r * (K + 1) + K];
-    if (tid == 0) {
-        int kind = d.kind;
-        if (kind == 2) {
-            double tot = 0.0;
-            for (int c = 0; c < nch; ++c) tot += mass[(int64_t)r * nch + c];
-            if (!(tot > 0.0)) kind = 1;  // empty residual: draw from the target row
-        }
-        // chunk masses in the units of the element masses used below
+    // chunk masses, in the units of the element masses used below
+    int kind = d.kind;
+    if (kind == 2) {
+        double t = 0.0;
+        for (int c = tid; c < nch; c += kAccThreads) t += mass[(int64_t)r * nch + c];
+        t = wave_sum_f64(t);
+        if (lane == 0) s_scan[wave] = t;
+        __syncthreads();
         double tot = 0.0;
-        for (int c = 0; c < nch; ++c) {
-            const double w = kind == 2 ? mass[(int64_t)r * nch + c]
-                                       : (st[c].a > -__builtin_huge_valf()
-                                              ? (double)st[c].b * (double)exp2f(st[c].a - ri.M)
-                                              : 0.0);
-            tot += w;
-        }
+        for (int q = 0; q < kAccThreads / DSPARK_WAVE; ++q) tot += s_scan[q];
+        if (!(tot > 0.0)) kind = 1;  // empty residual: draw from the target row
+        __syncthreads();
+    }
+    for (int c = tid; c < nch; c += kAccThreads) {
+        const ChunkStat x = st[c];
+        s_w[c] = kind == 2 ? mass[(int64_t)r * nch + c]
+                           : (x.a > -__builtin_huge_valf()
+                                  ? (double)x.b * (double)exp2f(x.a - ri.M) : 0.0);
+    }
+    __syncthreads();
+    if (tid == 0) {
+        double tot = 0.0;
+        for (int c = 0; c < nch; ++c) tot += s_w[c];
         const double thr = uu * tot;
-        double cum = 0.0;
+        double cum = 0.0, before = 0.0;
         int pick = -1, lastpos = 0;
-        double before = 0.0;
         for (int c = 0; c < nch; ++c) {
-            const double w = kind == 2 ? mass[(int64_t)r * nch + c]
-                                       : (st[c].a > -__builtin_huge_valf()
-                                              ? (double)st[c].b * (double)exp2f(st[c].a - ri.M)
-                                              : 0.0);
+            const double w = s_w[c];
             if (w > 0.0) lastpos = c;
             if (pick < 0 && cum + w > thr) { pick = c; before = cum; }
             cum += w;
         }
-        if (pick < 0) {  // rounding pushed u*total past the end: take the last non-empty chunk
+        if (pick < 0) {  // rounding pushed u*total past the end: last non-empty chunk
             pick = lastpos;
-            before = cum - (kind == 2 ? mass[(int64_t)r * nch + pick]
-                                      : (double)st[pick].b * (double)exp2f(st[pick].a - ri.M));
+            before = cum - s_w[pick];
         }
         s_chunk = pick;
         s_thr = thr - before;
@@ -398,7 +466,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_draw(
     }
     __syncthreads();
     const int c = s_chunk;
-    const int kind = s_kind;
+    kind = s_kind;
     const double thr = s_thr;
     const int v0 = c * kChunk;
     const int v1 = min(V, v0 + kChunk);
@@ -406,26 +474,65 @@ __global__ __launch_bounds__(kAccThreads) void acc_draw(
     const void* rp = (const char*)logits + (size_t)d.row * (size_t)ld * esz;
     const float* pd = draft_p + ((int64_t)r * K + d.t) * V;
     const float invS = 1.0f / ri.S;
+    // this thread's contiguous slice [first, first + kPerThread) of the chunk
     const int first = v0 + tid * kPerThread;
-    float w[kPerThread];
+    float x[kPerThread], q[kPerThread];
+    const bool full = first + kPerThread <= v1;
+    const bool xvec = full && ((uintptr_t)rp % 16 == 0);
+    if (xvec && BF16) {
+        const u32x4* p4 = (const u32x4*)((const uint16_t*)rp + first);
+#pragma unroll
+        for (int k = 0; k < kPerThread / 8; ++k) {
+            const u32x4 w = p4[k];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                x[8 * k + 2 * e] = __uint_as_float(w[e] << 16);
+                x[8 * k + 2 * e + 1] = __uint_as_float(w[e] & 0xffff0000u);
+            }
+        }
+    } else if (xvec) {
+        const f32x4* p4 = (const f32x4*)((const float*)rp + first);
+#pragma unroll
+        for (int k = 0; k < kPerThread / 4; ++k) {
+            const f32x4 w = p4[k];
+            x[4 * k] = w[0]; x[4 * k + 1] = w[1]; x[4 * k + 2] = w[2]; x[4 * k + 3] = w[3];
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < kPerThread; ++e) {
+            const float xv = load_logit<BF16>(rp, min(first + e, v1 - 1));
+            x[e] = first + e < v1 ? xv : -__builtin_huge_valf();
+        }
+    }
+    if (kind == 2) {
+        if (full && ((uintptr_t)(pd + first) % 16 == 0)) {
+            const f32x4* p4 = (const f32x4*)(pd + first);
+#pragma unroll
+            for (int k = 0; k < kPerThread / 4; ++k) {
+                const f32x4 w = p4[k];
+                q[4 * k] = w[0]; q[4 * k + 1] = w[1]; q[4 * k + 2] = w[2]; q[4 * k + 3] = w[3];
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < kPerThread; ++e) {
+                const float qv = pd[min(first + e, v1 - 1)];
+                q[e] = first + e < v1 ? qv : 0.0f;
+            }
+        }
+    }
+    float wv[kPerThread];
     double loc = 0.0;
     int lastpos = -1;
 #pragma unroll
     for (int e = 0; e < kPerThread; ++e) {
-        const int v = first + e;
-        float m = 0.0f;
-        if (v < v1) {
-            const float y = load_logit<BF16>(rp, v) * scale2;
-            if (kind == 2) {
-                const float pt = exp2f(y - ri.M) * invS;
-                m = fmaxf(pt - pd[v], 0.0f);
-            } else {
-                m = exp2f(y - ri.M);
-            }
-        }
-        w[e] = m;
+        const float y = x[e] * scale2;
+        float m;
+        if (kind == 2) m = fmaxf(exp2f(y - ri.M) * invS - q[e], 0.0f);
+        else m = exp2f(y - ri.M);
+        if (first + e >= v1) m = 0.0f;
+        wv[e] = m;
         loc += (double)m;
-        if (m > 0.0f) lastpos = v;
+        if (m > 0.0f) lastpos = first + e;
     }
     // exclusive scan of the per-thread sums over the block
     double incl = loc;
@@ -437,13 +544,13 @@ __global__ __launch_bounds__(kAccThreads) void acc_draw(
     if (lane == DSPARK_WAVE - 1) s_scan[wave] = incl;
     __syncthreads();
     double pre = incl - loc;
-    for (int q = 0; q < wave; ++q) pre += s_scan[q];
+    for (int k = 0; k < wave; ++k) pre += s_scan[k];
     // the smallest index whose running mass exceeds thr; threads past the
     // crossing also propose a candidate, and the minimum wins
     if (pre + loc > thr) {
         double cum = pre;
         for (int e = 0; e < kPerThread; ++e) {
-            cum += (double)w[e];
+            cum += (double)wv[e];
             if (cum > thr) { atomicMin(&s_pick, first + e); break; }
         }
     }
@@ -458,7 +565,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_draw(
 
 // ---------------------------------------------------------------- analytic rate
 
-template <bool BF16, bool VEC>
+template <bool BF16, bool VEC, bool PDVEC>
 __global__ __launch_bounds__(kAccThreads) void acc_rate_pass(
     const float* __restrict__ draft_p, const void* __restrict__ logits, int64_t ld,
     const int32_t* __restrict__ cu_q, int R, int K, int V, float scale2,
@@ -482,16 +589,14 @@ __global__ __launch_bounds__(kAccThreads) void acc_rate_pass(
         const int v1 = min(V, v0 + kChunk);
         const void* rp = (const char*)logits + (size_t)row * (size_t)ld * esz;
         const float* pd = draft_p + ((int64_t)r * K + ri.t) * V;
-        float x[kPerThread];
+        float x[kPerThread], q[kPerThread];
         load_chunk<BF16, VEC>(rp, v0, v1, x);
-        const int first = v0 + threadIdx.x * kPerThread;
+        load_draft<BF16, VEC && PDVEC>(pd, v0, v1, q);
         const float invS = 1.0f / ri.S;
         float acc = 0.0f;
 #pragma unroll
-        for (int e = 0; e < kPerThread; ++e) {
-            const int v = first + e;
-            if (v < v1) acc += fminf(exp2f(x[e] * scale2 - ri.M) * invS, pd[v]);
-        }
+        for (int e = 0; e < kPerThread; ++e)
+            acc += fminf(exp2f(x[e] * scale2 - ri.M) * invS, q[e]);
         double w = wave_sum_f64((double)acc);
         if (lane == 0) s_w[wave] = w;
         __syncthreads();
@@ -553,21 +658,21 @@ static hipError_t launch_typed(const AcceptArgs& a, void* ws, hipStream_t s) {
                        a.logits, a.ld, a.u, a.cu_q, a.R, a.K, a.V, scale2, w.stats, w.rows,
                        w.draw, a.accepted_len, a.next_tok);
     const int rgrid = (int)std::max<int64_t>(1, std::min<int64_t>((int64_t)a.R * nch, 2048));
-    if (vec)
-        hipLaunchKernelGGL((acc_resid<BF16, true>), dim3(rgrid), blk, 0, s, a.draft_p, a.logits,
-                           a.ld, a.R, a.K, a.V, scale2, w.rows, w.draw, w.mass);
-    else
-        hipLaunchKernelGGL((acc_resid<BF16, false>), dim3(rgrid), blk, 0, s, a.draft_p,
-                           a.logits, a.ld, a.R, a.K, a.V, scale2, w.rows, w.draw, w.mass);
+    // draft rows start at multiples of V floats: 16-byte aligned when V % 4 == 0
+    const bool pdvec = a.V % 4 == 0 && ((uintptr_t)a.draft_p % 16) == 0;
+#define DS_RESID(VV, PV)                                                                      \
+    hipLaunchKernelGGL((acc_resid<BF16, VV, PV>), dim3(rgrid), blk, 0, s, a.draft_p, a.logits, \
+                       a.ld, a.R, a.K, a.V, scale2, w.rows, w.draw, w.mass)
+    if (vec && pdvec) DS_RESID(true, true); else if (vec) DS_RESID(true, false); else DS_RESID(false, false);
+#undef DS_RESID
     hipLaunchKernelGGL((acc_draw<BF16>), dim3(a.R), blk, 0, s, a.draft_p, a.logits, a.ld, a.u,
                        a.R, a.K, a.V, scale2, w.stats, w.rows, w.draw, w.mass, a.next_tok);
     if (a.accept_rate) {
-        if (vec)
-            hipLaunchKernelGGL((acc_rate_pass<BF16, true>), dim3(grid), blk, 0, s, a.draft_p,
-                               a.logits, a.ld, a.cu_q, a.R, a.K, a.V, scale2, w.rows, w.rate);
-        else
-            hipLaunchKernelGGL((acc_rate_pass<BF16, false>), dim3(grid), blk, 0, s, a.draft_p,
-                               a.logits, a.ld, a.cu_q, a.R, a.K, a.V, scale2, w.rows, w.rate);
+#define DS_RATE(VV, PV)                                                                      \
+        hipLaunchKernelGGL((acc_rate_pass<BF16, VV, PV>), dim3(grid), blk, 0, s, a.draft_p,   \
+                           a.logits, a.ld, a.cu_q, a.R, a.K, a.V, scale2, w.rows, w.rate)
+        if (vec && pdvec) DS_RATE(true, true); else if (vec) DS_RATE(true, false); else DS_RATE(false, false);
+#undef DS_RATE
         const int fgrid = (int)std::max<int64_t>(
             1, std::min<int64_t>(((int64_t)a.R * (a.K + 1) + kAccThreads - 1) / kAccThreads, 1024));
         hipLaunchKernelGGL(acc_rate_final, dim3(fgrid), blk, 0, s, a.cu_q, a.R, a.V, max_rows, w.rows,

@@ -1,22 +1,32 @@
 // Ragged causal verify attention, bf16, head dim 128, on gfx950 matrix cores.
 //
-// Work item = (request r, KV head g, KV split s, row chunk rc).  The rows of an
-// item are the request's q_len verify tokens times the GQA group, packed
-// row = t * group + head_in_group, up to 64 per chunk (four 16-row tiles).
-// A split covers about 2048 keys; the workgroup's four waves each stream a
-// contiguous quarter of it in 32-key steps:
-//   S^T[key, row] = K Q^T      v_mfma_f32_16x16x32_bf16, K rows loaded straight
-//                              from the page into the A operand (16-byte loads);
-//   online softmax per row     exp2 on log2e-scaled scores, causal and length
-//                              masks, P rounded to bf16;
-//   O^T[d, row] += V^T P^T     V staged through LDS and read transposed as the
-//                              A operand; P^T is already in B-operand layout.
-// The key order inside a 32-key step is permuted so that the score tile's
-// accumulator layout equals the B-operand layout of the second product (no
-// shuffles).  The waves are combined through LDS in a fixed order; splits are
-// combined by the last workgroup of an item to finish (fixed split order), so
-// results are reproducible bit for bit.
+// Work item = (request r, KV head g, KV split s, row chunk rc).  The rows of a
+// request are its q_len verify tokens times the GQA group, packed
+// row = t * group + head_in_group.  A workgroup has four waves; the 16-row
+// tiles of the chunk (64 * TPW rows) are dealt to them round-robin, and all
+// four share the key/value stream of the split through LDS:
+//
+//   * the split (at most ~2048 keys) is walked in 32-key steps; each step's
+//     K and V rows (8 KB each) are copied from their page straight into LDS
+//     with global_load_lds_dwordx4 (no registers involved), into a ring of
+//     four buffers, three steps ahead of the one being computed; the waits
+//     for those copies are explicit vmcnt counts;
+//   * S^T[key, row] = K Q^T with v_mfma_f32_16x16x32_bf16: K fragments are
+//     16-byte LDS reads (A operand), the wave's Q fragments stay in registers
+//     (B operand); the key order inside a step is permuted so that the score
+//     accumulator already has the B-operand layout of the next product;
+//   * online softmax per row (exp2 of log2e-scaled scores, causal and length
+//     masks), P rounded to bf16;
+//   * O^T[d, row] += V^T P^T, V^T fragments read with ds_read_b64_tr_b16
+//     (two transposing 8-byte reads per 16 x 32 fragment).
+// LDS rows are 256 bytes; the 16-byte chunks of a row are XOR-swizzled (the
+// copy chooses which chunk each lane fetches) so that the K fragment reads and
+// the transposing V reads are free of bank conflicts.  Page ids of the split
+// are loaded once (one per lane) and picked per step with readlane.  Splits of
+// one item are combined by the last workgroup to finish, in split order
+// (bitwise reproducible).
 #include <algorithm>
+#include <type_traits>
 
 #include "device_common.h"
 #include "kernels.h"
@@ -25,411 +35,604 @@ namespace dspark {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kMfThreads = 256;
 constexpr int kMfWaves = 4;
-constexpr int kSplit = 2048;   // keys per split (upper bound)
-constexpr int kStep = 32;      // keys per inner step
-constexpr int kNT = 4;         // 16-row tiles per item
-constexpr int kRows = 16 * kNT;
+constexpr int kSplit = 2048;   // keys per split (upper bound, before rounding)
+constexpr int kStepTok = 32;   // keys per step
+constexpr int kRing = 4;       // LDS buffers; copies run kRing - 1 steps ahead
 constexpr int kD = 128;
-constexpr int kVPitch = 264;   // bytes per staged V row (256 + 8: conflict-free column reads)
-constexpr int kOPitch = 68;    // floats per d row of the wave-merge buffer
+constexpr int kRowBytes = kD * 2;
+constexpr int kTileBytes = kStepTok * kRowBytes;  // 8 KB
+constexpr int kCopiesPerStep = 4;                 // 16-byte copies per thread per step
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
-constexpr int kSlotFloats = kRows * (kD + 2);
+
+// Two 16-row tiles per wave when a request can have more than 64 rows.
+static int pick_tpw(const AttnArgs& a) { return a.max_q * (a.Hq / a.Hkv) > 64 ? 2 : 1; }
 
 bool attn_mfma_supported(const AttnArgs& a) {
-    return a.bf16 && a.Dqk == kD && a.Dv == kD && a.page % kStep == 0 && a.Hq % a.Hkv == 0 &&
-           a.ks[2] % 8 == 0 && a.vs[2] % 8 == 0 && a.ks[1] % 8 == 0 && a.vs[1] % 8 == 0 &&
-           a.ks[0] % 8 == 0 && a.vs[0] % 8 == 0 && ((uintptr_t)a.q % 16) == 0 &&
-           ((uintptr_t)a.k % 16) == 0 && ((uintptr_t)a.v % 16) == 0;
+    // power-of-two pages of 64 keys or more: a split (<= kSplit + 32 keys) then
+    // spans at most 34 pages, whose ids fit one per lane of a wave
+    const int64_t lim = (int64_t)1 << 30;  // byte strides fit 32-bit offsets
+    return a.bf16 && a.Dqk == kD && a.Dv == kD && a.page >= 64 && (a.page & (a.page - 1)) == 0 &&
+           a.ks[0] < lim && a.ks[1] < lim && a.ks[2] < lim && a.vs[0] < lim && a.vs[1] < lim &&
+           a.vs[2] < lim && a.ks[2] > 0 && a.vs[2] > 0 &&
+           a.Hq % a.Hkv == 0 && a.ks[2] % 8 == 0 && a.vs[2] % 8 == 0 && a.ks[1] % 8 == 0 &&
+           a.vs[1] % 8 == 0 && a.ks[0] % 8 == 0 && a.vs[0] % 8 == 0 &&
+           ((uintptr_t)a.q % 16) == 0 && ((uintptr_t)a.k % 16) == 0 &&
+           ((uintptr_t)a.v % 16) == 0 && ((uintptr_t)a.out % 8) == 0;
 }
 
 struct MfGeom {
-    int group, max_splits, rc_max;
-    int64_t n_items;
-    size_t counter_bytes, part_bytes;
+    int tpw, chunk_rows, group, max_splits, rc_max;
+    int64_t n_items;  // upper bound on work items
+    size_t counter_bytes, list_bytes, slot_floats, part_bytes;
 };
 
 static MfGeom mf_geom(const AttnArgs& a) {
     MfGeom g;
+    g.tpw = pick_tpw(a);
+    g.chunk_rows = 16 * kMfWaves * g.tpw;
     g.group = a.Hq / a.Hkv;
     const int64_t max_kv = (int64_t)a.max_pages * a.page;
     g.max_splits = (int)std::max<int64_t>(1, (max_kv + kSplit - 1) / kSplit);
-    g.rc_max = (a.max_q * g.group + kRows - 1) / kRows;
-    g.n_items = (int64_t)a.R * a.Hkv * g.max_splits;
+    g.rc_max = (a.max_q * g.group + g.chunk_rows - 1) / g.chunk_rows;
     const int64_t slots = (int64_t)a.R * a.Hkv * g.rc_max;
-    g.counter_bytes = ((size_t)slots * sizeof(int) + 255) & ~(size_t)255;
-    g.part_bytes = (size_t)slots * g.max_splits * kSlotFloats * sizeof(float);
+    g.n_items = slots * g.max_splits;
+    // [0] work counter, [1] number of items, then one merge counter per slot
+    g.counter_bytes = ((size_t)(slots + 2) * sizeof(int) + 255) & ~(size_t)255;
+    g.list_bytes = ((size_t)g.n_items * 2 * sizeof(int4) + 255) & ~(size_t)255;
+    g.slot_floats = (size_t)g.chunk_rows * (kD + 2);
+    g.part_bytes = (size_t)slots * g.max_splits * g.slot_floats * sizeof(float);
     return g;
 }
 
 size_t attn_mfma_workspace(const AttnArgs& a) {
     const MfGeom g = mf_geom(a);
-    return g.counter_bytes + g.part_bytes;
+    return g.counter_bytes + g.list_bytes + g.part_bytes;
 }
 
 struct MfParams {
     AttnArgs a;
-    int group, max_splits, rc_max;
-    int64_t n_items;
+    int group, max_splits, rc_max, chunk_rows;
+    int page_shift;                      // log2(page size)
+    uint32_t ks0b, ks1b, ks2b, vs0b, vs1b, vs2b;  // KV strides in bytes
     float scale2;
-    int* counters;
+    int* work;      // [0] next item, [1] number of items
+    int* counters;  // merge counter per (request, KV head, row chunk)
+    int4* list;     // work items, two int4 each: {r, g, split, row chunk}, {q0, q_len, kv, splits}
     float* part;
 };
 
-__global__ void mf_zero(int* p, int n) {
-    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
+// Builds the work list on the device from cu_q / kv_len (no host round trip)
+// and clears the counters.  One workgroup; requests are handled in contiguous
+// ranges per thread and placed by an exclusive scan of their item counts.
+constexpr int kPlanThreads = 1024;
+__global__ __launch_bounds__(kPlanThreads) void mf_plan(MfParams p) {
+    const AttnArgs& a = p.a;
+    __shared__ int s_wave[kPlanThreads / 64];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int nslots = a.R * a.Hkv * p.rc_max;
+    for (int i = tid; i < nslots; i += kPlanThreads) p.counters[i] = 0;
+    const int per = (a.R + kPlanThreads - 1) / kPlanThreads;
+    const int r0 = min(a.R, tid * per), r1 = min(a.R, r0 + per);
+    auto items_of = [&](int r, int& nsplit, int& nrc) {
+        const int ql = a.cu_q[r + 1] - a.cu_q[r];
+        const int kv = a.kv_len[r];
+        nsplit = nrc = 0;
+        if (ql < 1 || ql > a.max_q || kv < ql || kv > a.max_pages * a.page) return 0;
+        nsplit = (kv + kSplit - 1) / kSplit;
+        nrc = (ql * p.group + p.chunk_rows - 1) / p.chunk_rows;
+        return a.Hkv * nsplit * nrc;
+    };
+    int mine = 0;
+    for (int r = r0; r < r1; ++r) { int ns, nr; mine += items_of(r, ns, nr); }
+    int incl = mine;
+    for (int o = 1; o < 64; o <<= 1) {
+        const int t = __shfl_up(incl, o, 64);
+        if (lane >= o) incl += t;
+    }
+    if (lane == 63) s_wave[wave] = incl;
+    __syncthreads();
+    int off = incl - mine;
+    for (int w = 0; w < wave; ++w) off += s_wave[w];
+    for (int r = r0; r < r1; ++r) {
+        int ns, nr;
+        if (!items_of(r, ns, nr)) continue;
+        // row chunks of one split next to each other (they re-read the same keys)
+        for (int g = 0; g < a.Hkv; ++g)
+            for (int sp = 0; sp < ns; ++sp)
+                for (int rc = 0; rc < nr; ++rc) {
+                    p.list[2 * off] = int4{r, g, sp, rc};
+                    p.list[2 * off + 1] = int4{a.cu_q[r], a.cu_q[r + 1] - a.cu_q[r], a.kv_len[r], ns};
+                    ++off;
+                }
+    }
+    if (tid == kPlanThreads - 1) {
+        p.work[0] = 0;
+        p.work[1] = off;  // the last thread ends at the total
+    }
 }
 
 __device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
     return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
 }
 
-__global__ __launch_bounds__(kMfThreads) void attn_mfma_kernel(MfParams p) {
-    const AttnArgs& a = p.a;
-    // LDS: per-wave staged V (4 x 32 x 264 B) / later the wave-merge buffer (128 x 68 floats)
-    __shared__ __align__(16) unsigned char lds[kD * kOPitch * 4];
-    __shared__ float s_m[kMfWaves][kRows];
-    __shared__ float s_l[kMfWaves][kRows];
-    __shared__ int s_last;
+// 16-byte chunk slot of chunk c in LDS row t (t < 32) of the K / V tile.
+__device__ __forceinline__ int k_slot(int t, int c) { return c ^ ((t & 3) | (((t >> 3) & 3) << 2)); }
+__device__ __forceinline__ int v_slot(int t, int c) { return c ^ (((t & 3) ^ ((t >> 3) & 3)) << 1); }
 
-    // ---- item decode: consecutive items go to different XCDs, the row chunks of
-    // one item share an XCD (blockIdx % 8 selects the XCD)
-    const int b = blockIdx.x;
-    const int xcd = b & 7;
-    const int y = b >> 3;
-    const int rc = y % p.rc_max;
-    const int64_t item = (int64_t)(y / p.rc_max) * 8 + xcd;
-    if (item >= p.n_items) return;
-    const int s = (int)(item % p.max_splits);
-    const int rg = (int)(item / p.max_splits);
-    const int g = rg % a.Hkv;
-    const int r = rg / a.Hkv;
-    const int q0 = a.cu_q[r];
-    const int ql = a.cu_q[r + 1] - q0;
-    const int kv = a.kv_len[r];
-    if (ql < 1 || ql > a.max_q || kv < ql || kv > a.max_pages * a.page) return;
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
+
+// A head-dim row of zeros in device memory (zero-initialised at load, never
+// written): keys at or past a split's end are copied from here instead of
+// from the page, so stale or NaN page tails never reach LDS.
+__device__ __align__(16) uint16_t g_zero_row[kD];
+
+// 16-byte copy global -> LDS for a whole wave: lane L's 16 bytes land at
+// lds_base + 16 L (lds_base is wave-uniform).  Emitted as inline asm so that
+// the compiler does not add its own conservative waits for it; the kernel
+// waits for these copies with explicit vmcnt counts.
+__device__ __forceinline__ void lds_copy16(const void* gsrc, uint32_t lds_addr) {
+    const uint32_t m0 = __builtin_amdgcn_readfirstlane(lds_addr);
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "global_load_lds_dwordx4 %1, off"
+        :
+        : "s"(m0), "v"(gsrc)
+        : "memory", "m0");
+}
+
+// s_waitcnt vmcnt(N) leaving the other counters alone (gfx9 encoding)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// NaN-propagating maximum (v_maximum3_f32; no operand canonicalisation)
+__device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+
+// max over the four lanes that share a row (lanes lr, lr + 16, lr + 32, lr + 48)
+__device__ __forceinline__ float row_max4(float v) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = vmax(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return vmax(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){lo, hi}, bf16x2));
+}
+
+// copy with a wave-uniform 64-bit base (SGPRs) and a per-lane 32-bit offset
+__device__ __forceinline__ void lds_copy16_s(uint64_t sbase, uint32_t voff, uint32_t lds_addr) {
+    const uint32_t m0 = __builtin_amdgcn_readfirstlane(lds_addr);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)sbase);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(sbase >> 32));
+    const uint64_t sb = ((uint64_t)hi << 32) | lo;
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "global_load_lds_dwordx4 %1, %2"
+        :
+        : "s"(m0), "v"(voff), "s"(sb)
+        : "memory", "m0");
+}
+
+// Split partials are exchanged between workgroups that may run on different
+// XCDs (each with its own L2).  They are written and read with relaxed
+// device-scope atomic accesses, which are coherent across XCDs per location;
+// the writer waits for its stores to complete before it bumps the merge
+// counter.  (A device-scope fence would write back and invalidate the whole L2
+// of the XCD instead.)
+__device__ __forceinline__ void st_agent(float* p, float v) {
+    __hip_atomic_store((uint32_t*)p, __float_as_uint(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_agent4(float* p, f32x4 v) {  // p 16-byte aligned
+    const u32x4 u = __builtin_bit_cast(u32x4, v);
+    __hip_atomic_store((uint64_t*)p, (uint64_t)u[0] | ((uint64_t)u[1] << 32), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store((uint64_t*)p + 1, (uint64_t)u[2] | ((uint64_t)u[3] << 32), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_agent(const float* p) {
+    return __uint_as_float(__hip_atomic_load((const uint32_t*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+}
+__device__ __forceinline__ f32x4 ld_agent4(const float* p) {
+    const uint64_t a = __hip_atomic_load((const uint64_t*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint64_t b = __hip_atomic_load((const uint64_t*)p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return __builtin_bit_cast(f32x4, u32x4{(uint32_t)a, (uint32_t)(a >> 32), (uint32_t)b, (uint32_t)(b >> 32)});
+}
+
+constexpr float kRescale = 8.0f;  // log2 headroom before the running max is moved
+
+template <int TPW>
+__device__ __forceinline__ void attn_item(const MfParams& p, const int r, const int g, const int s,
+                                          const int rc, const int q0, const int ql, const int kv,
+                                          const int nsplit, const uint32_t lds0,
+                                          int& s_last) {
+    const AttnArgs& a = p.a;
+    constexpr int kChunkRows = 16 * kMfWaves * TPW;
+    constexpr int kSlotFloats = kChunkRows * (kD + 2);
+    const int rg = r * a.Hkv + g;
+    // the plan only lists valid items: 1 <= ql <= max_q, ql <= kv <= max_pages * page,
+    // s < nsplit, rc * kChunkRows < ql * group
     const int rows = ql * p.group;
-    const int row0 = rc * kRows;
-    if (row0 >= rows) return;
-    const int nsplit = (kv + kSplit - 1) / kSplit;
-    if (s >= nsplit) return;
-    const int start = (int)(((int64_t)s * kv / nsplit) & ~(int64_t)(kStep - 1));
-    const int end = (s + 1 == nsplit) ? kv
-                                      : (int)(((int64_t)(s + 1) * kv / nsplit) & ~(int64_t)(kStep - 1));
-    const int nrows = min(kRows, rows - row0);
+    const int row0 = rc * kChunkRows;
+    const int start = (int)(((int64_t)s * kv / nsplit) & ~(int64_t)(kStepTok - 1));
+    const int end = (s + 1 == nsplit)
+                        ? kv
+                        : (int)(((int64_t)(s + 1) * kv / nsplit) & ~(int64_t)(kStepTok - 1));
+    const int nrows = min(kChunkRows, rows - row0);
     const int nt = (nrows + 15) >> 4;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
     const int lr = lane & 15;
     const int lq = lane >> 4;
+    // tiles are dealt round-robin: wave w owns tiles w, w + 4, ...
+    const int nt_w = nt > wave ? min((nt - wave + kMfWaves - 1) / kMfWaves, TPW) : 0;
 
     const uint16_t* __restrict__ qg = (const uint16_t*)a.q;
     const uint16_t* __restrict__ kc = (const uint16_t*)a.k;
     const uint16_t* __restrict__ vc = (const uint16_t*)a.v;
-    const int32_t* __restrict__ bt = a.block_table + (int64_t)r * a.max_pages;
+
+    // ---- page ids of the split, one per lane
+    const int pg0 = start >> p.page_shift;
+    const int npg = ((end - 1) >> p.page_shift) - pg0 + 1;  // <= 34 (pages of >= 64 keys)
+    const int my_page = lane < npg ? a.block_table[(int64_t)r * a.max_pages + pg0 + lane] : 0;
 
     // ---- query fragments (B operand of S^T = K Q^T) and causal limits
-    bf16x8 qf[kNT][4];
-    int lim[kNT];
+    bf16x8 qf[TPW][4];
+    int lim[TPW];
+    int lim_min = 0x7fffffff;  // smallest causal limit of this wave's rows
 #pragma unroll
-    for (int i = 0; i < kNT; ++i) {
-        const int row = row0 + 16 * i + lr;
+    for (int j = 0; j < TPW; ++j) {
+        const int row = row0 + 16 * (wave + kMfWaves * j) + lr;
         if (row < rows) {
             const int t = row / p.group;
             const int h = g * p.group + (row - t * p.group);
             const uint16_t* qp = qg + ((int64_t)(q0 + t) * a.Hq + h) * kD + 8 * lq;
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) qf[i][ks] = *(const bf16x8*)(qp + 32 * ks);
-            lim[i] = kv - ql + t;
+            for (int ks = 0; ks < 4; ++ks) qf[j][ks] = *(const bf16x8*)(qp + 32 * ks);
+            lim[j] = kv - ql + t;
+            if (j < nt_w) lim_min = min(lim_min, lim[j]);
         } else {
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) qf[i][ks] = bf16x8{};
-            lim[i] = -1;
+            for (int ks = 0; ks < 4; ++ks) qf[j][ks] = bf16x8{};
+            lim[j] = -1;
         }
     }
+    lim_min = __reduce_min_sync(~0ull, lim_min);
 
-    f32x4 acc[kNT][8];
-    float mrow[kNT], lsum[kNT];
+    f32x4 acc[TPW][8];
+    float mrow[TPW], lsum[TPW];
 #pragma unroll
-    for (int i = 0; i < kNT; ++i) {
-        mrow[i] = -__builtin_huge_valf();
-        lsum[i] = 0.0f;
+    for (int j = 0; j < TPW; ++j) {
+        mrow[j] = -__builtin_huge_valf();
+        lsum[j] = 0.0f;
 #pragma unroll
-        for (int db = 0; db < 8; ++db) acc[i][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int db = 0; db < 8; ++db) acc[j][db] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
 
-    const int nblk = (end - start + kStep - 1) / kStep;
-    const int b0 = wave * nblk / kMfWaves;
-    const int b1 = (wave + 1) * nblk / kMfWaves;
-    unsigned char* vt = lds + wave * kStep * kVPitch;
+    // ---- per-lane LDS offsets of the MFMA fragments (loop invariant)
+    int koff[2][4];
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+        const int t = 8 * (lr >> 2) + 4 * mb + (lr & 3);
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+            koff[mb][ks] = lds0 + t * kRowBytes + k_slot(t, 4 * ks + lq) * 16;
+    }
+    int voff[8][2];
+#pragma unroll
+    for (int db = 0; db < 8; ++db)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int t = 8 * lq + 4 * h + (lr >> 2);
+            const int c = 2 * db + ((lr & 3) >> 1);
+            voff[db][h] = lds0 + kTileBytes + t * kRowBytes + v_slot(t, c) * 16 + (lr & 1) * 8;
+        }
 
-    // key held by this lane as the A-operand row of the score product, per 16-key half
-    const int tau0 = 8 * (lr >> 2) + (lr & 3);
+    // ---- copy geometry: wave w, copy i (0, 1) fills LDS slots (2w + i) * 64 + lane
+    // of a 512-slot tile: row t = 4 (2w + i) + lane / 16, physical chunk lane % 16,
+    // which holds source chunk (physical ^ swizzle(t)).
+    int cp_row[2], cp_kchunk[2], cp_vchunk[2];
+    uint32_t cp_koff[2], cp_voff[2];  // byte offsets from the step's first key
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int t = 4 * (2 * wave + i) + (lane >> 4);
+        cp_row[i] = t;
+        cp_kchunk[i] = k_slot(t, lane & 15);  // the map is an involution
+        cp_vchunk[i] = v_slot(t, lane & 15);
+        cp_koff[i] = t * p.ks2b + 16 * cp_kchunk[i];
+        cp_voff[i] = t * p.vs2b + 16 * cp_vchunk[i];
+    }
+    const int nsteps = (end - start + kStepTok - 1) / kStepTok;  // >= 1
+    const int last = nsteps - 1;
+    // this wave's copy destinations start 2 KB into each tile (wave-uniform)
+    const uint32_t lds_wave = __builtin_amdgcn_readfirstlane(lds0 + wave * 2048);
+    const uint64_t kc_head = (uint64_t)(uintptr_t)kc + (uint64_t)((uint32_t)g * p.ks1b);
+    const uint64_t vc_head = (uint64_t)(uintptr_t)vc + (uint64_t)((uint32_t)g * p.vs1b);
 
-    bf16x8 kf[2][4];
-    uint4 vr[8];
-    auto load_step = [&](int blk) {
-        const int tok0 = start + blk * kStep;
-        const int64_t page = bt[tok0 / a.page];
-        const int slot0 = tok0 % a.page;
-        const uint16_t* kb = kc + page * a.ks[0] + (int64_t)g * a.ks[1] + (int64_t)slot0 * a.ks[2];
-        const uint16_t* vb = vc + page * a.vs[0] + (int64_t)g * a.vs[1] + (int64_t)slot0 * a.vs[2];
+    auto issue = [&](int n) {
+        const int tok0 = start + n * kStepTok;
+        const int page = __builtin_amdgcn_readlane(my_page, (tok0 >> p.page_shift) - pg0);
+        const int slot0 = tok0 & ((1 << p.page_shift) - 1);
+        const uint32_t kd = lds_wave + ((unsigned)n & (kRing - 1)) * (2 * kTileBytes);
+        const uint32_t vd = kd + kTileBytes;
+        if (tok0 + kStepTok <= end) {
+            const uint64_t kb = kc_head + (uint64_t)(uint32_t)page * p.ks0b + (uint32_t)slot0 * p.ks2b;
+            const uint64_t vb = vc_head + (uint64_t)(uint32_t)page * p.vs0b + (uint32_t)slot0 * p.vs2b;
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
+            for (int i = 0; i < 2; ++i) {
+                lds_copy16_s(kb, cp_koff[i], kd + i * 1024);
+                lds_copy16_s(vb, cp_voff[i], vd + i * 1024);
+            }
+        } else {
+            // last, partial step: keys at or past the end come from the zero row
+            const uint16_t* kb = kc + (int64_t)page * a.ks[0] + (int64_t)g * a.ks[1];
+            const uint16_t* vb = vc + (int64_t)page * a.vs[0] + (int64_t)g * a.vs[1];
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks)
-                kf[mb][ks] = *(const bf16x8*)(kb + (int64_t)(tau0 + 4 * mb) * a.ks[2] + 32 * ks + 8 * lq);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int c = i * 64 + lane;
-            const int tk = c >> 4;
-            const int d8 = (c & 15) * 8;
-            vr[i] = (tok0 + tk < end) ? *(const uint4*)(vb + (int64_t)tk * a.vs[2] + d8)
-                                      : uint4{0u, 0u, 0u, 0u};
+            for (int i = 0; i < 2; ++i) {
+                const int64_t tr = slot0 + cp_row[i];
+                const bool in = tok0 + cp_row[i] < end;
+                const uint16_t* ksrc = in ? kb + tr * a.ks[2] + 8 * cp_kchunk[i] : g_zero_row + 8 * cp_kchunk[i];
+                const uint16_t* vsrc = in ? vb + tr * a.vs[2] + 8 * cp_vchunk[i] : g_zero_row + 8 * cp_vchunk[i];
+                lds_copy16(ksrc, kd + i * 1024);
+                lds_copy16(vsrc, vd + i * 1024);
+            }
         }
     };
 
-    if (b0 < b1) load_step(b0);
-    for (int blk = b0; blk < b1; ++blk) {
-        const int tok0 = start + blk * kStep;
-        // stage V (keys past the split end are zero) and keep K in registers
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int c = i * 64 + lane;
-            const int tk = c >> 4;
-            const int d8 = (c & 15) * 8;
-            uint2* dst = (uint2*)(vt + tk * kVPitch + d8 * 2);
-            dst[0] = uint2{vr[i].x, vr[i].y};
-            dst[1] = uint2{vr[i].z, vr[i].w};
-        }
-        bf16x8 kcur[2][4];
+    auto compute = [&](int n, auto bufc) {
+        constexpr unsigned buf = decltype(bufc)::value;
+        const int tok0 = start + n * kStepTok;
+        constexpr uint32_t boff = buf * (2 * kTileBytes);
+        // all K fragments of the step first (8 LDS reads in flight), then the scores
+        bf16x8 kfr[2][4];
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) kcur[mb][ks] = kf[mb][ks];
-        if (blk + 1 < b1) load_step(blk + 1);
-        wave_lds_sync();
-
-        bf16x8 pf[kNT];
+            for (int ks = 0; ks < 4; ++ks) kfr[mb][ks] = *(const lds_bf16x8*)(koff[mb][ks] + boff);
+        f32x4 sc[TPW][2];
 #pragma unroll
-        for (int i = 0; i < kNT; ++i) {
-            if (i < nt) {
-                f32x4 sc[2];
+        for (int j = 0; j < TPW; ++j)
 #pragma unroll
-                for (int mb = 0; mb < 2; ++mb) {
-                    f32x4 c4 = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int mb = 0; mb < 2; ++mb) {
+                sc[j][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+                if (j < nt_w)
 #pragma unroll
                     for (int ks = 0; ks < 4; ++ks)
-                        c4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kcur[mb][ks], qf[i][ks], c4, 0, 0, 0);
-                    sc[mb] = c4;
-                }
+                        sc[j][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kfr[mb][ks], qf[j][ks], sc[j][mb], 0, 0, 0);
+            }
+        // V^T fragments (16 transposing reads in flight) while the softmax runs.
+        bf16x8 vfr[8];
+#pragma unroll
+        for (int db = 0; db < 8; ++db) {
+            const s16x4 h0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (lds_s16x4*)(voff[db][0] + boff));
+            const s16x4 h1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (lds_s16x4*)(voff[db][1] + boff));
+            vfr[db] = __builtin_bit_cast(
+                bf16x8, (short __attribute__((ext_vector_type(8)))){h0[0], h0[1], h0[2], h0[3],
+                                                                     h1[0], h1[1], h1[2], h1[3]});
+        }
+        // keys of this lane: tok0 + 8 lq + 4 mb + e; masks only where needed
+        const bool full = tok0 + kStepTok <= end && tok0 + kStepTok - 1 <= lim_min;
+        bf16x8 pf[TPW];
+#pragma unroll
+        for (int j = 0; j < TPW; ++j) {
+            if (j < nt_w) {
+                // raw scores; the scale is applied inside the exponent below
                 float sv[8];
-                float bm = -__builtin_huge_valf();
 #pragma unroll
                 for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int key = tok0 + 8 * lq + 4 * mb + e;
-                        const bool ok = key < end && key <= lim[i];
-                        const float v = ok ? sc[mb][e] * p.scale2 : -__builtin_huge_valf();
-                        sv[4 * mb + e] = v;
-                        bm = fmaxf(bm, v);
-                    }
-                bm = fmaxf(bm, __shfl_xor(bm, 16, 64));
-                bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
-                const float mn = fmaxf(mrow[i], bm);
-                float alpha = 1.0f;
-                float pr[8];
-                if (mn == -__builtin_huge_valf()) {
+                    for (int e = 0; e < 4; ++e) sv[4 * mb + e] = sc[j][mb][e];
+                if (!full) {
 #pragma unroll
-                    for (int k = 0; k < 8; ++k) pr[k] = 0.0f;
-                } else {
-                    alpha = exp2f(mrow[i] - mn);
-#pragma unroll
-                    for (int k = 0; k < 8; ++k) pr[k] = exp2f(sv[k] - mn);
-                }
-                float ps = 0.0f;
-#pragma unroll
-                for (int k = 0; k < 8; ++k) ps += pr[k];
-                lsum[i] = lsum[i] * alpha + ps;
-                mrow[i] = mn;
-#pragma unroll
-                for (int db = 0; db < 8; ++db) acc[i][db] *= alpha;
-                uint4 pk;
-                pk.x = pack2_bf16(pr[0], pr[1]);
-                pk.y = pack2_bf16(pr[2], pr[3]);
-                pk.z = pack2_bf16(pr[4], pr[5]);
-                pk.w = pack2_bf16(pr[6], pr[7]);
-                pf[i] = __builtin_bit_cast(bf16x8, pk);
-            }
-        }
-        // O^T[d, row] += V^T P^T: A = V[key 8*lq + i][d = 16*db + lr], read from LDS
-#pragma unroll
-        for (int db = 0; db < 8; ++db) {
-            const unsigned char* col = vt + (16 * db + lr) * 2 + 8 * lq * kVPitch;
-            uint16_t hv[8];
-#pragma unroll
-            for (int i = 0; i < 8; ++i) hv[i] = *(const uint16_t*)(col + i * kVPitch);
-            uint4 pk;
-            pk.x = (uint32_t)hv[0] | ((uint32_t)hv[1] << 16);
-            pk.y = (uint32_t)hv[2] | ((uint32_t)hv[3] << 16);
-            pk.z = (uint32_t)hv[4] | ((uint32_t)hv[5] << 16);
-            pk.w = (uint32_t)hv[6] | ((uint32_t)hv[7] << 16);
-            const bf16x8 vf = __builtin_bit_cast(bf16x8, pk);
-#pragma unroll
-            for (int i = 0; i < kNT; ++i)
-                if (i < nt) acc[i][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[i], acc[i][db], 0, 0, 0);
-        }
-        wave_lds_sync();
-    }
-
-    // ---- combine the four waves (fixed order) -------------------------------
-#pragma unroll
-    for (int i = 0; i < kNT; ++i) {
-        lsum[i] += __shfl_xor(lsum[i], 16, 64);
-        lsum[i] += __shfl_xor(lsum[i], 32, 64);
-        if (lq == 0) {
-            s_m[wave][16 * i + lr] = mrow[i];
-            s_l[wave][16 * i + lr] = lsum[i];
-        }
-    }
-    __syncthreads();
-    float Mrow[kNT], Lrow[kNT];
-#pragma unroll
-    for (int i = 0; i < kNT; ++i) {
-        const int rr = 16 * i + lr;
-        float M = s_m[0][rr];
-#pragma unroll
-        for (int w = 1; w < kMfWaves; ++w) M = fmaxf(M, s_m[w][rr]);
-        float L = 0.0f;
-#pragma unroll
-        for (int w = 0; w < kMfWaves; ++w)
-            if (s_m[w][rr] > -__builtin_huge_valf()) L += s_l[w][rr] * exp2f(s_m[w][rr] - M);
-        const float f = mrow[i] > -__builtin_huge_valf() ? exp2f(mrow[i] - M) : 0.0f;
-#pragma unroll
-        for (int db = 0; db < 8; ++db) acc[i][db] *= f;
-        Mrow[i] = M;
-        Lrow[i] = L;
-    }
-    float* ob = (float*)lds;  // [d][kOPitch]
-    for (int w = kMfWaves - 1; w >= 0; --w) {
-        if (wave == w) {
-#pragma unroll
-            for (int i = 0; i < kNT; ++i) {
-                if (i < nt) {
-#pragma unroll
-                    for (int db = 0; db < 8; ++db)
+                    for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
                         for (int e = 0; e < 4; ++e) {
-                            float* cell = ob + (16 * db + 4 * lq + e) * kOPitch + 16 * i + lr;
-                            if (w == kMfWaves - 1) *cell = acc[i][db][e];
-                            else if (w > 0) *cell = *cell + acc[i][db][e];
-                            else acc[i][db][e] = acc[i][db][e] + *cell;
+                            const int key = tok0 + 8 * lq + 4 * mb + e;
+                            if (!(key < end && key <= lim[j])) sv[4 * mb + e] = -__builtin_huge_valf();
                         }
                 }
+                float bm = vmax(vmax(vmax(sv[0], sv[1]), sv[2]),
+                                vmax(vmax(sv[3], sv[4]), vmax(vmax(sv[5], sv[6]), sv[7])));
+                bm = row_max4(bm) * p.scale2;
+                // move the running max only when the new one exceeds it by kRescale
+                // (P stays below 2^kRescale; the result is normalised at the end)
+                const bool need = bm > mrow[j] + kRescale;
+                if (__builtin_amdgcn_ballot_w64(need)) {
+                    const float mn = need ? bm : mrow[j];
+                    const float alpha = need ? __builtin_amdgcn_exp2f(mrow[j] - mn) : 1.0f;
+                    lsum[j] *= alpha;
+#pragma unroll
+                    for (int db = 0; db < 8; ++db) acc[j][db] *= alpha;
+                    mrow[j] = mn;
+                }
+                const float mu = mrow[j] == -__builtin_huge_valf() ? 0.0f : mrow[j];
+                float pr[8];
+#pragma unroll
+                for (int k = 0; k < 8; ++k) pr[k] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[k], p.scale2, -mu));
+                lsum[j] += ((pr[0] + pr[1]) + (pr[2] + pr[3])) + ((pr[4] + pr[5]) + (pr[6] + pr[7]));
+                // k-slot 8 lq + i <-> key 8 lq + i: M-block 0 gives i = 0..3, M-block 1 i = 4..7
+                u32x4 pk;
+                pk[0] = cvt_pk_bf16(pr[0], pr[1]);
+                pk[1] = cvt_pk_bf16(pr[2], pr[3]);
+                pk[2] = cvt_pk_bf16(pr[4], pr[5]);
+                pk[3] = cvt_pk_bf16(pr[6], pr[7]);
+                pf[j] = __builtin_bit_cast(bf16x8, pk);
             }
         }
-        __syncthreads();
-    }
+#pragma unroll
+        for (int j = 0; j < TPW; ++j)
+            if (j < nt_w)
+#pragma unroll
+                for (int db = 0; db < 8; ++db)
+                    acc[j][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vfr[db], pf[j], acc[j][db], 0, 0, 0);
+    };
 
-    // ---- wave 0 writes the item's result -------------------------------------------
+    // ---- main loop.  Every thread issues kCopiesPerStep copies per step, in step
+    // order, also past the last step (re-reading the last one into a buffer that
+    // is not read again), so "step n has landed" is always
+    // vmcnt <= (kRing - 2) * kCopiesPerStep.  Keys past the split end are copied
+    // as zeros (masked scores, zero values).  The loop is unrolled by the ring
+    // size so that every LDS address is a per-lane base plus an immediate.
+    wait_vmcnt<0>();
+#pragma unroll
+    for (int n = 0; n < kRing - 1; ++n) issue(min(n, last));
+    auto one = [&](int n, auto bufc) {
+        wait_vmcnt<(kRing - 2) * kCopiesPerStep>();
+        lds_barrier();  // step n visible to all; everyone is done with step n - 1
+        issue(min(n + kRing - 1, last));
+        if (nt_w > 0) compute(n, bufc);
+    };
+    for (int n = 0; n < nsteps; n += kRing) {
+        one(n, std::integral_constant<unsigned, 0>{});
+        if (n + 1 < nsteps) one(n + 1, std::integral_constant<unsigned, 1>{});
+        if (n + 2 < nsteps) one(n + 2, std::integral_constant<unsigned, 2>{});
+        if (n + 3 < nsteps) one(n + 3, std::integral_constant<unsigned, 3>{});
+    }
+    wait_vmcnt<0>();
+
+    // ---- finish rows: total l over the four lanes of a row
+#pragma unroll
+    for (int j = 0; j < TPW; ++j) {
+        lsum[j] += __shfl_xor(lsum[j], 16, 64);
+        lsum[j] += __shfl_xor(lsum[j], 32, 64);
+    }
     uint16_t* outp = (uint16_t*)a.out;
     if (nsplit == 1) {
-        if (wave == 0) {
 #pragma unroll
-            for (int i = 0; i < kNT; ++i) {
-                const int row = row0 + 16 * i + lr;
-                if (i < nt && row < rows) {
-                    const int t = row / p.group;
-                    const int h = g * p.group + (row - t * p.group);
-                    const int64_t orow = (int64_t)(q0 + t) * a.Hq + h;
-                    const float inv = 1.0f / Lrow[i];
+        for (int j = 0; j < TPW; ++j) {
+            const int row = row0 + 16 * (wave + kMfWaves * j) + lr;
+            if (j < nt_w && row < rows) {
+                const int t = row / p.group;
+                const int h = g * p.group + (row - t * p.group);
+                const int64_t orow = (int64_t)(q0 + t) * a.Hq + h;
+                const float inv = 1.0f / lsum[j];
 #pragma unroll
-                    for (int db = 0; db < 8; ++db) {
-                        uint2 pk;
-                        pk.x = pack2_bf16(acc[i][db][0] * inv, acc[i][db][1] * inv);
-                        pk.y = pack2_bf16(acc[i][db][2] * inv, acc[i][db][3] * inv);
-                        *(uint2*)(outp + orow * kD + 16 * db + 4 * lq) = pk;
-                    }
-                    if (a.lse && lq == 0) a.lse[orow] = (Mrow[i] + log2f(Lrow[i])) * kLn2;
+                for (int db = 0; db < 8; ++db) {
+                    uint2 pk;
+                    pk.x = pack2_bf16(acc[j][db][0] * inv, acc[j][db][1] * inv);
+                    pk.y = pack2_bf16(acc[j][db][2] * inv, acc[j][db][3] * inv);
+                    *(uint2*)(outp + orow * kD + 16 * db + 4 * lq) = pk;
                 }
+                if (a.lse && lq == 0) a.lse[orow] = (mrow[j] + log2f(lsum[j])) * kLn2;
             }
         }
         return;
     }
 
-    // ---- several splits: publish this split's partial, the last one merges ---------
+    // ---- several splits: publish this split's partial, the last one merges
     const int64_t slot_base = ((int64_t)rg * p.rc_max + rc) * p.max_splits;
-    if (wave == 0) {
+    {
         float* part = p.part + (slot_base + s) * kSlotFloats;
 #pragma unroll
-        for (int i = 0; i < kNT; ++i) {
-            const int rr = 16 * i + lr;
-            if (i < nt) {
+        for (int j = 0; j < TPW; ++j) {
+            const int rr = 16 * (wave + kMfWaves * j) + lr;
+            if (j < nt_w) {
                 if (lq == 0) {
-                    part[rr] = Mrow[i];
-                    part[kRows + rr] = Lrow[i];
+                    st_agent(part + rr, mrow[j]);
+                    st_agent(part + kChunkRows + rr, lsum[j]);
                 }
 #pragma unroll
                 for (int db = 0; db < 8; ++db)
-                    *(f32x4*)(part + 2 * kRows + rr * kD + 16 * db + 4 * lq) = acc[i][db];
+                    st_agent4(part + 2 * kChunkRows + rr * kD + 16 * db + 4 * lq, acc[j][db]);
             }
         }
-        __threadfence();
+        // the stores are complete (at the device coherence point) before the count
+        wait_vmcnt<0>();
     }
     __syncthreads();
     if (tid == 0) {
-        const int prev = atomicAdd(p.counters + (int64_t)rg * p.rc_max + rc, 1);
+        const int prev = __hip_atomic_fetch_add(p.counters + (int64_t)rg * p.rc_max + rc, 1,
+                                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         s_last = prev == nsplit - 1;
     }
     __syncthreads();
     if (!s_last) return;
-    __threadfence();
-    // merge: thread -> (row, quarter of d)
-    const int mrow_i = tid >> 2;
-    const int dq = (tid & 3) * 32;
-    if (mrow_i < nrows) {
+    constexpr int kTPR = kMfThreads / kChunkRows;  // threads per row
+    constexpr int kDPT = kD / kTPR;                // d values per thread
+    const int mr = tid / kTPR;
+    const int dq = (tid % kTPR) * kDPT;
+    if (mr < nrows) {
         const float* base = p.part + slot_base * kSlotFloats;
         float M = -__builtin_huge_valf();
-        for (int sp = 0; sp < nsplit; ++sp) M = fmaxf(M, base[sp * kSlotFloats + mrow_i]);
+        for (int sp = 0; sp < nsplit; ++sp) M = fmaxf(M, ld_agent(base + sp * kSlotFloats + mr));
         float L = 0.0f;
-        float o[32];
+        float o[kDPT];
 #pragma unroll
-        for (int k = 0; k < 32; ++k) o[k] = 0.0f;
+        for (int k = 0; k < kDPT; ++k) o[k] = 0.0f;
         for (int sp = 0; sp < nsplit; ++sp) {
             const float* sl = base + sp * kSlotFloats;
-            const float ms = sl[mrow_i];
+            const float ms = ld_agent(sl + mr);
             if (!(ms > -__builtin_huge_valf())) continue;
             const float f = exp2f(ms - M);
-            L += sl[kRows + mrow_i] * f;
-            const f32x4* src = (const f32x4*)(sl + 2 * kRows + mrow_i * kD + dq);
+            L += ld_agent(sl + kChunkRows + mr) * f;
+            const float* src = sl + 2 * kChunkRows + mr * kD + dq;
 #pragma unroll
-            for (int k = 0; k < 8; ++k) {
-                const f32x4 v = src[k];
+            for (int k = 0; k < kDPT / 4; ++k) {
+                const f32x4 v = ld_agent4(src + 4 * k);
                 o[4 * k + 0] += v[0] * f;
                 o[4 * k + 1] += v[1] * f;
                 o[4 * k + 2] += v[2] * f;
                 o[4 * k + 3] += v[3] * f;
             }
         }
-        const int row = row0 + mrow_i;
+        const int row = row0 + mr;
         const int t = row / p.group;
         const int h = g * p.group + (row - t * p.group);
         const int64_t orow = (int64_t)(q0 + t) * a.Hq + h;
         const float inv = 1.0f / L;
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
+        for (int k = 0; k < kDPT / 4; ++k) {
             uint2 pk;
             pk.x = pack2_bf16(o[4 * k] * inv, o[4 * k + 1] * inv);
             pk.y = pack2_bf16(o[4 * k + 2] * inv, o[4 * k + 3] * inv);
             *(uint2*)(outp + orow * kD + dq + 4 * k) = pk;
         }
         if (a.lse && dq == 0) a.lse[orow] = (M + log2f(L)) * kLn2;
+    }
+}
+
+// Persistent workgroups pull items from the device-built list.
+template <int TPW>
+__global__ __launch_bounds__(kMfThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void attn_mfma_kernel(MfParams p) {
+    __shared__ __align__(16) unsigned char lds[kRing][2][kTileBytes];  // [buffer][K | V]
+    __shared__ int s_last;
+    __shared__ int s_item;
+    // the ring's LDS address as a plain integer (all LDS addressing below is
+    // integer arithmetic on it)
+    uint32_t lds0 = (uint32_t)(uintptr_t)&lds[0][0][0];
+    asm volatile("" : "+s"(lds0));
+    const int total = p.work[1];
+    if (threadIdx.x == 0) s_item = atomicAdd(p.work, 1);
+    __syncthreads();
+    int it = __builtin_amdgcn_readfirstlane(s_item);
+    while (it < total) {
+        const int4 e0 = p.list[2 * it];      // uniform: scalar loads
+        const int4 e1 = p.list[2 * it + 1];
+        // take the next item now; its index is needed only at the end
+        int nxt = 0;
+        if (threadIdx.x == 0) nxt = atomicAdd(p.work, 1);
+        attn_item<TPW>(p, e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w, lds0, s_last);
+        __syncthreads();  // everyone is done with this item's LDS and s_item
+        if (threadIdx.x == 0) s_item = nxt;
+        __syncthreads();
+        it = __builtin_amdgcn_readfirstlane(s_item);
     }
 }
 
@@ -440,15 +643,32 @@ hipError_t launch_attn_mfma(const AttnArgs& a, void* ws, hipStream_t s) {
     p.group = g.group;
     p.max_splits = g.max_splits;
     p.rc_max = g.rc_max;
-    p.n_items = g.n_items;
+    p.chunk_rows = g.chunk_rows;
     p.scale2 = a.scale * kLog2e;
-    p.counters = (int*)ws;
-    p.part = (float*)((char*)ws + g.counter_bytes);
-    const int n_counters = a.R * a.Hkv * g.rc_max;
-    hipLaunchKernelGGL(mf_zero, dim3(std::min(1024, (n_counters + 255) / 256)), dim3(256), 0, s,
-                       p.counters, n_counters);
-    const int64_t grid = ((g.n_items + 7) / 8) * 8 * g.rc_max;
-    hipLaunchKernelGGL(attn_mfma_kernel, dim3((unsigned)grid), dim3(kMfThreads), 0, s, p);
+    p.page_shift = __builtin_ctz((unsigned)a.page);
+    p.ks0b = (uint32_t)(a.ks[0] * 2);
+    p.ks1b = (uint32_t)(a.ks[1] * 2);
+    p.ks2b = (uint32_t)(a.ks[2] * 2);
+    p.vs0b = (uint32_t)(a.vs[0] * 2);
+    p.vs1b = (uint32_t)(a.vs[1] * 2);
+    p.vs2b = (uint32_t)(a.vs[2] * 2);
+    p.work = (int*)ws;
+    p.counters = p.work + 2;
+    p.list = (int4*)((char*)ws + g.counter_bytes);
+    p.part = (float*)((char*)ws + g.counter_bytes + g.list_bytes);
+    hipLaunchKernelGGL(mf_plan, dim3(1), dim3(kPlanThreads), 0, s, p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    int dev = 0, cus = 0;
+    e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    // two resident workgroups per CU (64 KB of LDS and <= 256 VGPRs each)
+    const int64_t grid = std::min<int64_t>((int64_t)cus * 2, std::max<int64_t>(g.n_items, 1));
+    if (g.tpw == 2)
+        hipLaunchKernelGGL(attn_mfma_kernel<2>, dim3((unsigned)grid), dim3(kMfThreads), 0, s, p);
+    else
+        hipLaunchKernelGGL(attn_mfma_kernel<1>, dim3((unsigned)grid), dim3(kMfThreads), 0, s, p);
     return hipGetLastError();
 }
 

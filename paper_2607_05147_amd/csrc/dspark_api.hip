@@ -39,7 +39,7 @@ constexpr int kMaxK = 64;
 constexpr int kMaxSchedCand = 8192;
 constexpr int kMaxR = 8192;
 constexpr int kMaxD = 576;
-constexpr int kMaxV = 1 << 24;
+constexpr int kMaxV = 1 << 20;
 
 dspark::AttnArgs make_attn(const void* q, const void* k_cache, const void* v_cache,
                            const int64_t* k_strides, const int64_t* v_strides,

@@ -36,6 +36,8 @@ size_t schedule_lds_bytes(int R, int K) {
     size_t b = (size_t)Np * 8 + (size_t)Np * 2;
     b = (b + 15) & ~(size_t)15;
     b += (size_t)R * 4;
+    b = (b + 15) & ~(size_t)15;
+    b += (size_t)(N > 0 ? N : 1) * 4;  // staged confidences
     return b;
 }
 
@@ -52,8 +54,9 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
     extern __shared__ __align__(16) unsigned char smem[];
     uint64_t* key = reinterpret_cast<uint64_t*>(smem);
     uint16_t* idx = reinterpret_cast<uint16_t*>(key + Np);
-    int32_t* lenl = reinterpret_cast<int32_t*>(
-        smem + ((((size_t)Np * 10) + 15) & ~(size_t)15));
+    const size_t len_off = (((size_t)Np * 10) + 15) & ~(size_t)15;
+    int32_t* lenl = reinterpret_cast<int32_t*>(smem + len_off);
+    float* confl = reinterpret_cast<float*>(smem + ((len_off + (size_t)R * 4 + 15) & ~(size_t)15));
 
     __shared__ double s_wave_tot[kSchedWaves];
     __shared__ int s_first;
@@ -70,12 +73,15 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
     if (tid == 0) s_ncand = 0;
     __syncthreads();
 
-    // 1. survival products, one request per thread
+    // 1. survival products, one request per thread; the confidences are first
+    // staged in LDS with coalesced loads
+    for (int i = tid; i < N; i += kSchedThreads) confl[i] = conf[i];
+    __syncthreads();
     int my_cand = 0;
     for (int r = tid; r < R; r += kSchedThreads) {
         double p = 1.0;
         for (int j = 0; j < K; ++j) {
-            p = p * sched_conf(conf[(int64_t)r * K + j]);
+            p = p * sched_conf(confl[r * K + j]);
             key[r * K + j] = (uint64_t)__double_as_longlong(p);
             idx[r * K + j] = (uint16_t)(r * K + j);
             my_cand += p > 0.0;

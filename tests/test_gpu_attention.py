@@ -124,5 +124,6 @@ def test_repeatable_bitwise():
     dkv = DevKV(kv, True)
     o1, l1 = gpu_attention(w, dkv, q, case.cu_q)
     o2, l2 = gpu_attention(w, dkv, q, case.cu_q)
-    assert bool((o1.view(-1).view(dtype=o1.dtype) == o2).all())
-    assert bool((l1 == l2).all())
+    import torch
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(l1.view(torch.int32), l2.view(torch.int32))
