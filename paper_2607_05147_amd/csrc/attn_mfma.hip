@@ -22,9 +22,15 @@
 // LDS rows are 256 bytes; the 16-byte chunks of a row are XOR-swizzled (the
 // copy chooses which chunk each lane fetches) so that the K fragment reads and
 // the transposing V reads are free of bank conflicts.  Page ids of the split
-// are loaded once (one per lane) and picked per step with readlane.  Splits of
-// one item are combined by the last workgroup to finish, in split order
-// (bitwise reproducible).
+// are loaded once (one per lane) and picked per step with readlane.
+//
+// The workgroups are persistent and take items from a list that a one-block
+// plan kernel builds on the device, longest first.  A request whose context
+// has more than one split stores per-split partials (m, l, unnormalised o);
+// a merge kernel combines them afterwards in split order (bitwise
+// reproducible).  Exchanging them across a kernel boundary needs no
+// device-scope fences, which on this part would write back and invalidate the
+// whole L2 of an XCD.
 #include <algorithm>
 #include <type_traits>
 
@@ -67,9 +73,12 @@ bool attn_mfma_supported(const AttnArgs& a) {
 
 struct MfGeom {
     int tpw, chunk_rows, group, max_splits, rc_max;
-    int64_t n_items;  // upper bound on work items
-    size_t counter_bytes, list_bytes, slot_floats, part_bytes;
+    int64_t n_items;   // upper bound on attention work items
+    int64_t n_merge;   // upper bound on merge items (8 rows each)
+    size_t counter_bytes, list_bytes, mlist_bytes, slot_floats, part_bytes;
 };
+
+constexpr int kMergeRows = 8;  // rows per merge item (32 threads of 4 values per row)
 
 static MfGeom mf_geom(const AttnArgs& a) {
     MfGeom g;
@@ -81,17 +90,19 @@ static MfGeom mf_geom(const AttnArgs& a) {
     g.rc_max = (a.max_q * g.group + g.chunk_rows - 1) / g.chunk_rows;
     const int64_t slots = (int64_t)a.R * a.Hkv * g.rc_max;
     g.n_items = slots * g.max_splits;
-    // [0] work counter, [1] number of items, then one merge counter per slot
-    g.counter_bytes = ((size_t)(slots + 2) * sizeof(int) + 255) & ~(size_t)255;
+    g.n_merge = g.max_splits > 1 ? slots * (g.chunk_rows / kMergeRows) : 0;
+    // [0] next item, [1] number of items, [2] number of merge items
+    g.counter_bytes = 256;
     g.list_bytes = ((size_t)g.n_items * 2 * sizeof(int4) + 255) & ~(size_t)255;
+    g.mlist_bytes = ((size_t)g.n_merge * 2 * sizeof(int4) + 255) & ~(size_t)255;
     g.slot_floats = (size_t)g.chunk_rows * (kD + 2);
-    g.part_bytes = (size_t)slots * g.max_splits * g.slot_floats * sizeof(float);
+    g.part_bytes = g.max_splits > 1 ? (size_t)slots * g.max_splits * g.slot_floats * sizeof(float) : 0;
     return g;
 }
 
 size_t attn_mfma_workspace(const AttnArgs& a) {
     const MfGeom g = mf_geom(a);
-    return g.counter_bytes + g.list_bytes + g.part_bytes;
+    return g.counter_bytes + g.list_bytes + g.mlist_bytes + g.part_bytes;
 }
 
 struct MfParams {
@@ -100,61 +111,99 @@ struct MfParams {
     int page_shift;                      // log2(page size)
     uint32_t ks0b, ks1b, ks2b, vs0b, vs1b, vs2b;  // KV strides in bytes
     float scale2;
-    int* work;      // [0] next item, [1] number of items
-    int* counters;  // merge counter per (request, KV head, row chunk)
-    int4* list;     // work items, two int4 each: {r, g, split, row chunk}, {q0, q_len, kv, splits}
-    float* part;
+    int* work;      // [0] next item, [1] number of items, [2] number of merge items
+    int4* list;     // attention items, two int4 each: {r, g, split, row chunk}, {q0, q_len, kv, splits}
+    int4* mlist;    // merge items: {r, g, row chunk, first row in chunk}, {q0, q_len, kv, splits}
+    float* part;    // split partials: [slot][split] {m[rows], l[rows], o[rows][128]}
 };
 
-// Builds the work list on the device from cu_q / kv_len (no host round trip)
-// and clears the counters.  One workgroup; requests are handled in contiguous
-// ranges per thread and placed by an exclusive scan of their item counts.
+// Keys [start, end) of split s of a context of kv keys in ns splits: split
+// bounds are rounded down to whole 32-key steps, the last split ends at kv.
+__host__ __device__ __forceinline__ void split_range(int kv, int ns, int s, int& start, int& end) {
+    start = (int)(((int64_t)s * kv / ns) & ~(int64_t)(kStepTok - 1));
+    end = (s + 1 == ns) ? kv : (int)(((int64_t)(s + 1) * kv / ns) & ~(int64_t)(kStepTok - 1));
+}
+
+// Builds the work lists on the device from cu_q / kv_len (no host round trip).
+// One workgroup.  Attention items are placed longest first (a counting sort on
+// their step count), so that the persistent workgroups end together; merge
+// items list the 8-row groups of every (request, KV head, row chunk) that has
+// more than one split.
 constexpr int kPlanThreads = 1024;
+constexpr int kBins = kSplit / kStepTok + 2;  // steps per item are at most kSplit / 32 + 1
 __global__ __launch_bounds__(kPlanThreads) void mf_plan(MfParams p) {
     const AttnArgs& a = p.a;
-    __shared__ int s_wave[kPlanThreads / 64];
+    __shared__ int s_bin[kBins];
+    __shared__ int s_merge;
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
-    const int nslots = a.R * a.Hkv * p.rc_max;
-    for (int i = tid; i < nslots; i += kPlanThreads) p.counters[i] = 0;
+    for (int i = tid; i < kBins; i += kPlanThreads) s_bin[i] = 0;
+    if (tid == 0) s_merge = 0;
+    __syncthreads();
     const int per = (a.R + kPlanThreads - 1) / kPlanThreads;
     const int r0 = min(a.R, tid * per), r1 = min(a.R, r0 + per);
-    auto items_of = [&](int r, int& nsplit, int& nrc) {
-        const int ql = a.cu_q[r + 1] - a.cu_q[r];
-        const int kv = a.kv_len[r];
-        nsplit = nrc = 0;
-        if (ql < 1 || ql > a.max_q || kv < ql || kv > a.max_pages * a.page) return 0;
-        nsplit = (kv + kSplit - 1) / kSplit;
-        nrc = (ql * p.group + p.chunk_rows - 1) / p.chunk_rows;
-        return a.Hkv * nsplit * nrc;
+    auto shape = [&](int r, int& q0, int& ql, int& kv, int& ns, int& nr) {
+        q0 = a.cu_q[r];
+        ql = a.cu_q[r + 1] - q0;
+        kv = a.kv_len[r];
+        if (ql < 1 || ql > a.max_q || kv < ql || kv > a.max_pages * a.page) return false;
+        ns = (kv + kSplit - 1) / kSplit;
+        nr = (ql * p.group + p.chunk_rows - 1) / p.chunk_rows;
+        return true;
     };
-    int mine = 0;
-    for (int r = r0; r < r1; ++r) { int ns, nr; mine += items_of(r, ns, nr); }
-    int incl = mine;
-    for (int o = 1; o < 64; o <<= 1) {
-        const int t = __shfl_up(incl, o, 64);
-        if (lane >= o) incl += t;
-    }
-    if (lane == 63) s_wave[wave] = incl;
-    __syncthreads();
-    int off = incl - mine;
-    for (int w = 0; w < wave; ++w) off += s_wave[w];
+    auto steps_of = [&](int kv, int ns, int sp) {
+        int st, en;
+        split_range(kv, ns, sp, st, en);
+        return min((en - st + kStepTok - 1) / kStepTok, kBins - 1);
+    };
+    // histogram of item lengths
     for (int r = r0; r < r1; ++r) {
-        int ns, nr;
-        if (!items_of(r, ns, nr)) continue;
-        // row chunks of one split next to each other (they re-read the same keys)
-        for (int g = 0; g < a.Hkv; ++g)
-            for (int sp = 0; sp < ns; ++sp)
-                for (int rc = 0; rc < nr; ++rc) {
-                    p.list[2 * off] = int4{r, g, sp, rc};
-                    p.list[2 * off + 1] = int4{a.cu_q[r], a.cu_q[r + 1] - a.cu_q[r], a.kv_len[r], ns};
-                    ++off;
-                }
+        int q0, ql, kv, ns, nr;
+        if (!shape(r, q0, ql, kv, ns, nr)) continue;
+        for (int sp = 0; sp < ns; ++sp) atomicAdd(&s_bin[steps_of(kv, ns, sp)], a.Hkv * nr);
     }
-    if (tid == kPlanThreads - 1) {
+    __syncthreads();
+    if (tid == 0) {  // bin start offsets, longest first
+        int off = 0;
+        for (int b = kBins - 1; b >= 0; --b) {
+            const int c = s_bin[b];
+            s_bin[b] = off;
+            off += c;
+        }
         p.work[0] = 0;
-        p.work[1] = off;  // the last thread ends at the total
+        p.work[1] = off;
     }
+    __syncthreads();
+    for (int r = r0; r < r1; ++r) {
+        int q0, ql, kv, ns, nr;
+        if (!shape(r, q0, ql, kv, ns, nr)) continue;
+        const int4 meta = int4{q0, ql, kv, ns};
+        for (int sp = 0; sp < ns; ++sp) {
+            // the KV heads and row chunks of one split stay next to each other
+            int off = atomicAdd(&s_bin[steps_of(kv, ns, sp)], a.Hkv * nr);
+            for (int g = 0; g < a.Hkv; ++g)
+                for (int rc = 0; rc < nr; ++rc, ++off) {
+                    p.list[2 * off] = int4{r, g, sp, rc};
+                    p.list[2 * off + 1] = meta;
+                }
+        }
+        if (ns > 1) {
+            const int rows = ql * p.group;
+            int cnt = 0;
+            for (int rc = 0; rc < nr; ++rc)
+                cnt += (min(p.chunk_rows, rows - rc * p.chunk_rows) + kMergeRows - 1) / kMergeRows;
+            int off = atomicAdd(&s_merge, a.Hkv * cnt);
+            for (int g = 0; g < a.Hkv; ++g)
+                for (int rc = 0; rc < nr; ++rc) {
+                    const int nrows = min(p.chunk_rows, rows - rc * p.chunk_rows);
+                    for (int m0 = 0; m0 < nrows; m0 += kMergeRows, ++off) {
+                        p.mlist[2 * off] = int4{r, g, rc, m0};
+                        p.mlist[2 * off + 1] = meta;
+                    }
+                }
+        }
+    }
+    __syncthreads();
+    if (tid == 0) p.work[2] = s_merge;
 }
 
 __device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
@@ -226,38 +275,12 @@ __device__ __forceinline__ void lds_copy16_s(uint64_t sbase, uint32_t voff, uint
         : "memory", "m0");
 }
 
-// Split partials are exchanged between workgroups that may run on different
-// XCDs (each with its own L2).  They are written and read with relaxed
-// device-scope atomic accesses, which are coherent across XCDs per location;
-// the writer waits for its stores to complete before it bumps the merge
-// counter.  (A device-scope fence would write back and invalidate the whole L2
-// of the XCD instead.)
-__device__ __forceinline__ void st_agent(float* p, float v) {
-    __hip_atomic_store((uint32_t*)p, __float_as_uint(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void st_agent4(float* p, f32x4 v) {  // p 16-byte aligned
-    const u32x4 u = __builtin_bit_cast(u32x4, v);
-    __hip_atomic_store((uint64_t*)p, (uint64_t)u[0] | ((uint64_t)u[1] << 32), __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store((uint64_t*)p + 1, (uint64_t)u[2] | ((uint64_t)u[3] << 32), __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float ld_agent(const float* p) {
-    return __uint_as_float(__hip_atomic_load((const uint32_t*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-}
-__device__ __forceinline__ f32x4 ld_agent4(const float* p) {
-    const uint64_t a = __hip_atomic_load((const uint64_t*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const uint64_t b = __hip_atomic_load((const uint64_t*)p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return __builtin_bit_cast(f32x4, u32x4{(uint32_t)a, (uint32_t)(a >> 32), (uint32_t)b, (uint32_t)(b >> 32)});
-}
-
 constexpr float kRescale = 8.0f;  // log2 headroom before the running max is moved
 
 template <int TPW>
 __device__ __forceinline__ void attn_item(const MfParams& p, const int r, const int g, const int s,
                                           const int rc, const int q0, const int ql, const int kv,
-                                          const int nsplit, const uint32_t lds0,
-                                          int& s_last) {
+                                          const int nsplit, const uint32_t lds0) {
     const AttnArgs& a = p.a;
     constexpr int kChunkRows = 16 * kMfWaves * TPW;
     constexpr int kSlotFloats = kChunkRows * (kD + 2);
@@ -266,10 +289,8 @@ __device__ __forceinline__ void attn_item(const MfParams& p, const int r, const 
     // s < nsplit, rc * kChunkRows < ql * group
     const int rows = ql * p.group;
     const int row0 = rc * kChunkRows;
-    const int start = (int)(((int64_t)s * kv / nsplit) & ~(int64_t)(kStepTok - 1));
-    const int end = (s + 1 == nsplit)
-                        ? kv
-                        : (int)(((int64_t)(s + 1) * kv / nsplit) & ~(int64_t)(kStepTok - 1));
+    int start, end;
+    split_range(kv, nsplit, s, start, end);
     const int nrows = min(kChunkRows, rows - row0);
     const int nt = (nrows + 15) >> 4;
 
@@ -484,18 +505,18 @@ __device__ __forceinline__ void attn_item(const MfParams& p, const int r, const 
     };
 
     // ---- main loop.  Every thread issues kCopiesPerStep copies per step, in step
-    // order, also past the last step (re-reading the last one into a buffer that
-    // is not read again), so "step n has landed" is always
+    // order, also past the last step (copies of the zero row into buffers that
+    // are not read again), so "step n has landed" is always
     // vmcnt <= (kRing - 2) * kCopiesPerStep.  Keys past the split end are copied
     // as zeros (masked scores, zero values).  The loop is unrolled by the ring
     // size so that every LDS address is a per-lane base plus an immediate.
     wait_vmcnt<0>();
 #pragma unroll
-    for (int n = 0; n < kRing - 1; ++n) issue(min(n, last));
+    for (int n = 0; n < kRing - 1; ++n) issue(n);
     auto one = [&](int n, auto bufc) {
         wait_vmcnt<(kRing - 2) * kCopiesPerStep>();
         lds_barrier();  // step n visible to all; everyone is done with step n - 1
-        issue(min(n + kRing - 1, last));
+        issue(n + kRing - 1);
         if (nt_w > 0) compute(n, bufc);
     };
     for (int n = 0; n < nsteps; n += kRing) {
@@ -535,75 +556,21 @@ __device__ __forceinline__ void attn_item(const MfParams& p, const int r, const 
         return;
     }
 
-    // ---- several splits: publish this split's partial, the last one merges
-    const int64_t slot_base = ((int64_t)rg * p.rc_max + rc) * p.max_splits;
-    {
-        float* part = p.part + (slot_base + s) * kSlotFloats;
+    // ---- several splits: store this split's partial (m, l, unnormalised o);
+    // the merge kernel combines them after this kernel has ended
+    float* part = p.part + (((int64_t)rg * p.rc_max + rc) * p.max_splits + s) * kSlotFloats;
 #pragma unroll
-        for (int j = 0; j < TPW; ++j) {
-            const int rr = 16 * (wave + kMfWaves * j) + lr;
-            if (j < nt_w) {
-                if (lq == 0) {
-                    st_agent(part + rr, mrow[j]);
-                    st_agent(part + kChunkRows + rr, lsum[j]);
-                }
-#pragma unroll
-                for (int db = 0; db < 8; ++db)
-                    st_agent4(part + 2 * kChunkRows + rr * kD + 16 * db + 4 * lq, acc[j][db]);
+    for (int j = 0; j < TPW; ++j) {
+        const int rr = 16 * (wave + kMfWaves * j) + lr;
+        if (j < nt_w) {
+            if (lq == 0) {
+                part[rr] = mrow[j];
+                part[kChunkRows + rr] = lsum[j];
             }
-        }
-        // the stores are complete (at the device coherence point) before the count
-        wait_vmcnt<0>();
-    }
-    __syncthreads();
-    if (tid == 0) {
-        const int prev = __hip_atomic_fetch_add(p.counters + (int64_t)rg * p.rc_max + rc, 1,
-                                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        s_last = prev == nsplit - 1;
-    }
-    __syncthreads();
-    if (!s_last) return;
-    constexpr int kTPR = kMfThreads / kChunkRows;  // threads per row
-    constexpr int kDPT = kD / kTPR;                // d values per thread
-    const int mr = tid / kTPR;
-    const int dq = (tid % kTPR) * kDPT;
-    if (mr < nrows) {
-        const float* base = p.part + slot_base * kSlotFloats;
-        float M = -__builtin_huge_valf();
-        for (int sp = 0; sp < nsplit; ++sp) M = fmaxf(M, ld_agent(base + sp * kSlotFloats + mr));
-        float L = 0.0f;
-        float o[kDPT];
 #pragma unroll
-        for (int k = 0; k < kDPT; ++k) o[k] = 0.0f;
-        for (int sp = 0; sp < nsplit; ++sp) {
-            const float* sl = base + sp * kSlotFloats;
-            const float ms = ld_agent(sl + mr);
-            if (!(ms > -__builtin_huge_valf())) continue;
-            const float f = exp2f(ms - M);
-            L += ld_agent(sl + kChunkRows + mr) * f;
-            const float* src = sl + 2 * kChunkRows + mr * kD + dq;
-#pragma unroll
-            for (int k = 0; k < kDPT / 4; ++k) {
-                const f32x4 v = ld_agent4(src + 4 * k);
-                o[4 * k + 0] += v[0] * f;
-                o[4 * k + 1] += v[1] * f;
-                o[4 * k + 2] += v[2] * f;
-                o[4 * k + 3] += v[3] * f;
-            }
+            for (int db = 0; db < 8; ++db)
+                *(f32x4*)(part + 2 * kChunkRows + rr * kD + 16 * db + 4 * lq) = acc[j][db];
         }
-        const int row = row0 + mr;
-        const int t = row / p.group;
-        const int h = g * p.group + (row - t * p.group);
-        const int64_t orow = (int64_t)(q0 + t) * a.Hq + h;
-        const float inv = 1.0f / L;
-#pragma unroll
-        for (int k = 0; k < kDPT / 4; ++k) {
-            uint2 pk;
-            pk.x = pack2_bf16(o[4 * k] * inv, o[4 * k + 1] * inv);
-            pk.y = pack2_bf16(o[4 * k + 2] * inv, o[4 * k + 3] * inv);
-            *(uint2*)(outp + orow * kD + dq + 4 * k) = pk;
-        }
-        if (a.lse && dq == 0) a.lse[orow] = (M + log2f(L)) * kLn2;
     }
 }
 
@@ -612,7 +579,6 @@ template <int TPW>
 __global__ __launch_bounds__(kMfThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_mfma_kernel(MfParams p) {
     __shared__ __align__(16) unsigned char lds[kRing][2][kTileBytes];  // [buffer][K | V]
-    __shared__ int s_last;
     __shared__ int s_item;
     // the ring's LDS address as a plain integer (all LDS addressing below is
     // integer arithmetic on it)
@@ -628,11 +594,57 @@ void attn_mfma_kernel(MfParams p) {
         // take the next item now; its index is needed only at the end
         int nxt = 0;
         if (threadIdx.x == 0) nxt = atomicAdd(p.work, 1);
-        attn_item<TPW>(p, e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w, lds0, s_last);
+        attn_item<TPW>(p, e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w, lds0);
         __syncthreads();  // everyone is done with this item's LDS and s_item
         if (threadIdx.x == 0) s_item = nxt;
         __syncthreads();
         it = __builtin_amdgcn_readfirstlane(s_item);
+    }
+}
+
+// Combines the split partials of one 8-row group: 32 threads per row, four
+// values each.  Splits are taken in index order (bitwise reproducible).
+template <int TPW>
+__global__ __launch_bounds__(256) void attn_mfma_merge(MfParams p) {
+    constexpr int kChunkRows = 16 * kMfWaves * TPW;
+    constexpr int kSlotFloats = kChunkRows * (kD + 2);
+    const AttnArgs& a = p.a;
+    const int count = p.work[2];
+    const int tid = threadIdx.x;
+    for (int m = blockIdx.x; m < count; m += gridDim.x) {
+        const int4 e0 = p.mlist[2 * m];
+        const int4 e1 = p.mlist[2 * m + 1];
+        const int r = e0.x, g = e0.y, rc = e0.z;
+        const int q0 = e1.x, ql = e1.y, ns = e1.w;
+        const int rows = ql * p.group;
+        const int nrows = min(kChunkRows, rows - rc * kChunkRows);
+        const int mr = e0.w + (tid >> 5);  // row inside the chunk
+        if (mr >= nrows) continue;
+        const int c4 = (tid & 31) * 4;
+        const float* base = p.part + ((int64_t)(r * a.Hkv + g) * p.rc_max + rc) * p.max_splits * kSlotFloats;
+        float M = -__builtin_huge_valf();
+#pragma unroll 4
+        for (int sp = 0; sp < ns; ++sp) M = fmaxf(M, base[(int64_t)sp * kSlotFloats + mr]);
+        float L = 0.0f;
+        f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+        for (int sp = 0; sp < ns; ++sp) {
+            const float* sl = base + (int64_t)sp * kSlotFloats;
+            const float ms = sl[mr];
+            const float f = ms > -__builtin_huge_valf() ? exp2f(ms - M) : 0.0f;
+            L += sl[kChunkRows + mr] * f;
+            o += f * *(const f32x4*)(sl + 2 * kChunkRows + mr * kD + c4);
+        }
+        const int row = rc * kChunkRows + mr;
+        const int t = row / p.group;
+        const int h = g * p.group + (row - t * p.group);
+        const int64_t orow = (int64_t)(q0 + t) * a.Hq + h;
+        const float inv = 1.0f / L;
+        uint2 pk;
+        pk.x = pack2_bf16(o[0] * inv, o[1] * inv);
+        pk.y = pack2_bf16(o[2] * inv, o[3] * inv);
+        *(uint2*)((uint16_t*)a.out + orow * kD + c4) = pk;
+        if (a.lse && c4 == 0) a.lse[orow] = (M + log2f(L)) * kLn2;
     }
 }
 
@@ -653,9 +665,9 @@ hipError_t launch_attn_mfma(const AttnArgs& a, void* ws, hipStream_t s) {
     p.vs1b = (uint32_t)(a.vs[1] * 2);
     p.vs2b = (uint32_t)(a.vs[2] * 2);
     p.work = (int*)ws;
-    p.counters = p.work + 2;
     p.list = (int4*)((char*)ws + g.counter_bytes);
-    p.part = (float*)((char*)ws + g.counter_bytes + g.list_bytes);
+    p.mlist = (int4*)((char*)ws + g.counter_bytes + g.list_bytes);
+    p.part = (float*)((char*)ws + g.counter_bytes + g.list_bytes + g.mlist_bytes);
     hipLaunchKernelGGL(mf_plan, dim3(1), dim3(kPlanThreads), 0, s, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -669,6 +681,13 @@ hipError_t launch_attn_mfma(const AttnArgs& a, void* ws, hipStream_t s) {
         hipLaunchKernelGGL(attn_mfma_kernel<2>, dim3((unsigned)grid), dim3(kMfThreads), 0, s, p);
     else
         hipLaunchKernelGGL(attn_mfma_kernel<1>, dim3((unsigned)grid), dim3(kMfThreads), 0, s, p);
+    e = hipGetLastError();
+    if (e != hipSuccess || g.n_merge == 0) return e;
+    const int64_t mgrid = std::min<int64_t>((int64_t)cus * 8, g.n_merge);
+    if (g.tpw == 2)
+        hipLaunchKernelGGL(attn_mfma_merge<2>, dim3((unsigned)mgrid), dim3(256), 0, s, p);
+    else
+        hipLaunchKernelGGL(attn_mfma_merge<1>, dim3((unsigned)mgrid), dim3(256), 0, s, p);
     return hipGetLastError();
 }
 
