@@ -33,6 +33,7 @@ constexpr int kWaves = kBlk / kLanes;
 constexpr int kLanePer = kChunk / kLanes;      // 64 entries per lane and chunk
 constexpr int kThreadPer = kChunk / kBlk;      // 16 entries per thread (draw)
 constexpr int kMaxChunks = 256;                // V <= 2^20
+static_assert(kMaxChunks <= kBlk, "the draw loads one chunk mass per thread");
 constexpr float kLog2e = 1.4426950408889634f;
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -343,14 +344,18 @@ __global__ __launch_bounds__(kBlk) void acc_resolve(
     int32_t* __restrict__ accepted_len, int32_t* __restrict__ next_tok) {
     __shared__ int s_rej[65];
     __shared__ int s_arg[65];
+    __shared__ int s_tok[64];
     __shared__ float s_M[65], s_S[65];
     const int r = blockIdx.x;
     const int tid = threadIdx.x;
     const int lane = tid & (kLanes - 1);
     const int wave = tid / kLanes;
     const int nch = n_chunks(V);
+    // the drafts are loaded together with the request's row range
+    if (tid < K) s_tok[tid] = draft_tok[(int64_t)r * K + tid];
     const int row0 = cu_q[r];
     const int l = cu_q[r + 1] - row0 - 1;
+    __syncthreads();
     if (l < 0 || l > K || row0 < 0 || (int64_t)row0 + l + 1 > (int64_t)R * (K + 1)) {
         if (tid == 0) {
             accepted_len[r] = -1;
@@ -362,29 +367,36 @@ __global__ __launch_bounds__(kBlk) void acc_resolve(
     const size_t esz = BF16 ? 2 : 4;
     for (int t = wave; t <= l; t += kWaves) {
         const int64_t row = row0 + t;
+        // the tested draft's target logit, draft probability and uniform are
+        // loaded together with the chunk statistics
+        const int x = t < l ? s_tok[t] : -1;
+        const bool test = !GREEDY && lane == 0 && t < l && x >= 0 && x < V;
+        float y = 0.0f, pd = 0.0f, uu = 0.0f;
+        if (test) {
+            const void* rp = (const char*)logits + (size_t)row * (size_t)ld * esz;
+            y = load_logit<BF16>(rp, x) * scale2;
+            pd = draft_p[((int64_t)r * K + t) * V + x];
+            uu = u[(int64_t)r * (K + 1) + t];
+        }
         float A, B;
         int arg;
         row_stats<GREEDY>(stats + row * nch, nch, A, B, arg);
         if (lane == 0) {
             int rej = 0;
             if (GREEDY) {
-                if (t < l) rej = draft_tok[(int64_t)r * K + t] != arg;
+                if (t < l) rej = x != arg;
                 s_arg[t] = arg;
             } else {
                 rows[row] = RowInfo{A, B, r, t};
                 s_M[t] = A;
                 s_S[t] = B;
                 if (t < l) {
-                    const int x = draft_tok[(int64_t)r * K + t];
-                    if (x < 0 || x >= V) {
-                        rej = 1;
+                    if (!test) {
+                        rej = 1;  // draft token outside the vocabulary
                     } else {
-                        const void* rp = (const char*)logits + (size_t)row * (size_t)ld * esz;
-                        const float y = load_logit<BF16>(rp, x) * scale2;
                         const float pt = exp2f(y - A) / B;
-                        const float pd = draft_p[((int64_t)r * K + t) * V + x];
                         const float ratio = pd > 0.0f ? pt / pd : __builtin_huge_valf();
-                        rej = !(u[(int64_t)r * (K + 1) + t] < ratio);
+                        rej = !(uu < ratio);
                     }
                 }
             }
@@ -473,16 +485,17 @@ __global__ __launch_bounds__(kBlk) void acc_draw(
     const int lane = tid & (kLanes - 1);
     const int wave = tid / kLanes;
     const int nch = n_chunks(V);
+    // the residual chunk masses (nch <= kBlk) and u are loaded together with
+    // the draw record
+    const double mw = tid < nch ? mass[(int64_t)r * nch + tid] : 0.0;
+    const double uu = (double)u[(int64_t)r * (K + 1) + K];
     const DrawInfo d = draw[r];
     if (d.kind == 0) return;
     const ChunkStat* st = stats + (int64_t)d.row * nch;
-    const double uu = (double)u[(int64_t)r * (K + 1) + K];
     // chunk masses, in the units of the entry masses used below
     int kind = d.kind;
     if (kind == 2) {
-        double t = 0.0;
-        for (int c = tid; c < nch; c += kBlk) t += mass[(int64_t)r * nch + c];
-        t = wave_sum_f64(t);
+        double t = wave_sum_f64(mw);
         if (lane == 0) s_scan[wave] = t;
         __syncthreads();
         double tot = 0.0;
@@ -490,11 +503,13 @@ __global__ __launch_bounds__(kBlk) void acc_draw(
         if (!(tot > 0.0)) kind = 1;  // empty residual: draw from the target row
         __syncthreads();
     }
-    for (int c = tid; c < nch; c += kBlk) {
-        const ChunkStat x = st[c];
-        s_w[c] = kind == 2 ? mass[(int64_t)r * nch + c]
-                           : (x.a > -__builtin_huge_valf()
-                                  ? (double)x.b * (double)exp2f(x.a - d.M) : 0.0);
+    if (tid < nch) {
+        if (kind == 2) {
+            s_w[tid] = mw;
+        } else {
+            const ChunkStat x = st[tid];
+            s_w[tid] = x.a > -__builtin_huge_valf() ? (double)x.b * (double)exp2f(x.a - d.M) : 0.0;
+        }
     }
     __syncthreads();
     if (wave == 0) {

@@ -45,7 +45,7 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kMfThreads = 256;
 constexpr int kMfWaves = 4;
-constexpr int kSplit = 2048;   // keys per split (upper bound, before rounding)
+constexpr int kSplit = 2048;   // keys per split (the last split of a context holds the rest)
 constexpr int kStepTok = 32;   // keys per step
 constexpr int kRing = 4;       // LDS buffers; copies run kRing - 1 steps ahead
 constexpr int kD = 128;
@@ -117,30 +117,37 @@ struct MfParams {
     float* part;    // split partials: [slot][split] {m[rows], l[rows], o[rows][128]}
 };
 
-// Keys [start, end) of split s of a context of kv keys in ns splits: split
-// bounds are rounded down to whole 32-key steps, the last split ends at kv.
+// Keys [start, end) of split s of a context of kv keys: whole kSplit-key
+// pieces, the last one holding the remainder.  The remainders spread item
+// lengths down to a single step, so the longest-first list ends with short
+// items and the persistent workgroups finish close together.
 __host__ __device__ __forceinline__ void split_range(int kv, int ns, int s, int& start, int& end) {
-    start = (int)(((int64_t)s * kv / ns) & ~(int64_t)(kStepTok - 1));
-    end = (s + 1 == ns) ? kv : (int)(((int64_t)(s + 1) * kv / ns) & ~(int64_t)(kStepTok - 1));
+    (void)ns;
+    start = s * kSplit;
+    end = min(kv, start + kSplit);
 }
 
 // Builds the work lists on the device from cu_q / kv_len (no host round trip).
-// One workgroup.  Attention items are placed longest first (a counting sort on
-// their step count), so that the persistent workgroups end together; merge
-// items list the 8-row groups of every (request, KV head, row chunk) that has
-// more than one split.
+// One workgroup; eight threads per request (one per KV head, in turn).
+// Attention items are placed longest first (a counting sort on their step
+// count), so that the persistent workgroups end together; merge items list the
+// 8-row groups of every (request, KV head, row chunk) that has more than one
+// split.
 constexpr int kPlanThreads = 1024;
+constexpr int kPlanLanes = 8;                 // threads per request
 constexpr int kBins = kSplit / kStepTok + 2;  // steps per item are at most kSplit / 32 + 1
+static_assert(kBins <= 2 * DSPARK_WAVE, "bin scan covers two bins per lane");
 __global__ __launch_bounds__(kPlanThreads) void mf_plan(MfParams p) {
     const AttnArgs& a = p.a;
     __shared__ int s_bin[kBins];
     __shared__ int s_merge;
     const int tid = threadIdx.x;
+    const int lane = tid & (DSPARK_WAVE - 1);
+    const int sub = tid % kPlanLanes;
+    const int leader = lane & ~(kPlanLanes - 1);  // the request's first lane
     for (int i = tid; i < kBins; i += kPlanThreads) s_bin[i] = 0;
     if (tid == 0) s_merge = 0;
     __syncthreads();
-    const int per = (a.R + kPlanThreads - 1) / kPlanThreads;
-    const int r0 = min(a.R, tid * per), r1 = min(a.R, r0 + per);
     auto shape = [&](int r, int& q0, int& ql, int& kv, int& ns, int& nr) {
         q0 = a.cu_q[r];
         ql = a.cu_q[r + 1] - q0;
@@ -155,44 +162,56 @@ __global__ __launch_bounds__(kPlanThreads) void mf_plan(MfParams p) {
         split_range(kv, ns, sp, st, en);
         return min((en - st + kStepTok - 1) / kStepTok, kBins - 1);
     };
-    // histogram of item lengths
-    for (int r = r0; r < r1; ++r) {
+    // histogram of item lengths (the request's lanes share its splits)
+    for (int r = tid / kPlanLanes; r < a.R; r += kPlanThreads / kPlanLanes) {
         int q0, ql, kv, ns, nr;
         if (!shape(r, q0, ql, kv, ns, nr)) continue;
-        for (int sp = 0; sp < ns; ++sp) atomicAdd(&s_bin[steps_of(kv, ns, sp)], a.Hkv * nr);
+        for (int sp = sub; sp < ns; sp += kPlanLanes) atomicAdd(&s_bin[steps_of(kv, ns, sp)], a.Hkv * nr);
     }
     __syncthreads();
-    if (tid == 0) {  // bin start offsets, longest first
-        int off = 0;
-        for (int b = kBins - 1; b >= 0; --b) {
-            const int c = s_bin[b];
-            s_bin[b] = off;
-            off += c;
+    if (tid < DSPARK_WAVE) {  // bin start offsets, longest first: lane l owns bins kBins-1-2l, kBins-2-2l
+        const int b0 = kBins - 1 - 2 * lane, b1 = b0 - 1;
+        const int c0 = b0 >= 0 ? s_bin[b0] : 0, c1 = b1 >= 0 ? s_bin[b1] : 0;
+        int incl = c0 + c1;
+        for (int o = 1; o < DSPARK_WAVE; o <<= 1) {
+            const int t = __shfl_up(incl, o, DSPARK_WAVE);
+            if (lane >= o) incl += t;
         }
-        p.work[0] = 0;
-        p.work[1] = off;
+        const int excl = incl - c0 - c1;
+        if (b0 >= 0) s_bin[b0] = excl;
+        if (b1 >= 0) s_bin[b1] = excl + c0;
+        if (lane == DSPARK_WAVE - 1) {
+            p.work[0] = 0;
+            p.work[1] = incl;
+        }
     }
     __syncthreads();
-    for (int r = r0; r < r1; ++r) {
+    for (int r = tid / kPlanLanes; r < a.R; r += kPlanThreads / kPlanLanes) {
         int q0, ql, kv, ns, nr;
-        if (!shape(r, q0, ql, kv, ns, nr)) continue;
+        if (!shape(r, q0, ql, kv, ns, nr)) continue;  // the same for the request's lanes
         const int4 meta = int4{q0, ql, kv, ns};
         for (int sp = 0; sp < ns; ++sp) {
             // the KV heads and row chunks of one split stay next to each other
-            int off = atomicAdd(&s_bin[steps_of(kv, ns, sp)], a.Hkv * nr);
-            for (int g = 0; g < a.Hkv; ++g)
-                for (int rc = 0; rc < nr; ++rc, ++off) {
+            int base = 0;
+            if (sub == 0) base = atomicAdd(&s_bin[steps_of(kv, ns, sp)], a.Hkv * nr);
+            base = __shfl(base, leader, DSPARK_WAVE);
+            for (int g = sub; g < a.Hkv; g += kPlanLanes)
+                for (int rc = 0; rc < nr; ++rc) {
+                    const int off = base + g * nr + rc;
                     p.list[2 * off] = int4{r, g, sp, rc};
                     p.list[2 * off + 1] = meta;
                 }
         }
         if (ns > 1) {
             const int rows = ql * p.group;
-            int cnt = 0;
+            int cnt = 0;  // merge groups per KV head
             for (int rc = 0; rc < nr; ++rc)
                 cnt += (min(p.chunk_rows, rows - rc * p.chunk_rows) + kMergeRows - 1) / kMergeRows;
-            int off = atomicAdd(&s_merge, a.Hkv * cnt);
-            for (int g = 0; g < a.Hkv; ++g)
+            int base = 0;
+            if (sub == 0) base = atomicAdd(&s_merge, a.Hkv * cnt);
+            base = __shfl(base, leader, DSPARK_WAVE);
+            for (int g = sub; g < a.Hkv; g += kPlanLanes) {
+                int off = base + g * cnt;
                 for (int rc = 0; rc < nr; ++rc) {
                     const int nrows = min(p.chunk_rows, rows - rc * p.chunk_rows);
                     for (int m0 = 0; m0 < nrows; m0 += kMergeRows, ++off) {
@@ -200,6 +219,7 @@ __global__ __launch_bounds__(kPlanThreads) void mf_plan(MfParams p) {
                         p.mlist[2 * off + 1] = meta;
                     }
                 }
+            }
         }
     }
     __syncthreads();
@@ -603,7 +623,10 @@ void attn_mfma_kernel(MfParams p) {
 }
 
 // Combines the split partials of one 8-row group: 32 threads per row, four
-// values each.  Splits are taken in index order (bitwise reproducible).
+// values each.  The partials of up to kMergeBatch splits are loaded in one
+// round (o does not depend on the row max), then combined in split order
+// (bitwise reproducible).
+constexpr int kMergeBatch = 8;
 template <int TPW>
 __global__ __launch_bounds__(256) void attn_mfma_merge(MfParams p) {
     constexpr int kChunkRows = 16 * kMfWaves * TPW;
@@ -623,17 +646,36 @@ __global__ __launch_bounds__(256) void attn_mfma_merge(MfParams p) {
         const int c4 = (tid & 31) * 4;
         const float* base = p.part + ((int64_t)(r * a.Hkv + g) * p.rc_max + rc) * p.max_splits * kSlotFloats;
         float M = -__builtin_huge_valf();
-#pragma unroll 4
-        for (int sp = 0; sp < ns; ++sp) M = fmaxf(M, base[(int64_t)sp * kSlotFloats + mr]);
         float L = 0.0f;
         f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-        for (int sp = 0; sp < ns; ++sp) {
-            const float* sl = base + (int64_t)sp * kSlotFloats;
-            const float ms = sl[mr];
-            const float f = ms > -__builtin_huge_valf() ? exp2f(ms - M) : 0.0f;
-            L += sl[kChunkRows + mr] * f;
-            o += f * *(const f32x4*)(sl + 2 * kChunkRows + mr * kD + c4);
+        for (int s0 = 0; s0 < ns; s0 += kMergeBatch) {
+            float ms[kMergeBatch], ls[kMergeBatch];
+            f32x4 os[kMergeBatch];
+#pragma unroll
+            for (int k = 0; k < kMergeBatch; ++k) {
+                const float* sl = base + (int64_t)min(s0 + k, ns - 1) * kSlotFloats;
+                ms[k] = sl[mr];
+                ls[k] = sl[kChunkRows + mr];
+                os[k] = *(const f32x4*)(sl + 2 * kChunkRows + mr * kD + c4);
+            }
+            float Mb = M;
+#pragma unroll
+            for (int k = 0; k < kMergeBatch; ++k)
+                if (s0 + k < ns) Mb = fmaxf(Mb, ms[k]);
+            // rescale what earlier batches accumulated (one batch when ns <= 8)
+            if (M > -__builtin_huge_valf() && Mb != M) {
+                const float f = exp2f(M - Mb);
+                L *= f;
+                o *= f;
+            }
+            M = Mb;
+#pragma unroll
+            for (int k = 0; k < kMergeBatch; ++k) {
+                if (s0 + k >= ns) break;
+                const float f = ms[k] > -__builtin_huge_valf() ? exp2f(ms[k] - M) : 0.0f;
+                L += ls[k] * f;
+                o += f * os[k];
+            }
         }
         const int row = rc * kChunkRows + mr;
         const int t = row / p.group;
@@ -683,7 +725,7 @@ hipError_t launch_attn_mfma(const AttnArgs& a, void* ws, hipStream_t s) {
         hipLaunchKernelGGL(attn_mfma_kernel<1>, dim3((unsigned)grid), dim3(kMfThreads), 0, s, p);
     e = hipGetLastError();
     if (e != hipSuccess || g.n_merge == 0) return e;
-    const int64_t mgrid = std::min<int64_t>((int64_t)cus * 8, g.n_merge);
+    const int64_t mgrid = std::min<int64_t>((int64_t)cus * 16, g.n_merge);
     if (g.tpw == 2)
         hipLaunchKernelGGL(attn_mfma_merge<2>, dim3((unsigned)mgrid), dim3(256), 0, s, p);
     else

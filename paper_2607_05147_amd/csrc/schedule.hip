@@ -4,9 +4,12 @@
 // Steps, all on the device so the verification step needs no host round trip:
 //   1. survival a[r][j] = prod_{i<=j} c[r][i] (fp64, multiplied in increasing j;
 //      the same sequence of roundings on every implementation);
-//   2. bitonic sort of the R*K candidates in LDS, descending a, ties by (r, j):
-//      the key is the bit pattern of a (non-negative doubles order like their
-//      bits) plus the flat index r*K + j;
+//   2. bitonic sort of the R*K candidates, descending a, ties by (r, j): the
+//      key is the bit pattern of a (non-negative doubles order like their
+//      bits) plus the flat index r*K + j.  Each thread keeps E = N/1024
+//      consecutive keys in registers: partners closer than E are swapped in
+//      registers, partners in the same wave through lane shuffles, and only
+//      partners in other waves go through LDS (with barriers);
 //   3. block-wide fp64 inclusive scan of the sorted a: tau_n = R + sum_{m<=n} a_m;
 //   4. Theta_n = tau_n * SPS(R + n + 1); mode 0 stops at the first n whose Theta
 //      does not exceed its predecessor's (Theta_{-1} = R * SPS(R)), mode 1 takes
@@ -47,6 +50,36 @@ __device__ __forceinline__ double sched_conf(float c) {
     return (double)c;
 }
 
+// A sort element: the survival probability's bits (hi, lo) and the flat index.
+struct SKey {
+    uint32_t hi, lo;
+    int idx;
+};
+
+// "x comes before y": larger a first, equal a by smaller flat index
+__device__ __forceinline__ bool before(const SKey& x, const SKey& y) {
+    if (x.hi != y.hi) return x.hi > y.hi;
+    if (x.lo != y.lo) return x.lo > y.lo;
+    return x.idx < y.idx;
+}
+
+// compare-exchange of the pair (e, e ^ J) inside a thread, for every e with bit
+// J clear; i0 is the thread's first flat position
+template <int E, int J>
+__device__ __forceinline__ void sort_in_thread(SKey (&v)[E], int i0, int k) {
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        if (e & J) continue;
+        const bool up = ((i0 + e) & k) == 0;
+        if (before(v[e ^ J], v[e]) == up) {
+            const SKey t = v[e];
+            v[e] = v[e ^ J];
+            v[e ^ J] = t;
+        }
+    }
+}
+
+template <int E>
 __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
     const float* __restrict__ conf, int R, int K, const double* __restrict__ sps, int mode,
     int Np, int32_t* __restrict__ len_out, int32_t* __restrict__ cu_q,
@@ -69,10 +102,16 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
     const int lane = tid & (DSPARK_WAVE - 1);
     const int wave = tid / DSPARK_WAVE;
     const int N = R * K;
+    const int i0 = tid * E;  // this thread's sorted positions i0 .. i0 + E - 1
+
+    // the throughput table at the positions this thread will examine (sorted
+    // position n needs SPS(R + n) and SPS(R + n + 1)), loaded while sorting
+    double spsv[E + 1];
+#pragma unroll
+    for (int e = 0; e <= E; ++e) spsv[e] = (i0 + e <= N) ? sps[R + i0 + e] : 0.0;
+    const double sps_r = sps[R];
 
     if (tid == 0) s_ncand = 0;
-    __syncthreads();
-
     // 1. survival products, one request per thread; the confidences are first
     // staged in LDS with coalesced loads
     for (int i = tid; i < N; i += kSchedThreads) confl[i] = conf[i];
@@ -80,11 +119,18 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
     int my_cand = 0;
     for (int r = tid; r < R; r += kSchedThreads) {
         double p = 1.0;
-        for (int j = 0; j < K; ++j) {
-            p = p * sched_conf(confl[r * K + j]);
-            key[r * K + j] = (uint64_t)__double_as_longlong(p);
-            idx[r * K + j] = (uint16_t)(r * K + j);
-            my_cand += p > 0.0;
+        for (int j0 = 0; j0 < K; j0 += 16) {
+            float c[16];
+#pragma unroll
+            for (int jj = 0; jj < 16; ++jj) c[jj] = j0 + jj < K ? confl[r * K + j0 + jj] : 1.0f;
+#pragma unroll
+            for (int jj = 0; jj < 16; ++jj) {
+                if (j0 + jj >= K) break;
+                p = p * sched_conf(c[jj]);
+                key[r * K + j0 + jj] = (uint64_t)__double_as_longlong(p);
+                idx[r * K + j0 + jj] = (uint16_t)(r * K + j0 + jj);
+                my_cand += p > 0.0;
+            }
         }
         lenl[r] = 0;
     }
@@ -95,40 +141,77 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
     if (my_cand) atomicAdd(&s_ncand, my_cand);
     __syncthreads();
 
-    // 2. bitonic sort: "x before y" iff key_x > key_y, or equal keys and idx_x < idx_y
+    // 2. bitonic sort with the keys in registers
+    const bool active = i0 < Np;
+    SKey v[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const uint64_t kk = active ? key[i0 + e] : 0;
+        v[e] = SKey{(uint32_t)(kk >> 32), (uint32_t)kk, active ? (int)idx[i0 + e] : 0xFFFF};
+    }
     for (int k = 2; k <= Np; k <<= 1) {
         for (int j = k >> 1; j > 0; j >>= 1) {
-            for (int i = tid; i < Np; i += kSchedThreads) {
-                const int p = i ^ j;
-                if (p > i) {
-                    const uint64_t ki = key[i], kp = key[p];
-                    const uint16_t ii = idx[i], ip = idx[p];
-                    const bool p_first = (kp > ki) || (kp == ki && ip < ii);
-                    const bool up = (i & k) == 0;
-                    if (up ? p_first : !p_first) {
-                        key[i] = kp; key[p] = ki;
-                        idx[i] = ip; idx[p] = ii;
+            if (j < E) {
+                if (E > 4 && j == 4) sort_in_thread<E, (E > 4 ? 4 : 1)>(v, i0, k);
+                else if (E > 2 && j == 2) sort_in_thread<E, (E > 2 ? 2 : 1)>(v, i0, k);
+                else sort_in_thread<E, 1>(v, i0, k);
+            } else if (j < DSPARK_WAVE * E) {
+                // partner element e of lane ^ (j / E)
+                const int m = j / E;
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    const SKey o{(uint32_t)__shfl_xor((int)v[e].hi, m, DSPARK_WAVE),
+                                 (uint32_t)__shfl_xor((int)v[e].lo, m, DSPARK_WAVE),
+                                 __shfl_xor(v[e].idx, m, DSPARK_WAVE)};
+                    const int i = i0 + e;
+                    const bool first = ((i & j) == 0) == ((i & k) == 0);  // keep the earlier one
+                    if (before(o, v[e]) == first) v[e] = o;
+                }
+            } else {
+                // partner in another wave: exchange through LDS
+                __syncthreads();  // everyone has read the previous exchange
+                if (active) {
+#pragma unroll
+                    for (int e = 0; e < E; ++e) {
+                        key[i0 + e] = ((uint64_t)v[e].hi << 32) | v[e].lo;
+                        idx[i0 + e] = (uint16_t)v[e].idx;
+                    }
+                }
+                __syncthreads();
+                if (active) {
+#pragma unroll
+                    for (int e = 0; e < E; ++e) {
+                        const int i = i0 + e;
+                        const uint64_t kk = key[i ^ j];
+                        const SKey o{(uint32_t)(kk >> 32), (uint32_t)kk, (int)idx[i ^ j]};
+                        const bool first = ((i & j) == 0) == ((i & k) == 0);
+                        if (before(o, v[e]) == first) v[e] = o;
                     }
                 }
             }
-            __syncthreads();
         }
     }
+    __syncthreads();
+    if (active) {
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            key[i0 + e] = ((uint64_t)v[e].hi << 32) | v[e].lo;
+            idx[i0 + e] = (uint16_t)v[e].idx;
+        }
+    }
+    __syncthreads();
     const int ncand = s_ncand;
 
-    // 3. inclusive scan of the sorted survival probabilities (fp64)
-    const int seg = Np >= kSchedThreads ? Np / kSchedThreads : 1;  // <= 8
-    const int base = tid * seg;
-    double loc[8];
+    // 3. inclusive scan of the sorted survival probabilities (fp64); thread t
+    // owns positions i0 .. i0 + E - 1 (E = 1 covers all when Np <= 1024)
+    double loc[E];
     double run = 0.0;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        if (e < seg) {
-            const int n = base + e;
-            const double a = (n < ncand) ? __longlong_as_double((long long)key[n]) : 0.0;
-            run = run + a;
-            loc[e] = run;
-        }
+    for (int e = 0; e < E; ++e) {
+        const int n = i0 + e;
+        const double a = (n < ncand) ? __longlong_as_double((long long)key[n]) : 0.0;
+        run = run + a;
+        loc[e] = run;
     }
     // wave inclusive scan of the per-thread totals
     double incl = run;
@@ -142,30 +225,31 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
     double wave_off = 0.0;
     for (int w = 0; w < wave; ++w) wave_off = wave_off + s_wave_tot[w];
     const double excl = wave_off + (incl - run);
-    __syncthreads();  // every thread has read its elements' keys
     const double Rd = (double)R;
+    // tau at this thread's positions, and at the position before them
+    double tau[E];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        if (e < seg) {
-            const int n = base + e;
-            if (n < ncand) key[n] = (uint64_t)__double_as_longlong(Rd + (excl + loc[e]));
-        }
-    }
+    for (int e = 0; e < E; ++e) tau[e] = Rd + (excl + loc[e]);
+    // Theta of position n - 1 for the first position of each thread: the
+    // previous thread's last tau (theta0 for position 0)
+    const double tau_prev_last = __shfl_up(tau[E - 1], 1, DSPARK_WAVE);
+    __shared__ double s_wave_last_tau[kSchedWaves];
+    if (lane == DSPARK_WAVE - 1) s_wave_last_tau[wave] = tau[E - 1];
     if (tid == 0) s_first = ncand;
     __syncthreads();
+    const double theta0 = Rd * sps_r;
+    double prev_tau = lane > 0 ? tau_prev_last : (wave > 0 ? s_wave_last_tau[wave - 1] : 0.0);
 
     // 4. throughput along the greedy path and the stop rule
-    const double theta0 = Rd * sps[R];
     int n_adm;
     if (mode == 0) {
         int first = ncand;
-        for (int e = 0; e < seg; ++e) {
-            const int n = base + e;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const int n = i0 + e;
             if (n >= ncand) break;
-            const double th = __longlong_as_double((long long)key[n]) * sps[R + n + 1];
-            const double prev = n == 0
-                ? theta0
-                : __longlong_as_double((long long)key[n - 1]) * sps[R + n];
+            const double th = tau[e] * spsv[e + 1];
+            const double prev = n == 0 ? theta0 : (e == 0 ? prev_tau : tau[e - 1]) * spsv[e];
             if (!(th > prev)) { first = n; break; }
         }
         if (first < ncand) atomicMin(&s_first, first);
@@ -174,10 +258,11 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
     } else {
         double bv = tid == 0 ? theta0 : -1.0 / 0.0;
         int bn = -1;
-        for (int e = 0; e < seg; ++e) {
-            const int n = base + e;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const int n = i0 + e;
             if (n >= ncand) break;
-            const double th = __longlong_as_double((long long)key[n]) * sps[R + n + 1];
+            const double th = tau[e] * spsv[e + 1];
             if (th > bv) { bv = th; bn = n; }
         }
         if (tid != 0 && bn == -1) bn = 0x7fffffff;
@@ -240,13 +325,25 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
     }
     if (R == 0 && tid == 0 && cu_q) cu_q[0] = 0;
     if (tok_req) {
-        __syncthreads();
-        // total = sum(1 + len) is known to the thread owning the last request;
-        // recompute it from the scan totals so every thread can clear the tail
+        // total = sum(1 + len) from the scan totals, so every thread can clear the tail
         int total = 0;
         for (int w = 0; w < kSchedWaves; ++w) total += s_wave_int[w];
         for (int i = total + tid; i < R * (K + 1); i += kSchedThreads) tok_req[i] = -1;
     }
+}
+
+template <int E>
+static hipError_t launch_e(const float* conf, int R, int K, const double* sps, int mode, int Np,
+                           size_t lds, int32_t* len, int32_t* cu_q, int32_t* tok_req,
+                           hipStream_t s) {
+    if (lds > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute((const void*)schedule_kernel<E>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(schedule_kernel<E>, dim3(1), dim3(kSchedThreads), lds, s, conf, R, K, sps,
+                       mode, Np, len, cu_q, tok_req);
+    return hipGetLastError();
 }
 
 hipError_t launch_schedule(const float* conf, int R, int K, const double* sps, int mode,
@@ -254,15 +351,13 @@ hipError_t launch_schedule(const float* conf, int R, int K, const double* sps, i
     const int N = R * K;
     const int Np = next_pow2(N > 0 ? N : 1);
     const size_t lds = schedule_lds_bytes(R, K);
-    if (lds > 64 * 1024) {
-        hipError_t e = hipFuncSetAttribute((const void*)schedule_kernel,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           (int)lds);
-        if (e != hipSuccess) return e;
+    // keys per thread (N <= 8192)
+    switch (Np <= kSchedThreads ? 1 : Np / kSchedThreads) {
+        case 1: return launch_e<1>(conf, R, K, sps, mode, Np, lds, len, cu_q, tok_req, s);
+        case 2: return launch_e<2>(conf, R, K, sps, mode, Np, lds, len, cu_q, tok_req, s);
+        case 4: return launch_e<4>(conf, R, K, sps, mode, Np, lds, len, cu_q, tok_req, s);
+        default: return launch_e<8>(conf, R, K, sps, mode, Np, lds, len, cu_q, tok_req, s);
     }
-    hipLaunchKernelGGL(schedule_kernel, dim3(1), dim3(kSchedThreads), lds, s, conf, R, K, sps,
-                       mode, Np, len, cu_q, tok_req);
-    return hipGetLastError();
 }
 
 }  // namespace dspark
