@@ -46,6 +46,12 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run a plain 1 GiB device copy 10 times (calibrates the HBM counters)")
+    ap.add_argument("--traffic-from", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV",
+                                                        "COPY_WRITE_CSV"),
+                    help="turn four rocprofv3 --pmc counter files (FETCH_SIZE and WRITE_SIZE of a bench "
+                         "run, then of a --copy-probe run) into the committed traffic summary")
     return ap.parse_args()
 
 
@@ -69,8 +75,113 @@ def accept_bytes(w, q_len: np.ndarray, accepted: np.ndarray) -> int:
     return rows + rejected * w.V * 4
 
 
+HERE = os.path.dirname(os.path.abspath(__file__))
+ATTN_SRC = os.path.join(HERE, "paper_2607_05147_amd", "csrc", "attn_mfma.hip")
+# the kernels of one dspark_verify_attn call on the MFMA path
+ATTN_KERNELS = ("mf_plan", "attn_mfma_kernel", "attn_mfma_merge")
+
+
+def traffic_file(workload: str) -> str:
+    return os.path.join(HERE, "profiles", f"verify_attn_{workload}_traffic.json")
+
+
+def source_sha(path: str) -> str:
+    import hashlib
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def _counter_rows(path: str):
+    """(kernel name, value) per dispatch of a rocprofv3 counter_collection.csv."""
+    import csv
+    per = {}
+    with open(path) as f:
+        for row in csv.DictReader(f):
+            key = (row["Dispatch_Id"], row["Kernel_Name"])
+            per[key] = per.get(key, 0.0) + float(row["Counter_Value"])
+    return [(k[1], v) for k, v in per.items()]
+
+
+def traffic_from(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, workload="serving"):
+    """Per-call HBM traffic of dspark_verify_attn from FETCH_SIZE / WRITE_SIZE
+    (KiB per dispatch), each scaled by what the same counter reads for a plain
+    1 GiB device copy; written next to the other profile summaries."""
+    def copy_scale(path):
+        vals = [v for name, v in _counter_rows(path) if "copyBuffer" in name or "copy" in name.lower()]
+        vals = [v for v in vals if v > 1e5]  # the 1 GiB copies
+        return (float(1 << 30) / 1024.0) / (sum(vals) / len(vals))
+
+    def per_call(path):
+        rows = _counter_rows(path)
+        calls = sum(1 for name, _ in rows if "attn_mfma_kernel" in name)
+        tot = {k: sum(v for name, v in rows if k in name) for k in ATTN_KERNELS}
+        return {k: tot[k] / calls * 1024.0 for k in ATTN_KERNELS}, calls
+
+    sf, sw = copy_scale(copy_fetch_csv), copy_scale(copy_write_csv)
+    fetch, calls = per_call(fetch_csv)
+    write, _ = per_call(write_csv)
+    out = {
+        "workload": workload,
+        "kernels": list(ATTN_KERNELS),
+        "calls": calls,
+        "copy_scale": {"FETCH_SIZE": sf, "WRITE_SIZE": sw},
+        "fetch_bytes_per_call": {k: v * sf for k, v in fetch.items()},
+        "write_bytes_per_call": {k: v * sw for k, v in write.items()},
+        "bytes_per_call": sum(fetch.values()) * sf + sum(write.values()) * sw,
+        "source_sha256": source_sha(ATTN_SRC),
+        "commands": [
+            "rocprofv3 --pmc FETCH_SIZE --output-format csv -d <dir> -o pmc -- python bench.py "
+            "--steps 5 --warmup 1 --no-cpu-baseline",
+            "rocprofv3 --pmc WRITE_SIZE --output-format csv -d <dir> -o pmc -- python bench.py "
+            "--steps 5 --warmup 1 --no-cpu-baseline",
+            "rocprofv3 --pmc FETCH_SIZE --output-format csv -d <dir> -o pmc -- python bench.py --copy-probe",
+            "rocprofv3 --pmc WRITE_SIZE --output-format csv -d <dir> -o pmc -- python bench.py --copy-probe",
+            "python bench.py --traffic-from <the four pmc_counter_collection.csv files>",
+        ],
+    }
+    os.makedirs(os.path.dirname(traffic_file(workload)), exist_ok=True)
+    with open(traffic_file(workload), "w") as f:
+        json.dump(out, f, indent=1)
+    log(f"traffic: {out['bytes_per_call'] / 1e9:.3f} GB per call (copy scale fetch {sf:.3f}, "
+        f"write {sw:.3f}) -> {traffic_file(workload)}")
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per verify-attention call from the committed counter summary,
+    or None when there is none or the kernel source changed since."""
+    try:
+        with open(traffic_file(workload)) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_sha256") != source_sha(ATTN_SRC):
+        return None
+    return t["bytes_per_call"]
+
+
+def copy_probe():
+    """A plain device copy of 1 GiB, ten times: the known byte count against
+    which rocprofv3's FETCH_SIZE / WRITE_SIZE counters are scaled."""
+    import torch
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda:0")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    torch.cuda.synchronize()
+    for _ in range(10):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    log(f"copy probe: 10 copies of {n} bytes")
+
+
 def main():
     args = parse()
+    if args.traffic_from:
+        traffic_from(*args.traffic_from)
+        return
+    if args.copy_probe:
+        copy_probe()
+        return
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (--gpus {args.gpus} requested); "
               "the multi-GPU layout is described in DESIGN.md", file=sys.stderr)
@@ -177,6 +288,7 @@ def main():
     ms_per_step = wall * 1e3 / args.steps
 
     ab = attention_bytes(w, kv.kv_len, q_len)
+    mfma = bf16 and w.Dqk == 128 and w.Dv == 128 and w.page >= 64
     cb = accept_bytes(w, q_len, accepted)
     attn_s = attn_ms.mean() / 1e3
     acc_s = acc_ms.mean() / 1e3
@@ -214,10 +326,14 @@ def main():
         "attn_accept_hbm": {"bytes": ab + cb, "achieved_gbps": both_gbps,
                             "frac_of_peak": both_gbps / HBM_PEAK_GBPS},
         "emitted_tokens_per_s": float((accepted + 1).sum()) / (ms_per_step / 1e3),
-        "roofline": {"kernel": "attn_mfma_kernel" if (bf16 and w.Dqk == 128) else "attn_generic_kernel",
+        # the dominant kernel: one dspark_verify_attn call (plan, attention and
+        # split-merge launches, bracketed together by the events)
+        "roofline": {"kernel": ("dspark_verify_attn: " + " + ".join(ATTN_KERNELS)) if mfma
+                               else "dspark_verify_attn: attn_generic_kernel + merge",
                      "bound": "hbm", "achieved": attn_gbps, "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": attn_gbps / HBM_PEAK_GBPS,
-                     "bytes_per_launch": ab, "traffic": None},
+                     "bytes_per_launch": ab,
+                     "traffic": measured_traffic(w.name) if mfma else None},
     }
 
     if not args.no_cpu_baseline:
@@ -254,12 +370,19 @@ def cpu_baseline(w, seed, conf, sps, ln, kv, q, logits, dr, target_s):
     while el < target_s / 4 and n < w.R:
         n = min(w.R, max(n + 1, int(n * min(8.0, target_s / max(el, 1e-3)))))
         el, rows = run(n)
-    log(f"oracle baseline: {n} requests, {rows} verify tokens in {el:.1f}s "
+    # a whole step that is quicker than the target is repeated up to it
+    reps = 1
+    while n == w.R and el < target_s * 0.7:
+        e2, _ = run(n)
+        el += e2
+        reps += 1
+    log(f"oracle baseline: {n} requests, {rows} verify tokens x {reps} in {el:.1f}s "
         f"on {oracle.threads()} threads")
-    return {"value": rows / el, "unit": "verified tokens/s", "cores": oracle.threads(),
+    return {"value": rows * reps / el, "unit": "verified tokens/s", "cores": oracle.threads(),
             "kind": "oracle",
             "sample": f"schedule over all {w.R} requests; attention + acceptance for requests "
-                      f"0..{n - 1} ({rows} verify tokens, {int(kvk.kv_len[:n].sum())} context tokens)",
+                      f"0..{n - 1} ({rows} verify tokens, {int(kvk.kv_len[:n].sum())} context tokens)"
+                      + (f", repeated {reps} times" if reps > 1 else ""),
             "seconds": el}
 
 
