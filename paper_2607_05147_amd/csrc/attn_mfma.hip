@@ -45,7 +45,8 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kMfThreads = 256;
 constexpr int kMfWaves = 4;
-constexpr int kSplit = 2048;   // keys per split (the last split of a context holds the rest)
+constexpr int kSplit = 4096;
+static_assert(kSplit / 64 <= DSPARK_WAVE, "a split's page ids fit one per lane");   // keys per split (the last split of a context holds the rest)
 constexpr int kStepTok = 32;   // keys per step
 constexpr int kRing = 4;       // LDS buffers; copies run kRing - 1 steps ahead
 constexpr int kD = 128;
@@ -59,8 +60,8 @@ constexpr float kLn2 = 0.6931471805599453f;
 static int pick_tpw(const AttnArgs& a) { return a.max_q * (a.Hq / a.Hkv) > 64 ? 2 : 1; }
 
 bool attn_mfma_supported(const AttnArgs& a) {
-    // power-of-two pages of 64 keys or more: a split (<= kSplit + 32 keys) then
-    // spans at most 34 pages, whose ids fit one per lane of a wave
+    // power-of-two pages of 64 keys or more: a split (kSplit keys, aligned) then
+    // spans at most 64 pages, whose ids fit one per lane of a wave
     const int64_t lim = (int64_t)1 << 30;  // byte strides fit 32-bit offsets
     return a.bf16 && a.Dqk == kD && a.Dv == kD && a.page >= 64 && (a.page & (a.page - 1)) == 0 &&
            a.ks[0] < lim && a.ks[1] < lim && a.ks[2] < lim && a.vs[0] < lim && a.vs[1] < lim &&
@@ -135,8 +136,8 @@ __host__ __device__ __forceinline__ void split_range(int kv, int ns, int s, int&
 // split.
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanLanes = 8;                 // threads per request
-constexpr int kBins = kSplit / kStepTok + 2;  // steps per item are at most kSplit / 32 + 1
-static_assert(kBins <= 2 * DSPARK_WAVE, "bin scan covers two bins per lane");
+constexpr int kBins = kSplit / kStepTok + 1;  // steps per item are at most kSplit / 32
+constexpr int kBinsPerLane = (kBins + DSPARK_WAVE - 1) / DSPARK_WAVE;
 __global__ __launch_bounds__(kPlanThreads) void mf_plan(MfParams p) {
     const AttnArgs& a = p.a;
     __shared__ int s_bin[kBins];
@@ -169,17 +170,28 @@ __global__ __launch_bounds__(kPlanThreads) void mf_plan(MfParams p) {
         for (int sp = sub; sp < ns; sp += kPlanLanes) atomicAdd(&s_bin[steps_of(kv, ns, sp)], a.Hkv * nr);
     }
     __syncthreads();
-    if (tid < DSPARK_WAVE) {  // bin start offsets, longest first: lane l owns bins kBins-1-2l, kBins-2-2l
-        const int b0 = kBins - 1 - 2 * lane, b1 = b0 - 1;
-        const int c0 = b0 >= 0 ? s_bin[b0] : 0, c1 = b1 >= 0 ? s_bin[b1] : 0;
-        int incl = c0 + c1;
+    if (tid < DSPARK_WAVE) {
+        // bin start offsets, longest first: lane l owns the bins at descending
+        // positions kBinsPerLane * l .. kBinsPerLane * (l + 1) - 1
+        int cnt[kBinsPerLane], mine = 0;
+#pragma unroll
+        for (int k = 0; k < kBinsPerLane; ++k) {
+            const int b = kBins - 1 - (kBinsPerLane * lane + k);
+            cnt[k] = b >= 0 ? s_bin[b] : 0;
+            mine += cnt[k];
+        }
+        int incl = mine;
         for (int o = 1; o < DSPARK_WAVE; o <<= 1) {
             const int t = __shfl_up(incl, o, DSPARK_WAVE);
             if (lane >= o) incl += t;
         }
-        const int excl = incl - c0 - c1;
-        if (b0 >= 0) s_bin[b0] = excl;
-        if (b1 >= 0) s_bin[b1] = excl + c0;
+        int run = incl - mine;
+#pragma unroll
+        for (int k = 0; k < kBinsPerLane; ++k) {
+            const int b = kBins - 1 - (kBinsPerLane * lane + k);
+            if (b >= 0) s_bin[b] = run;
+            run += cnt[k];
+        }
         if (lane == DSPARK_WAVE - 1) {
             p.work[0] = 0;
             p.work[1] = incl;
@@ -300,7 +312,7 @@ constexpr float kRescale = 8.0f;  // log2 headroom before the running max is mov
 template <int TPW>
 __device__ __forceinline__ void attn_item(const MfParams& p, const int r, const int g, const int s,
                                           const int rc, const int q0, const int ql, const int kv,
-                                          const int nsplit, const uint32_t lds0) {
+                                          const int nsplit, const uint32_t lds0, int& nxt) {
     const AttnArgs& a = p.a;
     constexpr int kChunkRows = 16 * kMfWaves * TPW;
     constexpr int kSlotFloats = kChunkRows * (kD + 2);
@@ -328,7 +340,7 @@ __device__ __forceinline__ void attn_item(const MfParams& p, const int r, const 
 
     // ---- page ids of the split, one per lane
     const int pg0 = start >> p.page_shift;
-    const int npg = ((end - 1) >> p.page_shift) - pg0 + 1;  // <= 34 (pages of >= 64 keys)
+    const int npg = ((end - 1) >> p.page_shift) - pg0 + 1;  // <= 64 (pages of >= 64 keys)
     const int my_page = lane < npg ? a.block_table[(int64_t)r * a.max_pages + pg0 + lane] : 0;
 
     // ---- query fragments (B operand of S^T = K Q^T) and causal limits
@@ -533,9 +545,15 @@ __device__ __forceinline__ void attn_item(const MfParams& p, const int r, const 
     wait_vmcnt<0>();
 #pragma unroll
     for (int n = 0; n < kRing - 1; ++n) issue(n);
+    // the next item is claimed three steps before this one ends: late enough
+    // that no claimed item waits behind a long one, early enough for the
+    // atomic to return before the end (it adds one operation to wave 0's
+    // count, which at worst makes one wait cover a copy of the next step too)
+    const int claim = max(nsteps - 3, 0);
     auto one = [&](int n, auto bufc) {
         wait_vmcnt<(kRing - 2) * kCopiesPerStep>();
         lds_barrier();  // step n visible to all; everyone is done with step n - 1
+        if (n == claim && tid == 0) nxt = atomicAdd(p.work, 1);
         issue(n + kRing - 1);
         if (nt_w > 0) compute(n, bufc);
     };
@@ -611,10 +629,8 @@ void attn_mfma_kernel(MfParams p) {
     while (it < total) {
         const int4 e0 = p.list[2 * it];      // uniform: scalar loads
         const int4 e1 = p.list[2 * it + 1];
-        // take the next item now; its index is needed only at the end
-        int nxt = 0;
-        if (threadIdx.x == 0) nxt = atomicAdd(p.work, 1);
-        attn_item<TPW>(p, e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w, lds0);
+        int nxt = 0;  // claimed by thread 0 near the end of the item
+        attn_item<TPW>(p, e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w, lds0, nxt);
         __syncthreads();  // everyone is done with this item's LDS and s_item
         if (threadIdx.x == 0) s_item = nxt;
         __syncthreads();
