@@ -1,0 +1,786 @@
+// Latent (MLA-style) verify attention on gfx950 matrix cores.
+//
+// Shape: query heads sharing one latent KV head per group, Dqk = 576 (512
+// latent + 64 rotary dims), Dv = 512 with the values being the first 512 dims
+// of the same cache rows, bf16.  With 128 query heads on one latent head every
+// verify token contributes 128 rows that read the same keys, so the work is a
+// dense contraction (about 1.2 kFLOP per KV byte): this path is MFMA-bound,
+// unlike the GQA path.
+//
+// Work item = (request r, KV head g, block of 64 rows, KV split s).  A
+// workgroup of four waves owns the block, one 16-row tile per wave (one wave
+// per SIMD); its query fragments stay in registers and its output
+// accumulators in the accumulation registers.  The split is walked in 32-key steps:
+//   * each step's 32 cache rows (36 KB) are copied into LDS with
+//     global_load_lds_dwordx4 (nine instructions per wave), into a ring of
+//     three buffers two steps ahead; LDS rows keep the 1152-byte cache pitch
+//     and the 16-byte chunks are swizzled (bits 0-2 of the chunk index XOR a
+//     function of the row, see pchunk) so that the score operand reads and the
+//     transposing value reads are free of bank conflicts while every read
+//     address stays a per-lane base plus an immediate;
+//   * S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (18 slices of the 576 dims,
+//     two key blocks: 36 products per wave and step);
+//   * softmax in exp2 units against a fixed per-row reference (the first
+//     step's maximum); a block whose scores outgrow it by more than 2^32
+//     runs again with the observed maxima (masks only at the diagonal);
+//   * O^T += V^T P^T with the values read by ds_read_b64_tr_b16 (32 blocks of
+//     16 dims: 32 products per wave and step).
+// The row blocks of one (request, split) read the same keys: work items go to
+// eight queues, one per XCD (workgroup b runs on XCD b % 8), so those blocks
+// run side by side on one XCD and share its L2.  A workgroup whose queue is
+// empty takes items from the others.  Splits of one row block are combined by
+// a merge kernel after this one, in split order (bitwise reproducible).
+#include <algorithm>
+#include <type_traits>
+
+#include "device_common.h"
+#include "kernels.h"
+
+namespace dspark {
+namespace mla {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
+
+constexpr int kDk = 576;
+constexpr int kDv = 512;
+constexpr int kThreads = 256;
+constexpr int kWaves = 4;
+constexpr int kTiles = 1;                           // 16-row tiles per wave
+constexpr int kRows = 16 * kTiles * kWaves;         // 64 rows per work item
+constexpr int kStep = 32;                           // keys per step
+constexpr int kRing = 3;                            // LDS buffers; copies run 2 steps ahead
+constexpr int kChunks = kDk / 8;                    // 72 16-byte chunks of a cache row
+constexpr int kRowChunks = kChunks;                 // LDS row pitch in chunks (no pad: the swizzle spreads banks)
+constexpr int kRowB = kRowChunks * 16;              // 1152 bytes
+constexpr int kTileChunks = kStep * kRowChunks;     // 2304
+constexpr int kTileB = kTileChunks * 16;            // 36864 bytes
+constexpr int kInstr = kTileChunks / 64;            // 36 wave copy instructions per step
+constexpr int kCopies = kInstr / kWaves;            // 9 per wave: 8 whole rows
+constexpr int kSplit = 8192;                        // keys per split (the last one holds the rest)
+constexpr int kPageRegs = kSplit / 64 / DSPARK_WAVE;  // page-id registers per lane (pages >= 64 keys)
+constexpr int kKs = kDk / 32;                       // 18 slices of the score product
+constexpr int kDb = kDv / 16;                       // 32 blocks of output dims
+constexpr int kQueues = 8;                          // one per XCD
+constexpr int kBins = kSplit / kStep + 1;           // item lengths in steps: 0 .. kSplit / 32
+constexpr int kMergeRows = 4;                       // rows per merge item (64 threads per row)
+constexpr int kAhead = 8;                           // LDS operand reads in flight ahead of the products
+constexpr int kSchedMfma = 0x008;                   // sched_group_barrier classes
+constexpr int kSchedDsRead = 0x100;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kRange = 32.0f;  // scores may exceed a row's reference by this (log2 units)
+static_assert(kInstr == kWaves * kCopies && kCopies * 64 == 8 * kRowChunks, "copy split over the waves");
+static_assert(kChunks % 8 == 0, "the swizzle permutes chunks within aligned groups of 8");
+static_assert(kPageRegs * DSPARK_WAVE * 64 >= kSplit, "page ids of a split fit the lanes");
+
+struct Geom {
+    int group, rb_max, max_splits;
+    int64_t n_items, n_merge;
+    size_t head_bytes, list_bytes, mlist_bytes, slot_floats, part_bytes;
+};
+
+struct Params {
+    AttnArgs a;
+    int group, rb_max, max_splits, page_shift;
+    uint32_t s0b, s1b, s2b;  // cache strides in bytes (values alias the keys)
+    float scale2;
+    int* head;               // [0..7] queue cursors, [8..15] queue begin, [16..23] queue end, [24] merges
+    int4* list;              // items: {r, g, row block, split}, {q0, q_len, kv, splits}
+    int4* mlist;             // merge items: {r, g, row block, first row}, {q0, q_len, kv, splits}
+    float* part;             // [slot][split] {m[kRows], l[kRows], o[kRows][512]}
+};
+
+static Geom geom(const AttnArgs& a) {
+    Geom g;
+    g.group = a.Hq / a.Hkv;
+    g.rb_max = (a.max_q * g.group + kRows - 1) / kRows;
+    const int64_t max_kv = (int64_t)a.max_pages * a.page;
+    g.max_splits = (int)std::max<int64_t>(1, (max_kv + kSplit - 1) / kSplit);
+    const int64_t slots = (int64_t)a.R * a.Hkv * g.rb_max;
+    g.n_items = slots * g.max_splits;
+    g.n_merge = g.max_splits > 1 ? slots * (kRows / kMergeRows) : 0;
+    g.head_bytes = 256;
+    g.list_bytes = ((size_t)g.n_items * 2 * sizeof(int4) + 255) & ~(size_t)255;
+    g.mlist_bytes = ((size_t)g.n_merge * 2 * sizeof(int4) + 255) & ~(size_t)255;
+    g.slot_floats = (size_t)kRows * (kDv + 2);
+    g.part_bytes = g.max_splits > 1 ? (size_t)slots * g.max_splits * g.slot_floats * sizeof(float) : 0;
+    return g;
+}
+
+__host__ __device__ __forceinline__ void split_range(int kv, int s, int& start, int& end) {
+    start = s * kSplit;
+    end = min(kv, start + kSplit);
+}
+
+// Physical chunk of chunk c in LDS row t: bits 0-2 of c XOR (t % 4 | (t / 8 % 2) << 2).
+// gfx950 serves a 16-byte LDS read in four 16-lane phases (lanes split by bit 5
+// and by the parity of bits 2 ^ 3 ^ 4) and a transposing 8-byte read in two
+// 32-lane halves, over 64 four-byte banks; with a 1152-byte pitch this XOR
+// puts the 16 (or 32) lanes of every phase of the score-operand and the
+// value-operand reads below on distinct banks.
+__device__ __forceinline__ int pchunk(int t, int c) { return c ^ ((t & 3) | (((t >> 3) & 1) << 2)); }
+
+// A cache row of zeros (zero-initialised at load, never written): keys at or
+// past a split's end are copied from here.
+__device__ __align__(16) uint16_t g_zero_row[kDk];
+
+__device__ __forceinline__ void lds_copy16(const void* gsrc, uint32_t lds_addr) {
+    const uint32_t m0 = __builtin_amdgcn_readfirstlane(lds_addr);
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "global_load_lds_dwordx4 %1, off"
+        :
+        : "s"(m0), "v"(gsrc)
+        : "memory", "m0");
+}
+
+__device__ __forceinline__ void lds_copy16_s(uint64_t sbase, uint32_t voff, uint32_t lds_addr) {
+    const uint32_t m0 = __builtin_amdgcn_readfirstlane(lds_addr);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)sbase);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(sbase >> 32));
+    const uint64_t sb = ((uint64_t)hi << 32) | lo;
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "global_load_lds_dwordx4 %1, %2"
+        :
+        : "s"(m0), "v"(voff), "s"(sb)
+        : "memory", "m0");
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+__device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+
+__device__ __forceinline__ float row_max4(float v) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = vmax(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return vmax(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){lo, hi}, bf16x2));
+}
+
+__device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
+    return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
+// ------------------------------------------------------------------ plan
+
+// Builds the per-XCD work queues and the merge list from cu_q / kv_len.  One
+// workgroup.  Groups (request, KV head, split) are dealt to the queues round
+// robin in request order; inside a queue the items are counting-sorted by
+// length, longest first, with the row blocks of a group kept together.
+constexpr int kPlanThreads = 1024;
+__global__ __launch_bounds__(kPlanThreads) void mla_plan(Params p) {
+    const AttnArgs& a = p.a;
+    __shared__ int s_bin[kQueues][kBins];
+    __shared__ int s_qtot[kQueues];
+    __shared__ int s_wave[kPlanThreads / DSPARK_WAVE];
+    __shared__ int s_merge;
+    const int tid = threadIdx.x;
+    const int lane = tid & (DSPARK_WAVE - 1);
+    const int wave = tid / DSPARK_WAVE;
+    for (int i = tid; i < kQueues * kBins; i += kPlanThreads) (&s_bin[0][0])[i] = 0;
+    if (tid == 0) s_merge = 0;
+    auto shape = [&](int r, int& q0, int& ql, int& kv, int& ns, int& nrb) {
+        q0 = a.cu_q[r];
+        ql = a.cu_q[r + 1] - q0;
+        kv = a.kv_len[r];
+        if (ql < 1 || ql > a.max_q || kv < ql || kv > a.max_pages * a.page) return false;
+        ns = (kv + kSplit - 1) / kSplit;
+        nrb = (ql * p.group + kRows - 1) / kRows;
+        return true;
+    };
+    auto steps_of = [&](int kv, int s) {
+        int st, en;
+        split_range(kv, s, st, en);
+        return min((en - st + kStep - 1) / kStep, kBins - 1);
+    };
+    // group ids: exclusive scan of the groups of each request (contiguous ranges)
+    const int per = (a.R + kPlanThreads - 1) / kPlanThreads;
+    const int r0 = min(a.R, tid * per), r1 = min(a.R, r0 + per);
+    int mine = 0;
+    for (int r = r0; r < r1; ++r) {
+        int q0, ql, kv, ns, nrb;
+        if (shape(r, q0, ql, kv, ns, nrb)) mine += a.Hkv * ns;
+    }
+    int incl = mine;
+    for (int o = 1; o < DSPARK_WAVE; o <<= 1) {
+        const int t = __shfl_up(incl, o, DSPARK_WAVE);
+        if (lane >= o) incl += t;
+    }
+    if (lane == DSPARK_WAVE - 1) s_wave[wave] = incl;
+    __syncthreads();
+    int gid0 = incl - mine;
+    for (int w = 0; w < wave; ++w) gid0 += s_wave[w];
+    // histogram per queue and length
+    {
+        int gid = gid0;
+        for (int r = r0; r < r1; ++r) {
+            int q0, ql, kv, ns, nrb;
+            if (!shape(r, q0, ql, kv, ns, nrb)) continue;
+            for (int g = 0; g < a.Hkv; ++g)
+                for (int s = 0; s < ns; ++s, ++gid) atomicAdd(&s_bin[gid % kQueues][steps_of(kv, s)], nrb);
+        }
+    }
+    __syncthreads();
+    if (tid < kQueues) {  // per queue: bin offsets, longest first
+        int off = 0;
+        for (int b = kBins - 1; b >= 0; --b) {
+            const int c = s_bin[tid][b];
+            s_bin[tid][b] = off;
+            off += c;
+        }
+        s_qtot[tid] = off;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int base = 0;
+        for (int q = 0; q < kQueues; ++q) {
+            p.head[q] = 0;
+            p.head[kQueues + q] = base;
+            base += s_qtot[q];
+            p.head[2 * kQueues + q] = base;
+            s_qtot[q] = p.head[kQueues + q];  // now the queue's start
+        }
+    }
+    __syncthreads();
+    {
+        int gid = gid0;
+        for (int r = r0; r < r1; ++r) {
+            int q0, ql, kv, ns, nrb;
+            if (!shape(r, q0, ql, kv, ns, nrb)) continue;
+            const int4 meta = int4{q0, ql, kv, ns};
+            for (int g = 0; g < a.Hkv; ++g)
+                for (int s = 0; s < ns; ++s, ++gid) {
+                    const int q = gid % kQueues;
+                    const int off = s_qtot[q] + atomicAdd(&s_bin[q][steps_of(kv, s)], nrb);
+                    for (int b = 0; b < nrb; ++b) {
+                        p.list[2 * (off + b)] = int4{r, g, b, s};
+                        p.list[2 * (off + b) + 1] = meta;
+                    }
+                }
+            if (ns > 1) {
+                const int rows = ql * p.group;
+                int cnt = 0;
+                for (int b = 0; b < nrb; ++b)
+                    cnt += (min(kRows, rows - b * kRows) + kMergeRows - 1) / kMergeRows;
+                int off = atomicAdd(&s_merge, a.Hkv * cnt);
+                for (int g = 0; g < a.Hkv; ++g)
+                    for (int b = 0; b < nrb; ++b) {
+                        const int nrows = min(kRows, rows - b * kRows);
+                        for (int m0 = 0; m0 < nrows; m0 += kMergeRows, ++off) {
+                            p.mlist[2 * off] = int4{r, g, b, m0};
+                            p.mlist[2 * off + 1] = meta;
+                        }
+                    }
+            }
+        }
+    }
+    __syncthreads();
+    if (tid == 0) p.head[3 * kQueues] = s_merge;
+}
+
+// ------------------------------------------------------------------ item
+
+__device__ __forceinline__ void item(const Params& p, const int r, const int g, const int rb,
+                                     const int s, const int q0, const int ql, const int kv,
+                                     const int nsplit, const uint32_t lds0, const int home,
+                                     int& nxt, int& s_flag) {
+    const AttnArgs& a = p.a;
+    constexpr int kSlotFloats = kRows * (kDv + 2);
+    const int rows = ql * p.group;
+    const int row0 = rb * kRows;
+    int start, end;
+    split_range(kv, s, start, end);
+    const int nrows = min(kRows, rows - row0);
+    const int nt = (nrows + 15) >> 4;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lr = lane & 15;
+    const int lq = lane >> 4;
+    const int nt_w = min(max(nt - kTiles * wave, 0), kTiles);  // tiles 2w, 2w + 1
+
+    const uint16_t* __restrict__ qg = (const uint16_t*)a.q;
+    const uint16_t* __restrict__ kc = (const uint16_t*)a.k;
+
+    // ---- page ids of the split, kPageRegs per lane
+    const int pg0 = start >> p.page_shift;
+    const int npg = ((end - 1) >> p.page_shift) - pg0 + 1;
+    int my_page[kPageRegs];
+#pragma unroll
+    for (int k = 0; k < kPageRegs; ++k) {
+        const int i = k * DSPARK_WAVE + lane;
+        my_page[k] = i < npg ? a.block_table[(int64_t)r * a.max_pages + pg0 + i] : 0;
+    }
+
+    // ---- query fragments (B operand of S^T = K Q^T) and causal limits
+    bf16x8 qf[kTiles][kKs];
+    int lim[kTiles];
+    int lim_min = 0x7fffffff;
+#pragma unroll
+    for (int j = 0; j < kTiles; ++j) {
+        const int row = row0 + 16 * (kTiles * wave + j) + lr;
+        if (row < rows) {
+            const int t = row / p.group;
+            const int h = g * p.group + (row - t * p.group);
+            const uint16_t* qp = qg + ((int64_t)(q0 + t) * a.Hq + h) * kDk + 8 * lq;
+#pragma unroll
+            for (int ks = 0; ks < kKs; ++ks) qf[j][ks] = *(const bf16x8*)(qp + 32 * ks);
+            lim[j] = kv - ql + t;
+            if (j < nt_w) lim_min = min(lim_min, lim[j]);
+        } else {
+#pragma unroll
+            for (int ks = 0; ks < kKs; ++ks) qf[j][ks] = bf16x8{};
+            lim[j] = -1;
+        }
+    }
+    lim_min = __reduce_min_sync(~0ull, lim_min);
+
+    // Softmax reference per row: exp2 is taken relative to mref, the row's first
+    // finite maximum, and the accumulators are never rescaled.  fp32 holds the
+    // probabilities comfortably while scores stay below mref + kRange; if one
+    // goes above (mobs tracks the maximum), the item is run again with
+    // mref = mobs.  Keeping the accumulators out of every VALU operation lets
+    // them stay in the accumulation registers.
+    f32x4 acc[kTiles][kDb];
+    float mref[kTiles], mobs[kTiles], lsum[kTiles];
+#pragma unroll
+    for (int j = 0; j < kTiles; ++j) mref[j] = mobs[j] = -__builtin_huge_valf();
+    bool over = false;  // some row of this wave went above mref + kRange
+
+    // ---- per-lane LDS offsets of the operand fragments (loop invariant)
+    // K (A operand): rows 8 (lr / 4) + 4 mb + lr % 4 (so that the score
+    // accumulator is the B operand of the value product), chunk 4 ks + lq;
+    // the swizzle sees ks only through its parity
+    uint32_t koff[2][2];  // [ks % 2][mb], + 128 (ks / 2)
+#pragma unroll
+    for (int kp = 0; kp < 2; ++kp)
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) {
+            const int t = 8 * (lr >> 2) + 4 * mb + (lr & 3);
+            koff[kp][mb] = lds0 + t * kRowB + pchunk(t, 4 * kp + lq) * 16;
+        }
+    // V^T (A operand of the value product, transposing reads): rows
+    // 8 lq + 4 h + lr / 4, chunk 2 db + (lr % 4) / 2, half lr % 2; the chunk
+    // swizzle sees db only through db % 4
+    uint32_t voff[4][2];  // [db % 4][h], + 128 (db / 4)
+#pragma unroll
+    for (int dq = 0; dq < 4; ++dq)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int t = 8 * lq + 4 * h + (lr >> 2);
+            const int c = 2 * dq + ((lr & 3) >> 1);
+            voff[dq][h] = lds0 + t * kRowB + pchunk(t, c) * 16 + (lr & 1) * 8;
+        }
+
+    // ---- copy geometry: this wave's copy instructions cover tile chunks
+    // p = (first + i) * 64 + lane, row p / 72, physical chunk p % 72
+    const int first = kCopies * wave;
+    // row and source chunk of copy i; the swizzle is an involution.  `ln` is
+    // the lane id passed through an empty asm at every use so that the
+    // geometry is recomputed per step (a few VALU operations) instead of being
+    // hoisted into registers that the operand pipeline needs.
+    auto cp_at = [&](int i, int ln, int& t, int& c) {
+        const int pp = (first + i) * 64 + ln;
+        t = pp / kRowChunks;
+        c = pchunk(t, pp - t * kRowChunks);
+    };
+    const int nsteps = (end - start + kStep - 1) / kStep;  // >= 1
+    const uint64_t kc_head = (uint64_t)(uintptr_t)kc + (uint64_t)((uint32_t)g * p.s1b);
+    const uint32_t lds_wave = __builtin_amdgcn_readfirstlane(lds0 + first * 1024);
+
+    auto page_of = [&](int idx) {
+        int pg = 0;
+#pragma unroll
+        for (int k = 0; k < kPageRegs; ++k)
+            if ((idx >> 6) == k) pg = __builtin_amdgcn_readlane(my_page[k], idx & 63);
+        return pg;
+    };
+    auto issue = [&](int n) {
+        const int tok0 = start + n * kStep;
+        const int pidx = min((tok0 >> p.page_shift) - pg0, kPageRegs * DSPARK_WAVE - 1);
+        const int page = page_of(pidx);
+        const int slot0 = tok0 & ((1 << p.page_shift) - 1);
+        const uint32_t dst = lds_wave + ((unsigned)n % kRing) * kTileB;
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        if (tok0 + kStep <= end) {
+            const uint64_t kb = kc_head + (uint64_t)(uint32_t)page * p.s0b + (uint32_t)slot0 * p.s2b;
+#pragma unroll
+            for (int i = 0; i < kCopies; ++i) {
+                int t, c;
+                cp_at(i, ln, t, c);
+                lds_copy16_s(kb, t * p.s2b + 16 * c, dst + i * 1024);
+            }
+        } else {
+            // last, partial step or past the end: keys at or past the end read the zero row
+            const uint16_t* kb = kc + (int64_t)page * a.ks[0] + (int64_t)g * a.ks[1];
+#pragma unroll
+            for (int i = 0; i < kCopies; ++i) {
+                int t, c;
+                cp_at(i, ln, t, c);
+                const bool in = tok0 + t < end;
+                const uint16_t* src = in ? kb + (int64_t)(slot0 + t) * a.ks[2] + 8 * c : g_zero_row + 8 * c;
+                lds_copy16(src, dst + i * 1024);
+            }
+        }
+    };
+
+    auto compute = [&](int n, auto bufc) {
+        constexpr unsigned buf = decltype(bufc)::value;
+        constexpr uint32_t boff = buf * kTileB;
+        const int tok0 = start + n * kStep;
+        // ---- scores S^T[key, row]: four accumulation chains (ks parity, key block)
+        f32x4 sc[kTiles][2][2];
+#pragma unroll
+        for (int j = 0; j < kTiles; ++j)
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb) sc[j][mb][0] = sc[j][mb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int ks = 0; ks < kKs; ++ks) {
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb) {
+                const bf16x8 kf = *(const lds_bf16x8*)(koff[ks & 1][mb] + boff + 128 * (ks >> 1));
+#pragma unroll
+                for (int j = 0; j < kTiles; ++j)
+                    sc[j][mb][ks & 1] =
+                        __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[j][ks], sc[j][mb][ks & 1], 0, 0, 0);
+            }
+        }
+        // software pipeline: kAhead fragment reads in flight ahead of the products
+        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, kAhead, 0);
+#pragma unroll
+        for (int i = 0; i < 2 * kKs - kAhead; ++i) {
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, kTiles, 0);
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, kTiles * kAhead, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        // ---- online softmax; keys of this lane: tok0 + 8 lq + 4 mb + e
+        const bool full = tok0 + kStep <= end && tok0 + kStep - 1 <= lim_min;
+        // (a tile past the block's rows has zero queries: finite scores, outputs never stored)
+        bf16x8 pf[kTiles];
+#pragma unroll
+        for (int j = 0; j < kTiles; ++j) {
+            {
+                float sv[8];
+#pragma unroll
+                for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) sv[4 * mb + e] = sc[j][mb][0][e] + sc[j][mb][1][e];
+                if (!full) {
+#pragma unroll
+                    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const int key = tok0 + 8 * lq + 4 * mb + e;
+                            if (!(key < end && key <= lim[j])) sv[4 * mb + e] = -__builtin_huge_valf();
+                        }
+                }
+                float bm = vmax(vmax(vmax(sv[0], sv[1]), sv[2]),
+                                vmax(vmax(sv[3], sv[4]), vmax(vmax(sv[5], sv[6]), sv[7])));
+                bm = row_max4(bm) * p.scale2;
+                mobs[j] = vmax(mobs[j], bm);
+                // the first finite maximum becomes the reference (nothing accumulated yet)
+                if (mref[j] == -__builtin_huge_valf()) mref[j] = bm;
+                over |= bm > mref[j] + kRange;
+                const float mu = mref[j] == -__builtin_huge_valf() ? 0.0f : mref[j];
+                float pr[8];
+#pragma unroll
+                for (int k = 0; k < 8; ++k) pr[k] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[k], p.scale2, -mu));
+                lsum[j] += ((pr[0] + pr[1]) + (pr[2] + pr[3])) + ((pr[4] + pr[5]) + (pr[6] + pr[7]));
+                u32x4 pk;
+                pk[0] = cvt_pk_bf16(pr[0], pr[1]);
+                pk[1] = cvt_pk_bf16(pr[2], pr[3]);
+                pk[2] = cvt_pk_bf16(pr[4], pr[5]);
+                pk[3] = cvt_pk_bf16(pr[6], pr[7]);
+                pf[j] = __builtin_bit_cast(bf16x8, pk);
+            }
+        }
+        // ---- O^T[d, row] += V^T P^T
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int db = 0; db < kDb; ++db) {
+            const uint32_t vo = boff + 128 * (db >> 2);
+            const s16x4 h0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(voff[db & 3][0] + vo));
+            const s16x4 h1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(voff[db & 3][1] + vo));
+            const bf16x8 vf = __builtin_bit_cast(
+                bf16x8, (short __attribute__((ext_vector_type(8)))){h0[0], h0[1], h0[2], h0[3],
+                                                                     h1[0], h1[1], h1[2], h1[3]});
+#pragma unroll
+            for (int j = 0; j < kTiles; ++j)
+                acc[j][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[j], acc[j][db], 0, 0, 0);
+        }
+        // software pipeline: two transposing reads per product, kAhead reads in flight
+        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, kAhead, 0);
+#pragma unroll
+        for (int i = 0; i < kDb - kAhead / 2; ++i) {
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, kTiles, 0);
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, kTiles * kAhead / 2, 0);
+        __builtin_amdgcn_sched_barrier(0);
+    };
+
+    // ---- main loop: every thread issues kCopies copies per step, in order, also
+    // past the last step (zero-row copies into buffers not read again), so
+    // "step n has landed" is vmcnt <= (kRing - 2) * kCopies.
+    const int claim = max(nsteps - 3, 0);
+    for (int attempt = 0;; ++attempt) {
+#pragma unroll
+        for (int j = 0; j < kTiles; ++j) {
+            lsum[j] = 0.0f;
+#pragma unroll
+            for (int db = 0; db < kDb; ++db) acc[j][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+        wait_vmcnt<0>();
+#pragma unroll
+        for (int n = 0; n < kRing - 1; ++n) issue(n);
+        auto one = [&](int n, auto bufc) {
+            wait_vmcnt<(kRing - 2) * kCopies>();
+            lds_barrier();  // step n visible to all; everyone is done with step n - 1
+            if (n == claim && tid == 0 && attempt == 0) nxt = atomicAdd(p.head + home, 1);
+            issue(n + kRing - 1);
+            if (nt_w > 0) compute(n, bufc);
+        };
+        for (int n = 0; n < nsteps; n += kRing) {
+            one(n, std::integral_constant<unsigned, 0>{});
+            if (n + 1 < nsteps) one(n + 1, std::integral_constant<unsigned, 1>{});
+            if (n + 2 < nsteps) one(n + 2, std::integral_constant<unsigned, 2>{});
+        }
+        wait_vmcnt<0>();
+        // did any row of the block outgrow its reference?  (all waves agree)
+        if (lane == 0 && __builtin_amdgcn_ballot_w64(over)) atomicOr(&s_flag, 1);
+        __syncthreads();
+        const int again = s_flag;
+        __syncthreads();
+        if (!again) break;
+        if (tid == 0) s_flag = 0;
+#pragma unroll
+        for (int j = 0; j < kTiles; ++j) mref[j] = mobs[j];
+        over = false;
+    }
+
+    // ---- finish rows: l over the four lanes of a row
+#pragma unroll
+    for (int j = 0; j < kTiles; ++j) {
+        lsum[j] += __shfl_xor(lsum[j], 16, 64);
+        lsum[j] += __shfl_xor(lsum[j], 32, 64);
+    }
+    if (nsplit == 1) {
+        uint16_t* outp = (uint16_t*)a.out;
+#pragma unroll
+        for (int j = 0; j < kTiles; ++j) {
+            const int row = row0 + 16 * (kTiles * wave + j) + lr;
+            if (j < nt_w && row < rows) {
+                const int t = row / p.group;
+                const int h = g * p.group + (row - t * p.group);
+                const int64_t orow = (int64_t)(q0 + t) * a.Hq + h;
+                const float inv = 1.0f / lsum[j];
+#pragma unroll
+                for (int db = 0; db < kDb; ++db) {
+                    uint2 pk;
+                    pk.x = pack2_bf16(acc[j][db][0] * inv, acc[j][db][1] * inv);
+                    pk.y = pack2_bf16(acc[j][db][2] * inv, acc[j][db][3] * inv);
+                    *(uint2*)(outp + orow * kDv + 16 * db + 4 * lq) = pk;
+                }
+                if (a.lse && lq == 0) a.lse[orow] = (mref[j] + log2f(lsum[j])) * kLn2;
+            }
+        }
+        return;
+    }
+    float* part = p.part + (((int64_t)(r * a.Hkv + g) * p.rb_max + rb) * p.max_splits + s) * kSlotFloats;
+#pragma unroll
+    for (int j = 0; j < kTiles; ++j) {
+        const int rr = 16 * (kTiles * wave + j) + lr;
+        if (j < nt_w) {
+            if (lq == 0) {
+                part[rr] = mref[j];
+                part[kRows + rr] = lsum[j];
+            }
+#pragma unroll
+            for (int db = 0; db < kDb; ++db)
+                *(f32x4*)(part + 2 * kRows + rr * kDv + 16 * db + 4 * lq) = acc[j][db];
+        }
+    }
+}
+
+// Persistent workgroups: workgroup b serves queue b % 8 (its XCD), then the others.
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void mla_kernel(Params p) {
+    __shared__ __align__(16) unsigned char lds[kRing * kTileB];
+    __shared__ int s_item;
+    __shared__ int s_flag;
+    if (threadIdx.x == 0) s_flag = 0;
+    uint32_t lds0 = (uint32_t)(uintptr_t)&lds[0];
+    asm volatile("" : "+s"(lds0));
+    const int home0 = blockIdx.x % kQueues;
+    // claim an item: the home queue first, then the others in turn
+    auto claim_any = [&](int q_first) {
+        for (int k = 0; k < kQueues; ++k) {
+            const int q = (q_first + k) % kQueues;
+            const int c = atomicAdd(p.head + q, 1);
+            if (p.head[kQueues + q] + c < p.head[2 * kQueues + q]) return (q << 24) | c;
+        }
+        return -1;
+    };
+    if (threadIdx.x == 0) s_item = claim_any(home0);
+    __syncthreads();
+    int cur = __builtin_amdgcn_readfirstlane(s_item);
+    while (cur >= 0) {
+        const int q = cur >> 24;
+        const int it = p.head[kQueues + q] + (cur & 0xffffff);
+        const int4 e0 = p.list[2 * it];
+        const int4 e1 = p.list[2 * it + 1];
+        int nxt = 0;  // index claimed from queue q near the end of the item
+        item(p, e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w, lds0, q, nxt, s_flag);
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            // the claim near the end came from queue q; past its end, look elsewhere
+            s_item = p.head[kQueues + q] + nxt < p.head[2 * kQueues + q] ? (q << 24) | nxt
+                                                                          : claim_any(q + 1);
+        }
+        __syncthreads();
+        cur = __builtin_amdgcn_readfirstlane(s_item);
+    }
+}
+
+// Combines the split partials of kMergeRows rows: 64 threads per row, eight
+// output dims each, splits in index order.
+constexpr int kMergeBatch = 8;
+__global__ __launch_bounds__(256) void mla_merge(Params p) {
+    constexpr int kSlotFloats = kRows * (kDv + 2);
+    const AttnArgs& a = p.a;
+    const int count = p.head[3 * kQueues];
+    const int tid = threadIdx.x;
+    for (int m = blockIdx.x; m < count; m += gridDim.x) {
+        const int4 e0 = p.mlist[2 * m];
+        const int4 e1 = p.mlist[2 * m + 1];
+        const int r = e0.x, g = e0.y, rb = e0.z;
+        const int q0 = e1.x, ql = e1.y, ns = e1.w;
+        const int rows = ql * p.group;
+        const int nrows = min(kRows, rows - rb * kRows);
+        const int mr = e0.w + (tid >> 6);
+        if (mr >= nrows) continue;
+        const int c8 = (tid & 63) * 8;
+        const float* base = p.part + ((int64_t)(r * a.Hkv + g) * p.rb_max + rb) * p.max_splits * kSlotFloats;
+        float M = -__builtin_huge_valf(), L = 0.0f;
+        f32x4 o0 = f32x4{0.f, 0.f, 0.f, 0.f}, o1 = o0;
+        for (int s0 = 0; s0 < ns; s0 += kMergeBatch) {
+            float ms[kMergeBatch], ls[kMergeBatch];
+            f32x4 a0[kMergeBatch], a1[kMergeBatch];
+#pragma unroll
+            for (int k = 0; k < kMergeBatch; ++k) {
+                const float* sl = base + (int64_t)min(s0 + k, ns - 1) * kSlotFloats;
+                ms[k] = sl[mr];
+                ls[k] = sl[kRows + mr];
+                a0[k] = *(const f32x4*)(sl + 2 * kRows + mr * kDv + c8);
+                a1[k] = *(const f32x4*)(sl + 2 * kRows + mr * kDv + c8 + 4);
+            }
+            float Mb = M;
+#pragma unroll
+            for (int k = 0; k < kMergeBatch; ++k)
+                if (s0 + k < ns) Mb = fmaxf(Mb, ms[k]);
+            if (M > -__builtin_huge_valf() && Mb != M) {
+                const float f = exp2f(M - Mb);
+                L *= f;
+                o0 *= f;
+                o1 *= f;
+            }
+            M = Mb;
+#pragma unroll
+            for (int k = 0; k < kMergeBatch; ++k) {
+                if (s0 + k >= ns) break;
+                const float f = ms[k] > -__builtin_huge_valf() ? exp2f(ms[k] - M) : 0.0f;
+                L += ls[k] * f;
+                o0 += f * a0[k];
+                o1 += f * a1[k];
+            }
+        }
+        const int row = rb * kRows + mr;
+        const int t = row / p.group;
+        const int h = g * p.group + (row - t * p.group);
+        const int64_t orow = (int64_t)(q0 + t) * a.Hq + h;
+        const float inv = 1.0f / L;
+        uint4 pk;
+        pk.x = pack2_bf16(o0[0] * inv, o0[1] * inv);
+        pk.y = pack2_bf16(o0[2] * inv, o0[3] * inv);
+        pk.z = pack2_bf16(o1[0] * inv, o1[1] * inv);
+        pk.w = pack2_bf16(o1[2] * inv, o1[3] * inv);
+        *(uint4*)((uint16_t*)a.out + orow * kDv + c8) = pk;
+        if (a.lse && c8 == 0) a.lse[orow] = (M + log2f(L)) * kLn2;
+    }
+}
+
+}  // namespace mla
+
+bool attn_mla_shape_ok(const AttnArgs& a) {
+    return a.bf16 && a.Dqk == mla::kDk && a.Dv == mla::kDv && a.Hq % a.Hkv == 0 &&
+           a.page >= 64 && (a.page & (a.page - 1)) == 0;
+}
+
+bool attn_mla_supported(const AttnArgs& a) {
+    const int64_t lim = (int64_t)1 << 30;
+    // values must be the first Dv dims of the key rows
+    return attn_mla_shape_ok(a) && a.v == a.k && a.vs[0] == a.ks[0] && a.vs[1] == a.ks[1] &&
+           a.vs[2] == a.ks[2] && a.ks[0] < lim && a.ks[1] < lim && a.ks[2] < lim &&
+           a.ks[0] % 8 == 0 && a.ks[1] % 8 == 0 && a.ks[2] % 8 == 0 &&
+           ((uintptr_t)a.q % 16) == 0 && ((uintptr_t)a.k % 16) == 0 && ((uintptr_t)a.out % 16) == 0;
+}
+
+size_t attn_mla_workspace(const AttnArgs& a) {
+    const mla::Geom g = mla::geom(a);
+    return g.head_bytes + g.list_bytes + g.mlist_bytes + g.part_bytes;
+}
+
+hipError_t launch_attn_mla(const AttnArgs& a, void* ws, hipStream_t s) {
+    const mla::Geom g = mla::geom(a);
+    mla::Params p;
+    p.a = a;
+    p.group = g.group;
+    p.rb_max = g.rb_max;
+    p.max_splits = g.max_splits;
+    p.page_shift = __builtin_ctz((unsigned)a.page);
+    p.s0b = (uint32_t)(a.ks[0] * 2);
+    p.s1b = (uint32_t)(a.ks[1] * 2);
+    p.s2b = (uint32_t)(a.ks[2] * 2);
+    p.scale2 = a.scale * mla::kLog2e;
+    p.head = (int*)ws;
+    p.list = (int4*)((char*)ws + g.head_bytes);
+    p.mlist = (int4*)((char*)ws + g.head_bytes + g.list_bytes);
+    p.part = (float*)((char*)ws + g.head_bytes + g.list_bytes + g.mlist_bytes);
+    hipLaunchKernelGGL(mla::mla_plan, dim3(1), dim3(mla::kPlanThreads), 0, s, p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    int dev = 0, cus = 0;
+    e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    // one workgroup per CU (114 KB of LDS, one wave per SIMD)
+    const int64_t grid = std::min<int64_t>(cus, std::max<int64_t>(g.n_items, 1));
+    hipLaunchKernelGGL(mla::mla_kernel, dim3((unsigned)grid), dim3(mla::kThreads), 0, s, p);
+    e = hipGetLastError();
+    if (e != hipSuccess || g.n_merge == 0) return e;
+    const int64_t mgrid = std::min<int64_t>((int64_t)cus * 16, g.n_merge);
+    hipLaunchKernelGGL(mla::mla_merge, dim3((unsigned)mgrid), dim3(256), 0, s, p);
+    return hipGetLastError();
+}
+
+}  // namespace dspark

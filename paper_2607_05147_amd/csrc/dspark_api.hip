@@ -4,9 +4,11 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <algorithm>
 #include <string>
 
 #include "dspark.h"
+
 #include "kernels.h"
 
 namespace {
@@ -146,9 +148,10 @@ size_t dspark_verify_attn_workspace_size(int R, int max_q, int Hq, int Hkv, int 
     dspark::AttnArgs a = make_attn(fake, fake, fake, ks, vs, nullptr, max_pages, nullptr, nullptr,
                                    R, max_q, Hq, Hkv, Dqk, Dv, page_size, 1.0f, dt, nullptr,
                                    nullptr);
-    const size_t m = dspark::attn_mfma_supported(a) ? dspark::attn_mfma_workspace(a) : 0;
-    const size_t gsz = dspark::attn_generic_workspace(a);
-    return m > gsz ? m : gsz;
+    size_t need = dspark::attn_generic_workspace(a);
+    if (dspark::attn_mfma_supported(a)) need = std::max(need, dspark::attn_mfma_workspace(a));
+    if (dspark::attn_mla_shape_ok(a)) need = std::max(need, dspark::attn_mla_workspace(a));
+    return need;
 }
 
 dspark_status dspark_verify_attn(const void* q, const void* k_cache, const void* v_cache,
@@ -177,14 +180,18 @@ dspark_status dspark_verify_attn(const void* q, const void* k_cache, const void*
     dspark::AttnArgs a = make_attn(q, k_cache, v_cache, k_strides, v_strides, block_table,
                                    max_pages, kv_len, cu_q, R, max_q, Hq, Hkv, Dqk, Dv, page_size,
                                    scale, dt, out, lse);
-    const bool mfma = dspark::attn_mfma_supported(a);
-    const size_t need = mfma ? dspark::attn_mfma_workspace(a) : dspark::attn_generic_workspace(a);
+    // matrix-core paths first: GQA head dim 128, then latent 576/512; else vector ALUs
+    const int path = dspark::attn_mfma_supported(a) ? 0 : (dspark::attn_mla_supported(a) ? 1 : 2);
+    const size_t need = path == 0 ? dspark::attn_mfma_workspace(a)
+                                  : (path == 1 ? dspark::attn_mla_workspace(a)
+                                               : dspark::attn_generic_workspace(a));
     if (ws_bytes < need || (need > 0 && !ws) || !aligned(ws, 256))
         return fail(DSPARK_EWORKSPACE, "workspace of %zu bytes (256-aligned) needed, got %zu",
                     need, ws_bytes);
     hipStream_t s = (hipStream_t)stream;
-    return hip_status(mfma ? dspark::launch_attn_mfma(a, ws, s)
-                           : dspark::launch_attn_generic(a, ws, s),
+    return hip_status(path == 0 ? dspark::launch_attn_mfma(a, ws, s)
+                                : (path == 1 ? dspark::launch_attn_mla(a, ws, s)
+                                             : dspark::launch_attn_generic(a, ws, s)),
                       "dspark_verify_attn");
 }
 

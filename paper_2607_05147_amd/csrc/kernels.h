@@ -34,6 +34,10 @@ struct AttnArgs {
 bool attn_mfma_supported(const AttnArgs& a);
 size_t attn_mfma_workspace(const AttnArgs& a);
 hipError_t launch_attn_mfma(const AttnArgs& a, void* ws, hipStream_t s);
+bool attn_mla_shape_ok(const AttnArgs& a);   // shape only (workspace sizing)
+bool attn_mla_supported(const AttnArgs& a);  // shape, value aliasing and alignment
+size_t attn_mla_workspace(const AttnArgs& a);
+hipError_t launch_attn_mla(const AttnArgs& a, void* ws, hipStream_t s);
 
 size_t attn_generic_workspace(const AttnArgs& a);
 hipError_t launch_attn_generic(const AttnArgs& a, void* ws, hipStream_t s);

@@ -71,6 +71,13 @@ def test_mla_reduced():
     _full_compare(w, 5, q_len=[3, 17], label="mla-small")
 
 
+def test_mla_split_contexts():
+    # several 8192-key splits per row block, ragged row blocks, partial last steps
+    base = synth.WORKLOADS["mla"]
+    w = synth.scaled(base, R=2, Hq=32, kv_dist=("uniform", 8200, 17000))
+    _full_compare(w, 7, q_len=[5, 2], label="mla-splits")
+
+
 def test_fp32_other_head_dims():
     base = synth.WORKLOADS["tiny"]
     for D, group in ((128, 8), (72, 1), (64, 16)):
@@ -113,6 +120,10 @@ def test_serving_full_size_sampled():
 
 def test_highconc_full_size_sampled():
     _sampled_compare("highconc", 0, n_per_req=1)
+
+
+def test_mla_full_size_sampled():
+    _sampled_compare("mla", 0, n_per_req=2)
 
 
 def test_repeatable_bitwise():
