@@ -457,7 +457,7 @@ __device__ __forceinline__ void item(const Params& p, const int r, const int g, 
         for (int ks = 0; ks < kKs; ++ks) {
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb) {
-                const bf16x8 kf = *(const lds_bf16x8*)(koff[ks & 1][mb] + boff + 128 * (ks >> 1));
+                const bf16x8 kf = *lds_ptr<const lds_bf16x8>(koff[ks & 1][mb] + boff + 128 * (ks >> 1));
 #pragma unroll
                 for (int j = 0; j < kTiles; ++j)
                     sc[j][mb][ks & 1] =
@@ -519,8 +519,8 @@ __device__ __forceinline__ void item(const Params& p, const int r, const int g, 
 #pragma unroll
         for (int db = 0; db < kDb; ++db) {
             const uint32_t vo = boff + 128 * (db >> 2);
-            const s16x4 h0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(voff[db & 3][0] + vo));
-            const s16x4 h1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(voff[db & 3][1] + vo));
+            const s16x4 h0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(lds_ptr<lds_s16x4>(voff[db & 3][0] + vo));
+            const s16x4 h1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(lds_ptr<lds_s16x4>(voff[db & 3][1] + vo));
             const bf16x8 vf = __builtin_bit_cast(
                 bf16x8, (short __attribute__((ext_vector_type(8)))){h0[0], h0[1], h0[2], h0[3],
                                                                      h1[0], h1[1], h1[2], h1[3]});

@@ -70,4 +70,10 @@ __device__ __forceinline__ void lds_barrier() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// Pointer into LDS (address space 3) from a 32-bit LDS byte address.
+template <typename T>
+__device__ __forceinline__ T* lds_ptr(uint32_t addr) {
+    return (T*)(uintptr_t)addr;
+}
+
 }  // namespace dspark
