@@ -29,6 +29,7 @@ import time
 import numpy as np
 
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak
 NCOPY = 3
 
 
@@ -65,6 +66,15 @@ def attention_bytes(w, kv_len: np.ndarray, q_len: np.ndarray) -> int:
     return kv + qo + bt
 
 
+def attention_flop(w, kv_len: np.ndarray, q_len: np.ndarray) -> int:
+    """Algorithmic FLOP of one verify-attention launch: query t of request r
+    scores and mixes kv_len - q_len + t + 1 keys (causal), Dqk + Dv MACs each."""
+    kv = kv_len.astype(np.int64)
+    ql = q_len.astype(np.int64)
+    keys = int((ql * (kv - ql) + ql * (ql + 1) // 2).sum())
+    return 2 * keys * w.Hq * (w.Dqk + w.Dv)
+
+
 def accept_bytes(w, q_len: np.ndarray, accepted: np.ndarray) -> int:
     """Algorithmic HBM bytes of one acceptance call: every verified logit row
     once, plus the draft row at the first rejection (stochastic)."""
@@ -76,9 +86,34 @@ def accept_bytes(w, q_len: np.ndarray, accepted: np.ndarray) -> int:
 
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-ATTN_SRC = os.path.join(HERE, "paper_2607_05147_amd", "csrc", "attn_mfma.hip")
-# the kernels of one dspark_verify_attn call on the MFMA path
-ATTN_KERNELS = ("mf_plan", "attn_mfma_kernel", "attn_mfma_merge")
+CSRC = os.path.join(HERE, "paper_2607_05147_amd", "csrc")
+# The launches of one dspark_verify_attn call per attention path, the source
+# they come from and the roofline that bounds the main kernel.
+ATTN_PATHS = {
+    "gqa": {"src": "attn_mfma.hip", "kernels": ("mf_plan", "attn_mfma_kernel", "attn_mfma_merge"),
+            "bound": "hbm"},
+    "latent": {"src": "attn_mla.hip", "kernels": ("mla_plan", "mla_kernel", "mla_merge"),
+               "bound": "mfma"},
+    "generic": {"src": "attn_generic.hip", "kernels": ("attn_generic_kernel", "attn_generic_merge"),
+                "bound": "hbm"},
+}
+
+
+def attn_path(w, bf16: bool) -> str:
+    """Which kernels dspark_verify_attn runs for the workload (the library's
+    own dispatch conditions; the bench's V aliases K on latent shapes)."""
+    pow2 = w.page >= 64 and (w.page & (w.page - 1)) == 0
+    if bf16 and w.Dqk == 128 and w.Dv == 128 and pow2:
+        return "gqa"
+    if bf16 and w.mla and w.Dqk == 576 and w.Dv == 512 and pow2:
+        return "latent"
+    return "generic"
+
+
+def path_of_workload(name: str) -> str:
+    import paper_2607_05147_amd.synth as synth
+    w = synth.WORKLOADS[name]
+    return attn_path(w, w.kv_elem_bytes == 2)
 
 
 def traffic_file(workload: str) -> str:
@@ -106,6 +141,8 @@ def traffic_from(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, workload=
     """Per-call HBM traffic of dspark_verify_attn from FETCH_SIZE / WRITE_SIZE
     (KiB per dispatch), each scaled by what the same counter reads for a plain
     1 GiB device copy; written next to the other profile summaries."""
+    path = ATTN_PATHS[path_of_workload(workload)]
+    kernels = path["kernels"]
     def copy_scale(path):
         vals = [v for name, v in _counter_rows(path) if "copyBuffer" in name or "copy" in name.lower()]
         vals = [v for v in vals if v > 1e5]  # the 1 GiB copies
@@ -113,30 +150,30 @@ def traffic_from(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, workload=
 
     def per_call(path):
         rows = _counter_rows(path)
-        calls = sum(1 for name, _ in rows if "attn_mfma_kernel" in name)
-        tot = {k: sum(v for name, v in rows if k in name) for k in ATTN_KERNELS}
-        return {k: tot[k] / calls * 1024.0 for k in ATTN_KERNELS}, calls
+        calls = sum(1 for name, _ in rows if kernels[1] in name)
+        tot = {k: sum(v for name, v in rows if k in name) for k in kernels}
+        return {k: tot[k] / calls * 1024.0 for k in kernels}, calls
 
     sf, sw = copy_scale(copy_fetch_csv), copy_scale(copy_write_csv)
     fetch, calls = per_call(fetch_csv)
     write, _ = per_call(write_csv)
     out = {
         "workload": workload,
-        "kernels": list(ATTN_KERNELS),
+        "kernels": list(kernels),
         "calls": calls,
         "copy_scale": {"FETCH_SIZE": sf, "WRITE_SIZE": sw},
         "fetch_bytes_per_call": {k: v * sf for k, v in fetch.items()},
         "write_bytes_per_call": {k: v * sw for k, v in write.items()},
         "bytes_per_call": sum(fetch.values()) * sf + sum(write.values()) * sw,
-        "source_sha256": source_sha(ATTN_SRC),
+        "source_sha256": source_sha(os.path.join(CSRC, path["src"])),
         "commands": [
-            "rocprofv3 --pmc FETCH_SIZE --output-format csv -d <dir> -o pmc -- python bench.py "
-            "--steps 5 --warmup 1 --no-cpu-baseline",
-            "rocprofv3 --pmc WRITE_SIZE --output-format csv -d <dir> -o pmc -- python bench.py "
-            "--steps 5 --warmup 1 --no-cpu-baseline",
+            f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d <dir> -o pmc -- python bench.py "
+            f"--workload {workload} --steps 5 --warmup 1 --no-cpu-baseline",
+            f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d <dir> -o pmc -- python bench.py "
+            f"--workload {workload} --steps 5 --warmup 1 --no-cpu-baseline",
             "rocprofv3 --pmc FETCH_SIZE --output-format csv -d <dir> -o pmc -- python bench.py --copy-probe",
             "rocprofv3 --pmc WRITE_SIZE --output-format csv -d <dir> -o pmc -- python bench.py --copy-probe",
-            "python bench.py --traffic-from <the four pmc_counter_collection.csv files>",
+            f"python bench.py --workload {workload} --traffic-from <the four pmc_counter_collection.csv files>",
         ],
     }
     os.makedirs(os.path.dirname(traffic_file(workload)), exist_ok=True)
@@ -154,7 +191,8 @@ def measured_traffic(workload: str):
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("source_sha256") != source_sha(ATTN_SRC):
+    src = os.path.join(CSRC, ATTN_PATHS[path_of_workload(workload)]["src"])
+    if t.get("source_sha256") != source_sha(src):
         return None
     return t["bytes_per_call"]
 
@@ -177,14 +215,15 @@ def copy_probe():
 def main():
     args = parse()
     if args.traffic_from:
-        traffic_from(*args.traffic_from)
+        traffic_from(*args.traffic_from, workload=args.workload)
         return
     if args.copy_probe:
         copy_probe()
         return
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only (--gpus {args.gpus} requested); "
-              "the multi-GPU layout is described in DESIGN.md", file=sys.stderr)
+        print(f"bench.py measures one GPU (--gpus {args.gpus} requested): the verify step "
+              "shards by request across GPUs with no exchange, so N GPUs run N copies of "
+              "this step", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -288,14 +327,16 @@ def main():
     ms_per_step = wall * 1e3 / args.steps
 
     ab = attention_bytes(w, kv.kv_len, q_len)
-    mfma = bf16 and w.Dqk == 128 and w.Dv == 128 and w.page >= 64
+    path = attn_path(w, bf16)
+    af = attention_flop(w, kv.kv_len, q_len)
     cb = accept_bytes(w, q_len, accepted)
     attn_s = attn_ms.mean() / 1e3
     acc_s = acc_ms.mean() / 1e3
     attn_gbps = ab / attn_s / 1e9
     both_gbps = (ab + cb) / (attn_s + acc_s) / 1e9
+    attn_tflops = af / attn_s / 1e12
     log(f"per step: schedule {sched_ms.mean() * 1e3:.1f} us, attention {attn_ms.mean() * 1e3:.1f} us "
-        f"({attn_gbps:.0f} GB/s), accept {acc_ms.mean() * 1e3:.1f} us; "
+        f"({attn_gbps:.0f} GB/s, {attn_tflops:.1f} TFLOP/s), accept {acc_ms.mean() * 1e3:.1f} us; "
         f"attention+accept {both_gbps:.0f} GB/s = {both_gbps / HBM_PEAK_GBPS:.1%} of peak")
 
     result = {
@@ -328,18 +369,32 @@ def main():
         "emitted_tokens_per_s": float((accepted + 1).sum()) / (ms_per_step / 1e3),
         # the dominant kernel: one dspark_verify_attn call (plan, attention and
         # split-merge launches, bracketed together by the events)
-        "roofline": {"kernel": ("dspark_verify_attn: " + " + ".join(ATTN_KERNELS)) if mfma
-                               else "dspark_verify_attn: attn_generic_kernel + merge",
-                     "bound": "hbm", "achieved": attn_gbps, "peak": HBM_PEAK_GBPS,
-                     "unit": "GB/s", "frac": attn_gbps / HBM_PEAK_GBPS,
-                     "bytes_per_launch": ab,
-                     "traffic": measured_traffic(w.name) if mfma else None},
+        "roofline": roofline_entry(w.name, path, ab, af, attn_s),
     }
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, seed, conf, sps, ln, kv, q, logits, dr,
                                               args.cpu_seconds)
     print(json.dumps(result), flush=True)
+
+
+def roofline_entry(workload: str, path: str, nbytes: int, flop: int, seconds: float) -> dict:
+    """Roofline of one dspark_verify_attn call (its plan, attention and merge
+    launches, bracketed together by the events): HBM-bound paths report
+    algorithmic bytes per second against the HBM peak, the latent path FLOP per
+    second against the dense bf16 matrix peak."""
+    info = ATTN_PATHS[path]
+    out = {"kernel": "dspark_verify_attn: " + " + ".join(info["kernels"]), "bound": info["bound"]}
+    if info["bound"] == "mfma":
+        achieved = flop / seconds / 1e12
+        out.update({"achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "flop_per_launch": flop})
+    else:
+        achieved = nbytes / seconds / 1e9
+        out.update({"achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                    "frac": achieved / HBM_PEAK_GBPS, "bytes_per_launch": nbytes})
+    out["traffic"] = measured_traffic(workload) if path != "generic" else None
+    return out
 
 
 def cpu_baseline(w, seed, conf, sps, ln, kv, q, logits, dr, target_s):

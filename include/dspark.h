@@ -122,8 +122,15 @@ dspark_status dspark_schedule(const float* conf, int R, int K, const double* sps
  *             scaled scores.
  *   dt        element type of q, k_cache, v_cache and out.
  *   Supported: Hq % Hkv == 0; Dqk, Dv multiples of 8 up to 576;
- *   page_size multiple of 16.  bf16 with Dqk == Dv == 128 and page_size a
- *   power of two >= 64 runs on MFMA tiles; other shapes run on vector ALUs.
+ *   page_size multiple of 16.  Which kernels run (results agree within the
+ *   bf16 tolerance either way):
+ *     - bf16, Dqk == Dv == 128, page_size a power of two >= 64, strides
+ *       multiples of 8 elements, q/k/v 16-byte aligned: MFMA tiles, HBM-bound;
+ *     - bf16, Dqk == 576, Dv == 512 (latent head), v_cache == k_cache with
+ *       identical strides (values are the first 512 dims of the key rows),
+ *       page_size a power of two >= 64, strides multiples of 8 elements,
+ *       q/k/out 16-byte aligned: MFMA tiles, bound by the matrix cores;
+ *     - anything else: vector ALUs.
  * ---------------------------------------------------------------------- */
 size_t dspark_verify_attn_workspace_size(int R, int max_q, int Hq, int Hkv, int Dqk, int Dv,
                                          int max_pages, int page_size, dspark_dtype dt);

@@ -20,7 +20,27 @@ pytestmark = pytest.mark.gpu
 TOL = {"f32": 1e-5, "bf16": 2e-2}
 
 
-def _full_compare(w, seed, q_len=None, label=""):
+def _scale_keys_after(kv, first, factor):
+    """Multiplies every cached key (and aliased value) of each request except
+    its first `first` tokens by `factor`, a power of two (exact in bf16)."""
+    P = kv.k.shape[2]
+    for r in range(len(kv.kv_len)):
+        npg = (int(kv.kv_len[r]) + P - 1) // P
+        for i in range(npg):
+            lo = max(0, first - i * P)
+            if lo >= P:
+                continue
+            pg = kv.block_table[r, i]
+            for arr in {id(kv.k): kv.k, id(kv.v): kv.v}.values():
+                blk = arr[pg, :, lo:, :]
+                if arr.dtype == np.uint16:
+                    f = (blk.astype(np.uint32) << 16).view(np.float32) * np.float32(factor)
+                    arr[pg, :, lo:, :] = (f.view(np.uint32) >> 16).astype(np.uint16)
+                else:
+                    arr[pg, :, lo:, :] = blk * np.float32(factor)
+
+
+def _full_compare(w, seed, q_len=None, label="", kv_fn=None):
     if q_len is None:
         case = guard.schedule_case(w, seed)
         cu = case.cu_q
@@ -28,6 +48,8 @@ def _full_compare(w, seed, q_len=None, label=""):
         cu = oracle.cu_from_len(np.asarray(q_len) - 1)
     qlen = np.diff(cu)
     kv = synth.paged_kv(w, seed)
+    if kv_fn is not None:
+        kv_fn(kv)
     q = synth.query_rows(w, seed, synth.flat_keys(qlen))
     log(f"[attn] {label} {w.name} R={w.R} Hq={w.Hq}/{w.Hkv} D={w.Dqk}/{w.Dv} "
         f"total_q={int(cu[-1])} kv={int(kv.kv_len.min())}..{int(kv.kv_len.max())}")
@@ -76,6 +98,32 @@ def test_mla_split_contexts():
     base = synth.WORKLOADS["mla"]
     w = synth.scaled(base, R=2, Hq=32, kv_dist=("uniform", 8200, 17000))
     _full_compare(w, 7, q_len=[5, 2], label="mla-splits")
+
+
+def test_mla_reference_rerun():
+    # keys past each request's first 32 score about 16x higher, far above the
+    # first step's maximum (the per-row softmax reference) plus 2^32, so every
+    # row block, including both splits of the long request, runs again with
+    # the observed maxima
+    base = synth.WORKLOADS["mla"]
+    w = synth.scaled(base, R=2, Hq=16, kv_dist=("uniform", 200, 9000))
+    seed, first = 0, 32
+    assert synth.kv_lengths(w, seed).max() > 8192  # two splits
+
+    def scale_and_check(kv):
+        _scale_keys_after(kv, first, 16.0)
+        # precondition: request 1's last query, head 0, scores (log2 units)
+        # past the first step exceed the first step's maximum by more than 32
+        cu = oracle.cu_from_len(np.array([3, 8]))
+        qb = synth.query_rows(w, seed, synth.flat_keys(np.diff(cu)))[int(cu[2]) - 1, 0]
+        q = synth.bf16_bits_to_f32(qb).astype(np.float64)
+        n = int(kv.kv_len[1])
+        keys = np.stack([synth.bf16_bits_to_f32(kv.k[kv.block_table[1, j // w.page], 0, j % w.page])
+                         for j in range(n)]).astype(np.float64)
+        s2 = keys @ q * w.scale / np.log(2.0)
+        assert s2[first:].max() > s2[:first].max() + 32
+
+    _full_compare(w, seed, q_len=[4, 9], label="mla-rerun", kv_fn=scale_and_check)
 
 
 def test_fp32_other_head_dims():
