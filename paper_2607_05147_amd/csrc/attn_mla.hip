@@ -50,8 +50,9 @@ constexpr int kDk = 576;
 constexpr int kDv = 512;
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
-constexpr int kTiles = 1;                           // 16-row tiles per wave
-constexpr int kRows = 16 * kTiles * kWaves;         // 64 rows per work item
+constexpr int kRows = 64;                           // rows per work item: four 16-row tiles
+constexpr int kTilesPV = kRows / 16;                // tiles of the value product (all, per wave)
+constexpr int kSTiles = 2;                          // tiles of the score product per wave
 constexpr int kStep = 32;                           // keys per step
 constexpr int kRing = 3;                            // LDS buffers; copies run 2 steps ahead
 constexpr int kChunks = kDk / 8;                    // 72 16-byte chunks of a cache row
@@ -65,10 +66,12 @@ constexpr int kSplit = 8192;                        // keys per split (the last 
 constexpr int kPageRegs = kSplit / 64 / DSPARK_WAVE;  // page-id registers per lane (pages >= 64 keys)
 constexpr int kKs = kDk / 32;                       // 18 slices of the score product
 constexpr int kDb = kDv / 16;                       // 32 blocks of output dims
+constexpr int kDbW = kDb / kWaves;                  // 8 blocks (128 dims) per wave
 constexpr int kQueues = 8;                          // one per XCD
 constexpr int kBins = kSplit / kStep + 1;           // item lengths in steps: 0 .. kSplit / 32
 constexpr int kMergeRows = 4;                       // rows per merge item (64 threads per row)
-constexpr int kAhead = 8;                           // LDS operand reads in flight ahead of the products
+constexpr int kAheadK = 6;                          // K fragment reads in flight ahead of the products
+constexpr int kAheadV = 8;                          // transposing V reads in flight ahead of the products
 constexpr int kSchedMfma = 0x008;                   // sched_group_barrier classes
 constexpr int kSchedDsRead = 0x100;
 constexpr float kLog2e = 1.4426950408889634f;
@@ -296,25 +299,39 @@ __global__ __launch_bounds__(kPlanThreads) void mla_plan(Params p) {
 
 // ------------------------------------------------------------------ item
 
+// LDS beside the copy ring: the probability exchange of every step and the
+// per-row statistics the waves of a row pair combine.
+struct Shared {
+    uint2 p[kTilesPV][2][DSPARK_WAVE];  // [row tile][key block][lane]: 4 bf16 probabilities
+    float mx[kWaves][kSTiles][16];      // row maxima (reference, observed maximum) per wave
+    float ls[kWaves][kSTiles][16];      // row sums per wave
+    int lim[kWaves];                    // per-wave minimum causal limit
+};
+
 __device__ __forceinline__ void item(const Params& p, const int r, const int g, const int rb,
                                      const int s, const int q0, const int ql, const int kv,
                                      const int nsplit, const uint32_t lds0, const int home,
-                                     int& nxt, int& s_flag) {
+                                     int& nxt, int& s_flag, Shared& sh) {
     const AttnArgs& a = p.a;
     constexpr int kSlotFloats = kRows * (kDv + 2);
     const int rows = ql * p.group;
     const int row0 = rb * kRows;
     int start, end;
     split_range(kv, s, start, end);
-    const int nrows = min(kRows, rows - row0);
-    const int nt = (nrows + 15) >> 4;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lr = lane & 15;
     const int lq = lane >> 4;
-    const int nt_w = min(max(nt - kTiles * wave, 0), kTiles);  // tiles 2w, 2w + 1
+    // Roles.  Scores: row tiles 2 hs and 2 hs + 1 (32 rows) against key block
+    // kb of every step (keys 8 i + 4 kb + 0..3), so each K fragment feeds two
+    // products.  Values: output dims [128 wave, 128 wave + 128) of all four row
+    // tiles, so each V fragment feeds four products; the probabilities of the
+    // other waves come through LDS.
+    const int hs = wave >> 1;
+    const int kb = wave & 1;
+    const int partner = wave ^ 1;  // same rows, the other key block
 
     const uint16_t* __restrict__ qg = (const uint16_t*)a.q;
     const uint16_t* __restrict__ kc = (const uint16_t*)a.k;
@@ -329,13 +346,15 @@ __device__ __forceinline__ void item(const Params& p, const int r, const int g, 
         my_page[k] = i < npg ? a.block_table[(int64_t)r * a.max_pages + pg0 + i] : 0;
     }
 
-    // ---- query fragments (B operand of S^T = K Q^T) and causal limits
-    bf16x8 qf[kTiles][kKs];
-    int lim[kTiles];
+    // ---- query fragments (B operand of S^T = K Q^T) and causal limits of the
+    // two score tiles; rows past the block's end get zero queries (finite
+    // scores, outputs never stored)
+    bf16x8 qf[kSTiles][kKs];
+    int lim[kSTiles];
     int lim_min = 0x7fffffff;
 #pragma unroll
-    for (int j = 0; j < kTiles; ++j) {
-        const int row = row0 + 16 * (kTiles * wave + j) + lr;
+    for (int j = 0; j < kSTiles; ++j) {
+        const int row = row0 + 16 * (kSTiles * hs + j) + lr;
         if (row < rows) {
             const int t = row / p.group;
             const int h = g * p.group + (row - t * p.group);
@@ -343,59 +362,68 @@ __device__ __forceinline__ void item(const Params& p, const int r, const int g, 
 #pragma unroll
             for (int ks = 0; ks < kKs; ++ks) qf[j][ks] = *(const bf16x8*)(qp + 32 * ks);
             lim[j] = kv - ql + t;
-            if (j < nt_w) lim_min = min(lim_min, lim[j]);
+            lim_min = min(lim_min, lim[j]);
         } else {
 #pragma unroll
             for (int ks = 0; ks < kKs; ++ks) qf[j][ks] = bf16x8{};
             lim[j] = -1;
         }
     }
-    lim_min = __reduce_min_sync(~0ull, lim_min);
-
-    // Softmax reference per row: exp2 is taken relative to mref, the row's first
-    // finite maximum, and the accumulators are never rescaled.  fp32 holds the
-    // probabilities comfortably while scores stay below mref + kRange; if one
-    // goes above (mobs tracks the maximum), the item is run again with
-    // mref = mobs.  Keeping the accumulators out of every VALU operation lets
-    // them stay in the accumulation registers.
-    f32x4 acc[kTiles][kDb];
-    float mref[kTiles], mobs[kTiles], lsum[kTiles];
+    // The second tile's fragments live in the accumulation registers (the
+    // products read their B operand from there directly), which leaves the
+    // vector registers for the operand pipeline.
 #pragma unroll
-    for (int j = 0; j < kTiles; ++j) mref[j] = mobs[j] = -__builtin_huge_valf();
+    for (int ks = 0; ks < kKs; ++ks) asm volatile("" : "+a"(qf[1][ks]));
+    // the whole block's minimum: steps below it need no masks
+    lim_min = __reduce_min_sync(~0ull, lim_min);  // whole wave: a collective
+    if (lane == 0) sh.lim[wave] = lim_min;
+    __syncthreads();
+    lim_min = min(min(sh.lim[0], sh.lim[1]), min(sh.lim[2], sh.lim[3]));
+
+    // Softmax reference per row: exp2 is taken relative to mref and the
+    // accumulators are never rescaled.  mref is the maximum of the item's first
+    // step over both key blocks (the two waves of a row pair exchange their
+    // halves), so both use the same reference.  fp32 holds the probabilities
+    // comfortably while scores stay below mref + kRange; if one goes above
+    // (mobs tracks the maximum), the item runs again with mref = the row's
+    // observed maximum.  Keeping the accumulators out of every VALU operation
+    // lets them stay in the accumulation registers.
+    f32x4 acc[kTilesPV][kDbW];
+    float mref[kSTiles], mobs[kSTiles], lsum[kSTiles];
+#pragma unroll
+    for (int j = 0; j < kSTiles; ++j) mref[j] = mobs[j] = -__builtin_huge_valf();
     bool over = false;  // some row of this wave went above mref + kRange
 
     // ---- per-lane LDS offsets of the operand fragments (loop invariant)
-    // K (A operand): rows 8 (lr / 4) + 4 mb + lr % 4 (so that the score
+    // K (A operand): rows 8 (lr / 4) + 4 kb + lr % 4 (so that the score
     // accumulator is the B operand of the value product), chunk 4 ks + lq;
     // the swizzle sees ks only through its parity
-    uint32_t koff[2][2];  // [ks % 2][mb], + 128 (ks / 2)
+    uint32_t koff[2];  // [ks % 2], + 128 (ks / 2)
 #pragma unroll
-    for (int kp = 0; kp < 2; ++kp)
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb) {
-            const int t = 8 * (lr >> 2) + 4 * mb + (lr & 3);
-            koff[kp][mb] = lds0 + t * kRowB + pchunk(t, 4 * kp + lq) * 16;
-        }
+    for (int kp = 0; kp < 2; ++kp) {
+        const int t = 8 * (lr >> 2) + 4 * kb + (lr & 3);
+        koff[kp] = lds0 + t * kRowB + pchunk(t, 4 * kp + lq) * 16;
+    }
     // V^T (A operand of the value product, transposing reads): rows
-    // 8 lq + 4 h + lr / 4, chunk 2 db + (lr % 4) / 2, half lr % 2; the chunk
-    // swizzle sees db only through db % 4
-    uint32_t voff[4][2];  // [db % 4][h], + 128 (db / 4)
+    // 8 lq + 4 h + lr / 4, chunk 2 db + (lr % 4) / 2, half lr % 2, for the
+    // wave's blocks db = 8 wave + d; the swizzle sees db only through db % 4
+    uint32_t voff[4][2];  // [d % 4][h], + 128 (d / 4)
 #pragma unroll
     for (int dq = 0; dq < 4; ++dq)
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             const int t = 8 * lq + 4 * h + (lr >> 2);
             const int c = 2 * dq + ((lr & 3) >> 1);
-            voff[dq][h] = lds0 + t * kRowB + pchunk(t, c) * 16 + (lr & 1) * 8;
+            voff[dq][h] = lds0 + t * kRowB + pchunk(t, c) * 16 + (lr & 1) * 8 + 256 * wave;
         }
+    // probability fragments: this wave writes [2 hs + j][kb][lane], reads [ti][0 / 1][lane]
+    uint2* const pw0 = &sh.p[kSTiles * hs][kb][lane];
+    const uint2* const pr0 = &sh.p[0][0][lane];
 
     // ---- copy geometry: this wave's copy instructions cover tile chunks
     // p = (first + i) * 64 + lane, row p / 72, physical chunk p % 72
     const int first = kCopies * wave;
-    // row and source chunk of copy i; the swizzle is an involution.  `ln` is
-    // the lane id passed through an empty asm at every use so that the
-    // geometry is recomputed per step (a few VALU operations) instead of being
-    // hoisted into registers that the operand pipeline needs.
+    // row and source chunk of copy i; the swizzle is an involution
     auto cp_at = [&](int i, int ln, int& t, int& c) {
         const int pp = (first + i) * 64 + ln;
         t = pp / kRowChunks;
@@ -412,23 +440,32 @@ __device__ __forceinline__ void item(const Params& p, const int r, const int g, 
             if ((idx >> 6) == k) pg = __builtin_amdgcn_readlane(my_page[k], idx & 63);
         return pg;
     };
+    // byte offsets of the copies of a whole step from its first key row; they
+    // live in the accumulation registers (one read each per step) so that
+    // neither the geometry arithmetic nor nine vector registers are spent per step
+    uint32_t cpo[kCopies];
+#pragma unroll
+    for (int i = 0; i < kCopies; ++i) {
+        int t, c;
+        cp_at(i, lane, t, c);
+        cpo[i] = t * p.s2b + 16 * c;
+    }
     auto issue = [&](int n) {
         const int tok0 = start + n * kStep;
         const int pidx = min((tok0 >> p.page_shift) - pg0, kPageRegs * DSPARK_WAVE - 1);
         const int page = page_of(pidx);
         const int slot0 = tok0 & ((1 << p.page_shift) - 1);
         const uint32_t dst = lds_wave + ((unsigned)n % kRing) * kTileB;
-        int ln = lane;
-        asm volatile("" : "+v"(ln));
         if (tok0 + kStep <= end) {
             const uint64_t kb = kc_head + (uint64_t)(uint32_t)page * p.s0b + (uint32_t)slot0 * p.s2b;
 #pragma unroll
             for (int i = 0; i < kCopies; ++i) {
-                int t, c;
-                cp_at(i, ln, t, c);
-                lds_copy16_s(kb, t * p.s2b + 16 * c, dst + i * 1024);
+                asm volatile("" : "+a"(cpo[i]));  // stays in (and is read from) an AGPR
+                lds_copy16_s(kb, cpo[i], dst + i * 1024);
             }
         } else {
+            int ln = lane;
+            asm volatile("" : "+v"(ln));
             // last, partial step or past the end: keys at or past the end read the zero row
             const uint16_t* kb = kc + (int64_t)page * a.ks[0] + (int64_t)g * a.ks[1];
 #pragma unroll
@@ -442,100 +479,104 @@ __device__ __forceinline__ void item(const Params& p, const int r, const int g, 
         }
     };
 
-    auto compute = [&](int n, auto bufc) {
+    auto compute = [&](int n, bool first_step, auto bufc) {
         constexpr unsigned buf = decltype(bufc)::value;
         constexpr uint32_t boff = buf * kTileB;
         const int tok0 = start + n * kStep;
-        // ---- scores S^T[key, row]: four accumulation chains (ks parity, key block)
-        f32x4 sc[kTiles][2][2];
+        // ---- scores S^T[key, row] of the two tiles: four accumulation chains
+        f32x4 sc[kSTiles][2];
 #pragma unroll
-        for (int j = 0; j < kTiles; ++j)
-#pragma unroll
-            for (int mb = 0; mb < 2; ++mb) sc[j][mb][0] = sc[j][mb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < kSTiles; ++j) sc[j][0] = sc[j][1] = f32x4{0.f, 0.f, 0.f, 0.f};
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int ks = 0; ks < kKs; ++ks) {
+            const bf16x8 kf = *lds_ptr<const lds_bf16x8>(koff[ks & 1] + boff + 128 * (ks >> 1));
 #pragma unroll
-            for (int mb = 0; mb < 2; ++mb) {
-                const bf16x8 kf = *lds_ptr<const lds_bf16x8>(koff[ks & 1][mb] + boff + 128 * (ks >> 1));
-#pragma unroll
-                for (int j = 0; j < kTiles; ++j)
-                    sc[j][mb][ks & 1] =
-                        __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[j][ks], sc[j][mb][ks & 1], 0, 0, 0);
-            }
+            for (int j = 0; j < kSTiles; ++j)
+                sc[j][ks & 1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[j][ks], sc[j][ks & 1], 0, 0, 0);
         }
-        // software pipeline: kAhead fragment reads in flight ahead of the products
-        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, kAhead, 0);
+        // software pipeline: kAheadK fragment reads in flight ahead of the products
+        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, kAheadK, 0);
 #pragma unroll
-        for (int i = 0; i < 2 * kKs - kAhead; ++i) {
-            __builtin_amdgcn_sched_group_barrier(kSchedMfma, kTiles, 0);
+        for (int i = 0; i < kKs - kAheadK; ++i) {
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, kSTiles, 0);
             __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
         }
-        __builtin_amdgcn_sched_group_barrier(kSchedMfma, kTiles * kAhead, 0);
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, kSTiles * kAheadK, 0);
         __builtin_amdgcn_sched_barrier(0);
-        // ---- online softmax; keys of this lane: tok0 + 8 lq + 4 mb + e
+
+        // ---- softmax over this wave's keys: tok0 + 8 lq + 4 kb + e
         const bool full = tok0 + kStep <= end && tok0 + kStep - 1 <= lim_min;
-        // (a tile past the block's rows has zero queries: finite scores, outputs never stored)
-        bf16x8 pf[kTiles];
+        float sv[kSTiles][4], bm[kSTiles];
 #pragma unroll
-        for (int j = 0; j < kTiles; ++j) {
-            {
-                float sv[8];
+        for (int j = 0; j < kSTiles; ++j) {
 #pragma unroll
-                for (int mb = 0; mb < 2; ++mb)
+            for (int e = 0; e < 4; ++e) sv[j][e] = sc[j][0][e] + sc[j][1][e];
+            if (!full) {
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) sv[4 * mb + e] = sc[j][mb][0][e] + sc[j][mb][1][e];
-                if (!full) {
-#pragma unroll
-                    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            const int key = tok0 + 8 * lq + 4 * mb + e;
-                            if (!(key < end && key <= lim[j])) sv[4 * mb + e] = -__builtin_huge_valf();
-                        }
+                for (int e = 0; e < 4; ++e) {
+                    const int key = tok0 + 8 * lq + 4 * kb + e;
+                    if (!(key < end && key <= lim[j])) sv[j][e] = -__builtin_huge_valf();
                 }
-                float bm = vmax(vmax(vmax(sv[0], sv[1]), sv[2]),
-                                vmax(vmax(sv[3], sv[4]), vmax(vmax(sv[5], sv[6]), sv[7])));
-                bm = row_max4(bm) * p.scale2;
-                mobs[j] = vmax(mobs[j], bm);
-                // the first finite maximum becomes the reference (nothing accumulated yet)
-                if (mref[j] == -__builtin_huge_valf()) mref[j] = bm;
-                over |= bm > mref[j] + kRange;
-                const float mu = mref[j] == -__builtin_huge_valf() ? 0.0f : mref[j];
-                float pr[8];
-#pragma unroll
-                for (int k = 0; k < 8; ++k) pr[k] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[k], p.scale2, -mu));
-                lsum[j] += ((pr[0] + pr[1]) + (pr[2] + pr[3])) + ((pr[4] + pr[5]) + (pr[6] + pr[7]));
-                u32x4 pk;
-                pk[0] = cvt_pk_bf16(pr[0], pr[1]);
-                pk[1] = cvt_pk_bf16(pr[2], pr[3]);
-                pk[2] = cvt_pk_bf16(pr[4], pr[5]);
-                pk[3] = cvt_pk_bf16(pr[6], pr[7]);
-                pf[j] = __builtin_bit_cast(bf16x8, pk);
             }
+            bm[j] = row_max4(vmax(vmax(sv[j][0], sv[j][1]), vmax(sv[j][2], sv[j][3]))) * p.scale2;
+            mobs[j] = vmax(mobs[j], bm[j]);
         }
-        // ---- O^T[d, row] += V^T P^T
-        __builtin_amdgcn_sched_barrier(0);
+        if (first_step) {
+            // the reference: the first step's maximum over both key blocks
+            if (lq == 0) {
 #pragma unroll
-        for (int db = 0; db < kDb; ++db) {
-            const uint32_t vo = boff + 128 * (db >> 2);
-            const s16x4 h0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(lds_ptr<lds_s16x4>(voff[db & 3][0] + vo));
-            const s16x4 h1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(lds_ptr<lds_s16x4>(voff[db & 3][1] + vo));
+                for (int j = 0; j < kSTiles; ++j) sh.mx[wave][j][lr] = bm[j];
+            }
+            lds_barrier();
+#pragma unroll
+            for (int j = 0; j < kSTiles; ++j) mref[j] = vmax(bm[j], sh.mx[partner][j][lr]);
+        }
+#pragma unroll
+        for (int j = 0; j < kSTiles; ++j) {
+            // rows with no visible key yet (only rows past the block's end can
+            // see keys later): take the first finite maximum
+            if (mref[j] == -__builtin_huge_valf()) mref[j] = bm[j];
+            over |= bm[j] > mref[j] + kRange;
+            const float mu = mref[j] == -__builtin_huge_valf() ? 0.0f : mref[j];
+            float pr[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) pr[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[j][e], p.scale2, -mu));
+            lsum[j] += (pr[0] + pr[1]) + (pr[2] + pr[3]);
+            pw0[j * 2 * DSPARK_WAVE] = uint2{cvt_pk_bf16(pr[0], pr[1]), cvt_pk_bf16(pr[2], pr[3])};
+        }
+        lds_barrier();  // every wave's probabilities visible
+
+        // ---- O^T[d, row] += V^T P^T for dims [128 wave, +128) of all four tiles
+        __builtin_amdgcn_sched_barrier(0);
+        bf16x8 pf[kTilesPV];
+#pragma unroll
+        for (int ti = 0; ti < kTilesPV; ++ti) {
+            const uint2 lo = pr0[ti * 2 * DSPARK_WAVE];
+            const uint2 hi = pr0[ti * 2 * DSPARK_WAVE + DSPARK_WAVE];
+            pf[ti] = __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, hi.x, hi.y});
+        }
+#pragma unroll
+        for (int d = 0; d < kDbW; ++d) {
+            const uint32_t vo = boff + 128 * (d >> 2);
+            const s16x4 h0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(lds_ptr<lds_s16x4>(voff[d & 3][0] + vo));
+            const s16x4 h1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(lds_ptr<lds_s16x4>(voff[d & 3][1] + vo));
             const bf16x8 vf = __builtin_bit_cast(
                 bf16x8, (short __attribute__((ext_vector_type(8)))){h0[0], h0[1], h0[2], h0[3],
                                                                      h1[0], h1[1], h1[2], h1[3]});
 #pragma unroll
-            for (int j = 0; j < kTiles; ++j)
-                acc[j][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[j], acc[j][db], 0, 0, 0);
+            for (int ti = 0; ti < kTilesPV; ++ti)
+                acc[ti][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[ti], acc[ti][d], 0, 0, 0);
         }
-        // software pipeline: two transposing reads per product, kAhead reads in flight
-        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, kAhead, 0);
+        // software pipeline: the probability reads, then two transposing reads
+        // per four products with kAheadV reads in flight
+        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2 * kTilesPV + kAheadV, 0);
 #pragma unroll
-        for (int i = 0; i < kDb - kAhead / 2; ++i) {
-            __builtin_amdgcn_sched_group_barrier(kSchedMfma, kTiles, 0);
+        for (int i = 0; i < kDbW - kAheadV / 2; ++i) {
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, kTilesPV, 0);
             __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
         }
-        __builtin_amdgcn_sched_group_barrier(kSchedMfma, kTiles * kAhead / 2, 0);
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, kTilesPV * kAheadV / 2, 0);
         __builtin_amdgcn_sched_barrier(0);
     };
 
@@ -545,11 +586,11 @@ __device__ __forceinline__ void item(const Params& p, const int r, const int g, 
     const int claim = max(nsteps - 3, 0);
     for (int attempt = 0;; ++attempt) {
 #pragma unroll
-        for (int j = 0; j < kTiles; ++j) {
-            lsum[j] = 0.0f;
+        for (int j = 0; j < kSTiles; ++j) lsum[j] = 0.0f;
 #pragma unroll
-            for (int db = 0; db < kDb; ++db) acc[j][db] = f32x4{0.f, 0.f, 0.f, 0.f};
-        }
+        for (int ti = 0; ti < kTilesPV; ++ti)
+#pragma unroll
+            for (int d = 0; d < kDbW; ++d) acc[ti][d] = f32x4{0.f, 0.f, 0.f, 0.f};
         wait_vmcnt<0>();
 #pragma unroll
         for (int n = 0; n < kRing - 1; ++n) issue(n);
@@ -558,7 +599,7 @@ __device__ __forceinline__ void item(const Params& p, const int r, const int g, 
             lds_barrier();  // step n visible to all; everyone is done with step n - 1
             if (n == claim && tid == 0 && attempt == 0) nxt = atomicAdd(p.head + home, 1);
             issue(n + kRing - 1);
-            if (nt_w > 0) compute(n, bufc);
+            compute(n, n == 0 && attempt == 0, bufc);
         };
         for (int n = 0; n < nsteps; n += kRing) {
             one(n, std::integral_constant<unsigned, 0>{});
@@ -567,57 +608,81 @@ __device__ __forceinline__ void item(const Params& p, const int r, const int g, 
         }
         wait_vmcnt<0>();
         // did any row of the block outgrow its reference?  (all waves agree)
-        if (lane == 0 && __builtin_amdgcn_ballot_w64(over)) atomicOr(&s_flag, 1);
+        // (the ballot runs on the whole wave, outside the lane condition)
+        const bool any_over = __builtin_amdgcn_ballot_w64(over) != 0;
+        if (lane == 0 && any_over) atomicOr(&s_flag, 1);
+        if (lq == 0) {
+#pragma unroll
+            for (int j = 0; j < kSTiles; ++j) sh.mx[wave][j][lr] = mobs[j];
+        }
         __syncthreads();
         const int again = s_flag;
+        float mnext[kSTiles];
+#pragma unroll
+        for (int j = 0; j < kSTiles; ++j) mnext[j] = vmax(mobs[j], sh.mx[partner][j][lr]);
         __syncthreads();
         if (!again) break;
         if (tid == 0) s_flag = 0;
 #pragma unroll
-        for (int j = 0; j < kTiles; ++j) mref[j] = mobs[j];
+        for (int j = 0; j < kSTiles; ++j) mref[j] = mnext[j];
         over = false;
     }
 
-    // ---- finish rows: l over the four lanes of a row
+    // ---- finish rows: l over the four lanes of a row and the two key blocks
 #pragma unroll
-    for (int j = 0; j < kTiles; ++j) {
+    for (int j = 0; j < kSTiles; ++j) {
         lsum[j] += __shfl_xor(lsum[j], 16, 64);
         lsum[j] += __shfl_xor(lsum[j], 32, 64);
+    }
+    if (lq == 0) {
+#pragma unroll
+        for (int j = 0; j < kSTiles; ++j) {
+            sh.ls[wave][j][lr] = lsum[j];
+            sh.mx[wave][j][lr] = mref[j];
+        }
+    }
+    __syncthreads();
+    float M[kTilesPV], L[kTilesPV];
+#pragma unroll
+    for (int ti = 0; ti < kTilesPV; ++ti) {
+        const int w0 = 2 * (ti / kSTiles);
+        M[ti] = sh.mx[w0][ti % kSTiles][lr];
+        L[ti] = sh.ls[w0][ti % kSTiles][lr] + sh.ls[w0 + 1][ti % kSTiles][lr];
     }
     if (nsplit == 1) {
         uint16_t* outp = (uint16_t*)a.out;
 #pragma unroll
-        for (int j = 0; j < kTiles; ++j) {
-            const int row = row0 + 16 * (kTiles * wave + j) + lr;
-            if (j < nt_w && row < rows) {
+        for (int ti = 0; ti < kTilesPV; ++ti) {
+            const int row = row0 + 16 * ti + lr;
+            if (row < rows) {
                 const int t = row / p.group;
                 const int h = g * p.group + (row - t * p.group);
                 const int64_t orow = (int64_t)(q0 + t) * a.Hq + h;
-                const float inv = 1.0f / lsum[j];
+                const float inv = 1.0f / L[ti];
 #pragma unroll
-                for (int db = 0; db < kDb; ++db) {
+                for (int d = 0; d < kDbW; ++d) {
                     uint2 pk;
-                    pk.x = pack2_bf16(acc[j][db][0] * inv, acc[j][db][1] * inv);
-                    pk.y = pack2_bf16(acc[j][db][2] * inv, acc[j][db][3] * inv);
-                    *(uint2*)(outp + orow * kDv + 16 * db + 4 * lq) = pk;
+                    pk.x = pack2_bf16(acc[ti][d][0] * inv, acc[ti][d][1] * inv);
+                    pk.y = pack2_bf16(acc[ti][d][2] * inv, acc[ti][d][3] * inv);
+                    *(uint2*)(outp + orow * kDv + 16 * (kDbW * wave + d) + 4 * lq) = pk;
                 }
-                if (a.lse && lq == 0) a.lse[orow] = (mref[j] + log2f(lsum[j])) * kLn2;
+                if (a.lse && wave == 0 && lq == 0) a.lse[orow] = (M[ti] + log2f(L[ti])) * kLn2;
             }
         }
         return;
     }
     float* part = p.part + (((int64_t)(r * a.Hkv + g) * p.rb_max + rb) * p.max_splits + s) * kSlotFloats;
 #pragma unroll
-    for (int j = 0; j < kTiles; ++j) {
-        const int rr = 16 * (kTiles * wave + j) + lr;
-        if (j < nt_w) {
-            if (lq == 0) {
-                part[rr] = mref[j];
-                part[kRows + rr] = lsum[j];
+    for (int ti = 0; ti < kTilesPV; ++ti) {
+        const int rr = 16 * ti + lr;
+        if (row0 + rr < rows) {
+            if (wave == 0 && lq == 0) {
+                part[rr] = M[ti];
+                part[kRows + rr] = L[ti];
             }
 #pragma unroll
-            for (int db = 0; db < kDb; ++db)
-                *(f32x4*)(part + 2 * kRows + rr * kDv + 16 * db + 4 * lq) = acc[j][db];
+            for (int d = 0; d < kDbW; ++d)
+                *(f32x4*)(part + 2 * kRows + rr * kDv + 16 * (kDbW * wave + d) + 4 * lq) = acc[ti][d];
         }
     }
 }
@@ -628,6 +693,7 @@ void mla_kernel(Params p) {
     __shared__ __align__(16) unsigned char lds[kRing * kTileB];
     __shared__ int s_item;
     __shared__ int s_flag;
+    __shared__ Shared sh;
     if (threadIdx.x == 0) s_flag = 0;
     uint32_t lds0 = (uint32_t)(uintptr_t)&lds[0];
     asm volatile("" : "+s"(lds0));
@@ -650,7 +716,7 @@ void mla_kernel(Params p) {
         const int4 e0 = p.list[2 * it];
         const int4 e1 = p.list[2 * it + 1];
         int nxt = 0;  // index claimed from queue q near the end of the item
-        item(p, e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w, lds0, q, nxt, s_flag);
+        item(p, e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w, lds0, q, nxt, s_flag, sh);
         __syncthreads();
         if (threadIdx.x == 0) {
             // the claim near the end came from queue q; past its end, look elsewhere

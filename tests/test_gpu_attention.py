@@ -126,6 +126,31 @@ def test_mla_reference_rerun():
     _full_compare(w, seed, q_len=[4, 9], label="mla-rerun", kv_fn=scale_and_check)
 
 
+def test_mla_reference_rerun_one_row():
+    # One key of request 1 is set to 160 times the unit direction of one query
+    # row (token 6, head 5: row 5 of its 16-row tile, not the tile's first).
+    # Only that row's score leaves its reference by more than 2^128 (exp2 would
+    # overflow), so the rerun has to be triggered by that row alone.
+    base = synth.WORKLOADS["mla"]
+    w = synth.scaled(base, R=2, Hq=16, kv_dist=("uniform", 200, 3000))
+    seed, q_len, t_star, h_star, j_key = 3, [4, 9], 6, 5, 100
+    cu = oracle.cu_from_len(np.array(q_len) - 1)
+
+    def plant(kv):
+        assert int(kv.kv_len[1]) - q_len[1] + t_star >= j_key  # the key is visible to the row
+        qb = synth.query_rows(w, seed, synth.flat_keys(np.diff(cu)))[int(cu[1]) + t_star, h_star]
+        q = synth.bf16_bits_to_f32(qb).astype(np.float64)
+        kvec = synth.f32_to_bf16_bits((160.0 * q / np.linalg.norm(q)).astype(np.float32))
+        kv.k[kv.block_table[1, j_key // w.page], 0, j_key % w.page] = kvec
+        keys = np.stack([synth.bf16_bits_to_f32(kv.k[kv.block_table[1, j // w.page], 0, j % w.page])
+                         for j in range(64)]).astype(np.float64)
+        s2 = keys @ q * w.scale / np.log(2.0)
+        k_star = synth.bf16_bits_to_f32(kvec).astype(np.float64)
+        assert (k_star @ q) * w.scale / np.log(2.0) > s2[:32].max() + 128
+
+    _full_compare(w, seed, q_len=q_len, label="mla-rerun-row", kv_fn=plant)
+
+
 def test_fp32_other_head_dims():
     base = synth.WORKLOADS["tiny"]
     for D, group in ((128, 8), (72, 1), (64, 16)):
