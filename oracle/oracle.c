@@ -12,7 +12,9 @@
  *   - attention is the textbook masked softmax attention, written out;
  *   - acceptance is the left-to-right speculative acceptance rule of the
  *     background section on speculative decoding, with the conventions listed
- *     at each function.
+ *     at each function;
+ *   - the Markov-head draft block follows the left-to-right factorisation of
+ *     the semi-autoregressive stage, one position at a time.
  * All arithmetic is fp64; bf16 inputs are widened exactly.  OpenMP only runs
  * independent rows side by side; no row's arithmetic is reordered.
  *
@@ -408,6 +410,87 @@ int oracle_accept(const int32_t* draft_tok, const float* draft_p, const void* lo
         accepted_len[r] = acc;
         next_tok[r] = tok;
         if (margin) margin[r] = mg;
+    }
+    return bad ? ORACLE_EINVAL : ORACLE_OK;
+}
+
+/* ------------------------------------------------ Markov-head draft block */
+
+/*
+ * The sequential stage of semi-autoregressive drafting with the Markov head
+ * (section on semi-autoregressive generation: the block distribution factors
+ * left to right, eq. sequential-factorization, and the Markov head's
+ * transition bias is the low-rank product of eq. markov), plus the confidence
+ * head of the confidence-scheduled verification section (eq. confidence) with
+ * the per-position temperatures of its post-hoc calibration.
+ *
+ * For every request r, with x_0 = anchor[r] and k = 1 .. K:
+ *   e_k      = W1[x_{k-1}]                       (embedding row, rank dims)
+ *   B_k(v)   = sum_j e_k[j] * W2[j, v]           (transition bias)
+ *   p_k      = softmax(inv_temp * (U_k + B_k))   (U_k = base logits of position k)
+ *   x_k      = inverse CDF of p_k at u[r, k-1]   (smallest v, ascending, whose
+ *                                                running mass exceeds u * total)
+ *   c_k      = sigmoid((w_h . h_k + w_e . e_k) / T_k)   (w = [w_h; w_e])
+ * Storage: U row (r, k) starts at element (r * K + k - 1) * ld (fp32 or bf16);
+ * W1 [V, rank] and the projection W2t [V, rank] (row v holds W2[:, v]) in
+ * bf16; hidden [R, K, d] bf16 (nullable when d = 0); w_conf [d + rank] fp32;
+ * sts_temp [K] fp32 (nullable: all 1); u [R, K] fp32.
+ * Outputs: draft_tok [R, K] = x_k, draft_p [R, K, V] = p_k (nullable),
+ * conf [R, K] = c_k, margin [R] (nullable) = the smallest distance of any draw
+ * from its bucket's edges, in units of the total mass.
+ */
+int oracle_markov_draft(const int32_t* anchor, const void* U, int u_dtype, int64_t ld,
+                        const uint16_t* W1, const uint16_t* W2t, int rank,
+                        const uint16_t* hidden, const float* w_conf, int d,
+                        const float* sts_temp, const float* u, double inv_temp, int R, int K,
+                        int V, int32_t* draft_tok, double* draft_p, double* conf,
+                        double* margin) {
+    if (!anchor || !U || !W1 || !W2t || !w_conf || !u || !draft_tok || !conf) return ORACLE_EINVAL;
+    if (R < 0 || K < 1 || V < 1 || rank < 1 || d < 0 || ld < V || (d > 0 && !hidden))
+        return ORACLE_EINVAL;
+    for (int r = 0; r < R; ++r)
+        if (anchor[r] < 0 || anchor[r] >= V) return ORACLE_EINVAL;
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(|| : bad)
+    for (int r = 0; r < R; ++r) {
+        double* z = (double*)malloc(sizeof(double) * (size_t)V);
+        double* e = (double*)malloc(sizeof(double) * (size_t)rank);
+        if (!z || !e) { bad = 1; free(z); free(e); continue; }
+        double worst = INFINITY;
+        int prev = anchor[r];
+        for (int k = 1; k <= K; ++k) {
+            const int64_t row = (int64_t)r * K + (k - 1);
+            /* embedding of the preceding token */
+            for (int j = 0; j < rank; ++j) e[j] = bf16_to_f64(W1[(int64_t)prev * rank + j]);
+            /* z = inv_temp * (U_k + B_k), then the softmax */
+            double m = -INFINITY;
+            for (int v = 0; v < V; ++v) {
+                double b = 0.0;
+                for (int j = 0; j < rank; ++j) b += e[j] * bf16_to_f64(W2t[(int64_t)v * rank + j]);
+                z[v] = inv_temp * (elem(U, row * ld + v, u_dtype) + b);
+                if (z[v] > m) m = z[v];
+            }
+            double S = 0.0;
+            for (int v = 0; v < V; ++v) { z[v] = exp(z[v] - m); S += z[v]; }
+            for (int v = 0; v < V; ++v) z[v] = z[v] / S;
+            if (draft_p)
+                memcpy(draft_p + row * (int64_t)V, z, sizeof(double) * (size_t)V);
+            /* draw x_k */
+            double mg;
+            const int x = inverse_cdf(z, V, (double)u[row], &mg);
+            if (mg < worst) worst = mg;
+            draft_tok[row] = x;
+            /* confidence of position k: the backbone state and the embedding of x_{k-1} */
+            double sacc = 0.0;
+            for (int i = 0; i < d; ++i) sacc += (double)w_conf[i] * bf16_to_f64(hidden[row * d + i]);
+            for (int j = 0; j < rank; ++j) sacc += (double)w_conf[d + j] * e[j];
+            const double T = sts_temp ? (double)sts_temp[k - 1] : 1.0;
+            conf[row] = 1.0 / (1.0 + exp(-sacc / T));
+            prev = x;
+        }
+        if (margin) margin[r] = worst;
+        free(z);
+        free(e);
     }
     return bad ? ORACLE_EINVAL : ORACLE_OK;
 }
