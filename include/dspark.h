@@ -187,6 +187,52 @@ dspark_status dspark_accept(const int32_t* draft_tok, const float* draft_p, cons
                             int32_t* accepted_len, int32_t* next_tok, float* accept_rate,
                             void* ws, size_t ws_bytes, dspark_stream stream);
 
+/* ------------------------------------------------------------------------
+ * Drafter: the Markov-head draft block, which produces the inputs of the
+ * three stages above (the sequential stage of semi-autoregressive drafting,
+ * eq. sequential-factorization, with the Markov head of eq. markov, and the
+ * confidence head of eq. confidence with the per-position temperatures of its
+ * post-hoc calibration).  For every request r, with x_0 = anchor[r] and
+ * k = 1 .. K, left to right:
+ *     e_k = W1[x_{k-1}]                                  (rank-dim embedding)
+ *     p_k = softmax(inv_temperature * (U_k + W2^T e_k))  (U_k: base logits)
+ *     x_k = the smallest v whose running mass (ascending v) exceeds
+ *           u[r, k-1] times the total mass
+ *     c_k = sigmoid((w_h . h_k + w_e . e_k) / T_k)       (w_conf = [w_h; w_e])
+ *
+ *   anchor      [R] int32: x_0 (the last token of the previous verification).
+ *   base_logits U_k of request r at element (r * K + k - 1) * ld; fp32 or
+ *               bf16 (base_dt); ld >= V.
+ *   W1          [V, rank] bf16 (uint16 bit patterns): embedding rows.
+ *   W2t         [V, rank] bf16: the projection stored vocabulary-major, row v
+ *               holding W2[:, v] (so a vocabulary tile is contiguous).
+ *   rank        32, 64, 128 or 256 (the paper's default is 256).
+ *   hidden      [R, K, d] bf16: the backbone state h_k of each position
+ *               (nullable when d == 0).
+ *   w_conf      [d + rank] fp32: confidence weights, hidden part first.
+ *   sts_temp    [K] fp32 per-position temperatures T_k (nullable: all 1).
+ *   u           [R, K] fp32 uniforms in [0, 1), one per draw.
+ *   draft_tok   [R, K] int32 out: x_1 .. x_K (dspark_accept's draft_tok).
+ *   draft_p     [R, K, V] fp32 out: p_1 .. p_K (dspark_accept's draft_p).
+ *   conf        [R, K] fp32 out: c_1 .. c_K (dspark_schedule's conf).
+ *   An anchor outside [0, V) marks its request invalid: its draft_tok row is
+ *   -1 and its conf row NaN (its draft_p rows hold finite values computed
+ *   with embedding row 0).
+ *   Limits: 1 <= R <= 8192, 1 <= K <= 64, 1 <= V <= 2^20, 0 <= d <= 2^16,
+ *   inv_temperature > 0; W1, W2t 16-byte aligned.  The base logits and
+ *   draft_p are read and written four entries at a time when V and ld are
+ *   multiples of 4 and the rows are aligned, else one at a time.
+ * ---------------------------------------------------------------------- */
+size_t dspark_markov_draft_workspace_size(int R, int V, int rank);
+
+dspark_status dspark_markov_draft(const int32_t* anchor, const void* base_logits,
+                                  dspark_dtype base_dt, int64_t ld, const uint16_t* W1,
+                                  const uint16_t* W2t, int rank, const uint16_t* hidden,
+                                  const float* w_conf, int d, const float* sts_temp,
+                                  const float* u, float inv_temperature, int R, int K, int V,
+                                  int32_t* draft_tok, float* draft_p, float* conf, void* ws,
+                                  size_t ws_bytes, dspark_stream stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -180,7 +180,8 @@ def markov_draft(anchor, U, u_dtype: str, W1, W2t, w_conf, u, K: int, V: int,
     """Markov-head draft block.  U: [R*K, >=V] rows (fp32 or bf16 bits), W1 /
     W2t: [V, rank] bf16 bits, hidden: [R, K, d] bf16 bits or None, w_conf:
     [d + rank] fp32, sts_temp: [K] or None, u: [R, K].  Returns (draft_tok
-    int32[R, K], draft_p f64[R, K, V] or None, conf f64[R, K], margin f64[R])."""
+    int32[R, K], draft_p f64[R, K, V] or None, conf f64[R, K], margin f64[R, K]:
+    each draw's distance from its bucket's edges in units of the total mass)."""
     dt = 0 if u_dtype == "f32" else 1
     store = np.float32 if dt == 0 else np.uint16
     U = _c(U, store)
@@ -199,7 +200,7 @@ def markov_draft(anchor, U, u_dtype: str, W1, W2t, w_conf, u, K: int, V: int,
     tok = np.zeros((R, K), dtype=np.int32)
     dp = np.empty((R, K, V), dtype=np.float64) if want_p else None
     conf = np.zeros((R, K), dtype=np.float64)
-    mg = np.zeros(R, dtype=np.float64)
+    mg = np.zeros((R, K), dtype=np.float64)
     it = float(np.float32(inv_temperature))
     rc = _load().oracle_markov_draft(_ptr(anc), _ptr(U), dt, ld, _ptr(W1), _ptr(W2t), rank,
                                      _ptr(hid), _ptr(wc), d, _ptr(st), _ptr(uu), it, R, K, V,

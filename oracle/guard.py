@@ -124,3 +124,61 @@ def build_case(w: synth.Workload, seed: int, mode: int = 0, with_kv: bool = True
     case.accepted_len, case.next_tok, case.accept_margin = acc, nxt, mg
     case.unguarded = [] if w.greedy else [r for r in range(R) if mg[r] < guard]
     return case
+
+
+# --------------------------------------------------------------------------
+# Markov-head draft block
+# --------------------------------------------------------------------------
+
+@dataclass
+class DraftCase:
+    inp: "synth.MarkovInputs"
+    tok: np.ndarray  # oracle draft tokens [n, K] of the requests in ``reqs``
+    p: Optional[np.ndarray]  # oracle draft distributions [n, K, V] (fp64) or None
+    conf: np.ndarray  # oracle confidences [n, K]
+    margin: np.ndarray  # per-draw margins [n, K]
+    reqs: List[int]
+    unguarded: List[int] = field(default_factory=list)
+
+
+def draft_case(w: synth.Workload, seed: int, rank: int, d: int, reqs: Optional[List[int]] = None,
+               inv_temperature: float = 1.0, want_p: bool = True, max_tries: int = 64) -> DraftCase:
+    """Inputs of the draft block and the oracle's outputs for ``reqs`` (all by
+    default), with each request's uniforms redrawn draw by draw, left to right,
+    until every draw is at least ACCEPT_GUARD (units of the total mass) from
+    its bucket's edges.  A redraw of draw k takes element k of the request's
+    next uniform sub-stream and changes every later draw, which is checked
+    again."""
+    inp = synth.markov_inputs(w, seed, rank=rank, d=d)
+    R, K, V = w.R, w.K, w.V
+    reqs = list(range(R)) if reqs is None else list(reqs)
+    tries = {r: np.zeros(K, dtype=np.int64) for r in reqs}
+    sub = np.array(reqs, dtype=np.int64)
+    unguarded: List[int] = []
+
+    def run(want):
+        base = inp.base.reshape(R, K, -1)[sub].reshape(len(sub) * K, -1)
+        hid = None if d == 0 else inp.hidden[sub]
+        return oracle.markov_draft(inp.anchor[sub], base, w.logit_dtype, inp.W1, inp.W2t,
+                                   inp.w_conf, inp.u[sub], K, V, hidden=hid,
+                                   sts_temp=inp.sts_temp, inv_temperature=inv_temperature,
+                                   want_p=want)
+
+    for _ in range(max_tries * K):
+        tok, _, _, mg = run(False)
+        bad = False
+        for i, r in enumerate(reqs):
+            ks = np.nonzero(mg[i] < ACCEPT_GUARD)[0]
+            if len(ks) == 0 or r in unguarded:
+                continue
+            k = int(ks[0])
+            tries[r][k] += 1
+            if tries[r][k] > max_tries:
+                unguarded.append(r)
+                continue
+            inp.u[r, k] = synth.markov_uniforms(seed, r, K, int(tries[r][k]))[k]
+            bad = True
+        if not bad:
+            break
+    tok, p, conf, mg = run(want_p)
+    return DraftCase(inp=inp, tok=tok, p=p, conf=conf, margin=mg, reqs=reqs, unguarded=unguarded)

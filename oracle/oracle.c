@@ -436,8 +436,8 @@ int oracle_accept(const int32_t* draft_tok, const float* draft_p, const void* lo
  * bf16; hidden [R, K, d] bf16 (nullable when d = 0); w_conf [d + rank] fp32;
  * sts_temp [K] fp32 (nullable: all 1); u [R, K] fp32.
  * Outputs: draft_tok [R, K] = x_k, draft_p [R, K, V] = p_k (nullable),
- * conf [R, K] = c_k, margin [R] (nullable) = the smallest distance of any draw
- * from its bucket's edges, in units of the total mass.
+ * conf [R, K] = c_k, margin [R, K] (nullable) = the distance of each draw from
+ * its bucket's edges, in units of the total mass.
  */
 int oracle_markov_draft(const int32_t* anchor, const void* U, int u_dtype, int64_t ld,
                         const uint16_t* W1, const uint16_t* W2t, int rank,
@@ -456,7 +456,6 @@ int oracle_markov_draft(const int32_t* anchor, const void* U, int u_dtype, int64
         double* z = (double*)malloc(sizeof(double) * (size_t)V);
         double* e = (double*)malloc(sizeof(double) * (size_t)rank);
         if (!z || !e) { bad = 1; free(z); free(e); continue; }
-        double worst = INFINITY;
         int prev = anchor[r];
         for (int k = 1; k <= K; ++k) {
             const int64_t row = (int64_t)r * K + (k - 1);
@@ -478,7 +477,7 @@ int oracle_markov_draft(const int32_t* anchor, const void* U, int u_dtype, int64
             /* draw x_k */
             double mg;
             const int x = inverse_cdf(z, V, (double)u[row], &mg);
-            if (mg < worst) worst = mg;
+            if (margin) margin[row] = mg;
             draft_tok[row] = x;
             /* confidence of position k: the backbone state and the embedding of x_{k-1} */
             double sacc = 0.0;
@@ -488,7 +487,6 @@ int oracle_markov_draft(const int32_t* anchor, const void* U, int u_dtype, int64
             conf[row] = 1.0 / (1.0 + exp(-sacc / T));
             prev = x;
         }
-        if (margin) margin[r] = worst;
         free(z);
         free(e);
     }

@@ -249,4 +249,64 @@ dspark_status dspark_accept(const int32_t* draft_tok, const float* draft_p, cons
     return hip_status(dspark::launch_accept(a, ws, (hipStream_t)stream), "dspark_accept");
 }
 
+size_t dspark_markov_draft_workspace_size(int R, int V, int rank) {
+    if (R < 1 || R > kMaxR || V < 1 || V > kMaxV || !dspark::markov_rank_supported(rank)) return 0;
+    return dspark::markov_workspace(R, V, rank);
+}
+
+dspark_status dspark_markov_draft(const int32_t* anchor, const void* base_logits,
+                                  dspark_dtype base_dt, int64_t ld, const uint16_t* W1,
+                                  const uint16_t* W2t, int rank, const uint16_t* hidden,
+                                  const float* w_conf, int d, const float* sts_temp,
+                                  const float* u, float inv_temperature, int R, int K, int V,
+                                  int32_t* draft_tok, float* draft_p, float* conf, void* ws,
+                                  size_t ws_bytes, dspark_stream stream) {
+    if (base_dt != DSPARK_F32 && base_dt != DSPARK_BF16)
+        return fail(DSPARK_EDTYPE, "base logit dtype %d", (int)base_dt);
+    if (R < 1 || R > kMaxR) return fail(DSPARK_EINVAL, "R=%d outside [1, %d]", R, kMaxR);
+    if (K < 1 || K > kMaxK) return fail(DSPARK_EINVAL, "K=%d outside [1, %d]", K, kMaxK);
+    if (V < 1 || V > kMaxV) return fail(DSPARK_EINVAL, "V=%d outside [1, %d]", V, kMaxV);
+    if (ld < V) return fail(DSPARK_ESHAPE, "ld=%lld smaller than V=%d", (long long)ld, V);
+    if (!dspark::markov_rank_supported(rank))
+        return fail(DSPARK_EUNSUPPORTED, "rank=%d (32, 64, 128 or 256)", rank);
+    if (d < 0 || d > (1 << 16)) return fail(DSPARK_EINVAL, "d=%d outside [0, 65536]", d);
+    if (!(inv_temperature > 0.0f) || !isfinite(inv_temperature))
+        return fail(DSPARK_EINVAL, "inv_temperature must be positive and finite");
+    if (!anchor || !base_logits || !W1 || !W2t || !w_conf || !u || !draft_tok || !draft_p ||
+        !conf || (d > 0 && !hidden))
+        return fail(DSPARK_EINVAL, "null argument");
+    const size_t esz = base_dt == DSPARK_BF16 ? 2 : 4;
+    if (!aligned(W1, 16) || !aligned(W2t, 16))
+        return fail(DSPARK_EUNSUPPORTED, "W1 and W2t must be 16-byte aligned");
+    if (!aligned(anchor, 4) || !aligned(base_logits, esz) || !aligned(hidden, 2) ||
+        !aligned(w_conf, 4) || !aligned(sts_temp, 4) || !aligned(u, 4) ||
+        !aligned(draft_tok, 4) || !aligned(draft_p, 4) || !aligned(conf, 4))
+        return fail(DSPARK_EINVAL, "misaligned pointer");
+    const size_t need = dspark::markov_workspace(R, V, rank);
+    if (ws_bytes < need || !ws || !aligned(ws, 256))
+        return fail(DSPARK_EWORKSPACE, "workspace of %zu bytes (256-aligned) needed, got %zu",
+                    need, ws_bytes);
+    dspark::MarkovArgs a;
+    a.anchor = anchor;
+    a.base = base_logits;
+    a.base_bf16 = base_dt == DSPARK_BF16;
+    a.ld = ld;
+    a.W1 = W1;
+    a.W2t = W2t;
+    a.rank = rank;
+    a.hidden = d > 0 ? hidden : nullptr;
+    a.w_conf = w_conf;
+    a.d = d;
+    a.sts_temp = sts_temp;
+    a.u = u;
+    a.inv_temp = inv_temperature;
+    a.R = R;
+    a.K = K;
+    a.V = V;
+    a.draft_tok = draft_tok;
+    a.draft_p = draft_p;
+    a.conf = conf;
+    return hip_status(dspark::launch_markov(a, ws, (hipStream_t)stream), "dspark_markov_draft");
+}
+
 }  // extern "C"

@@ -61,4 +61,28 @@ struct AcceptArgs {
 size_t accept_workspace(int R, int K, int V);
 hipError_t launch_accept(const AcceptArgs& a, void* ws, hipStream_t s);
 
+// ---- Markov-head draft block ----------------------------------------------------
+struct MarkovArgs {
+    const int32_t* anchor;
+    const void* base;  // base logits, row (r * K + k - 1) at element offset row * ld
+    int base_bf16;
+    int64_t ld;
+    const uint16_t* W1;   // [V, rank] bf16
+    const uint16_t* W2t;  // [V, rank] bf16, row v = W2[:, v]
+    int rank;
+    const uint16_t* hidden;  // [R, K, d] bf16 (null when d == 0)
+    const float* w_conf;     // [d + rank]
+    int d;
+    const float* sts_temp;  // [K] or null
+    const float* u;         // [R, K]
+    float inv_temp;
+    int R, K, V;
+    int32_t* draft_tok;  // [R, K]
+    float* draft_p;      // [R, K, V]
+    float* conf;         // [R, K]
+};
+size_t markov_workspace(int R, int V, int rank);
+bool markov_rank_supported(int rank);
+hipError_t launch_markov(const MarkovArgs& a, void* ws, hipStream_t s);
+
 }  // namespace dspark

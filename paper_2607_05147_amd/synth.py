@@ -40,6 +40,13 @@ _STREAM = {
     "draft_tok": 8,
     "draft_p": 9,
     "uniform": 10,
+    "mk_anchor": 11,
+    "mk_base": 12,
+    "mk_w1": 13,
+    "mk_w2": 14,
+    "mk_hidden": 15,
+    "mk_wconf": 16,
+    "mk_uniform": 17,
 }
 
 _KV_CHUNK_PAGES = 64  # pages per generator chunk of the KV pool
@@ -427,3 +434,58 @@ def drafts(w: Workload, seed: int, conf: np.ndarray,
         u_attempts = np.zeros(R, dtype=np.int64)
     u = np.stack([uniforms(w, seed, r, int(u_attempts[r])) for r in range(R)])
     return Drafts(draft_tok=tok, draft_p=dp, u=np.ascontiguousarray(u))
+
+
+# --------------------------------------------------------------------------
+# Markov-head draft block inputs (the drafter's sequential stage)
+# --------------------------------------------------------------------------
+
+MARKOV_RANK = 256  # the paper's default low rank of the transition bias
+MARKOV_HIDDEN = 4096  # width of the backbone state the confidence head reads
+
+
+@dataclass
+class MarkovInputs:
+    anchor: np.ndarray  # int32 [R] x_0
+    base: np.ndarray  # [R * K, V] base logits U_k (fp32, or uint16 bf16 bits)
+    W1: np.ndarray  # uint16 bf16 bits [V, rank]: embedding rows
+    W2t: np.ndarray  # uint16 bf16 bits [V, rank]: row v holds W2[:, v]
+    hidden: np.ndarray  # uint16 bf16 bits [R, K, d]
+    w_conf: np.ndarray  # fp32 [d + rank]
+    sts_temp: np.ndarray  # fp32 [K] per-position temperatures
+    u: np.ndarray  # fp32 [R, K] uniforms of the draws
+
+
+def markov_uniforms(seed: int, r: int, K: int, attempt: int = 0) -> np.ndarray:
+    """Uniforms of request r's K draws (redraw index ``attempt``)."""
+    return _rng(seed, "mk_uniform", r, attempt).random(K, dtype=np.float32)
+
+
+def markov_inputs(w: Workload, seed: int, rank: int = MARKOV_RANK, d: int = MARKOV_HIDDEN,
+                  u_attempts: Optional[np.ndarray] = None) -> MarkovInputs:
+    """Seeded synthetic inputs of the Markov-head draft block for workload w:
+    base logits logit_scale * N(0, 1) in the logit dtype; W1 ~ N(0, 1/rank)
+    (unit-norm embeddings) and W2 ~ N(0, 1), so the transition bias is about
+    N(0, 1); hidden ~ N(0, 1); w_conf ~ N(0, 1/(d + rank)); temperatures
+    1 + 0.05 k; anchors uniform over the vocabulary."""
+    R, K, V = w.R, w.K, w.V
+    anchor = _rng(seed, "mk_anchor").integers(0, V, R).astype(np.int32)
+    store = np.float32 if w.logit_dtype == "f32" else np.uint16
+    base = np.empty((R * K, V), dtype=store)
+
+    def base_row(i: int) -> None:
+        x = _rng(seed, "mk_base", i).standard_normal(V, dtype=np.float32) * np.float32(w.logit_scale)
+        base[i] = x if w.logit_dtype == "f32" else f32_to_bf16_bits(x)
+
+    with ThreadPoolExecutor(_threads()) as ex:
+        list(ex.map(base_row, range(R * K)))
+    g1 = _rng(seed, "mk_w1").standard_normal((V, rank), dtype=np.float32) * np.float32(1.0 / math.sqrt(rank))
+    g2 = _rng(seed, "mk_w2").standard_normal((V, rank), dtype=np.float32)
+    hidden = f32_to_bf16_bits(_rng(seed, "mk_hidden").standard_normal((R, K, d), dtype=np.float32))
+    w_conf = (_rng(seed, "mk_wconf").standard_normal(d + rank) / math.sqrt(d + rank)).astype(np.float32)
+    sts = (1.0 + 0.05 * np.arange(1, K + 1)).astype(np.float32)
+    if u_attempts is None:
+        u_attempts = np.zeros(R, dtype=np.int64)
+    u = np.stack([markov_uniforms(seed, r, K, int(u_attempts[r])) for r in range(R)])
+    return MarkovInputs(anchor=anchor, base=base, W1=f32_to_bf16_bits(g1), W2t=f32_to_bf16_bits(g2),
+                        hidden=hidden, w_conf=w_conf, sts_temp=sts, u=np.ascontiguousarray(u))

@@ -140,6 +140,41 @@ def test_accept_workspace_size(L):
     assert L.dspark_accept_workspace_size(0, 16, 129280) == 0
 
 
+def _draft(L, **kw):
+    a = dict(anchor=FAKE, base=FAKE, dt=1, ld=1024, W1=FAKE, W2t=FAKE, rank=256, hidden=FAKE,
+             wc=FAKE, d=64, sts=None, u=FAKE, it=1.0, R=4, K=8, V=1024, tok=FAKE, dp=FAKE,
+             conf=FAKE, ws=FAKE, ws_bytes=0)
+    a.update(kw)
+    return L.dspark_markov_draft(a["anchor"], a["base"], a["dt"], a["ld"], a["W1"], a["W2t"],
+                                 a["rank"], a["hidden"], a["wc"], a["d"], a["sts"], a["u"],
+                                 a["it"], a["R"], a["K"], a["V"], a["tok"], a["dp"], a["conf"],
+                                 a["ws"], a["ws_bytes"], None)
+
+
+def test_markov_draft_validation(L):
+    assert _draft(L, dt=7) == EDTYPE
+    assert _draft(L, K=0) == EINVAL
+    assert _draft(L, R=0) == EINVAL
+    assert _draft(L, V=0) == EINVAL
+    assert _draft(L, ld=1000) == ESHAPE
+    assert _draft(L, rank=96) == EUNSUPPORTED
+    assert _draft(L, d=-1) == EINVAL
+    assert _draft(L, it=0.0) == EINVAL
+    assert _draft(L, it=float("inf")) == EINVAL
+    assert _draft(L, hidden=None) == EINVAL  # d > 0 needs the hidden states
+    assert _draft(L, dp=None) == EINVAL
+    assert _draft(L, W2t=C.c_void_p((1 << 20) + 8)) == EUNSUPPORTED  # not 16-byte aligned
+    assert _draft(L) == EWORKSPACE  # every argument valid, no workspace
+    assert _draft(L, hidden=None, d=0) == EWORKSPACE
+
+
+def test_markov_draft_workspace_size(L):
+    n = L.dspark_markov_draft_workspace_size(128, 129280, 256)
+    # embeddings, per-tile statistics (505 tiles of 256 entries), per-row statistics
+    assert n >= 128 * 256 * 2 + 128 * 505 * 8 + 128 * 8
+    assert L.dspark_markov_draft_workspace_size(128, 129280, 96) == 0
+
+
 def test_binding_rejects_host_tensors():
     import torch
     with pytest.raises(dspark.DSparkError):
