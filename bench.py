@@ -43,6 +43,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="serving")
+    ap.add_argument("--stage", default="step", choices=["step", "draft"],
+                    help="step: the verification step (schedule, attention, acceptance); "
+                         "draft: the Markov-head draft block that produces its inputs")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample")
@@ -96,6 +99,9 @@ ATTN_PATHS = {
                "bound": "mfma"},
     "generic": {"src": "attn_generic.hip", "kernels": ("attn_generic_kernel", "attn_generic_merge"),
                 "bound": "hbm"},
+    # not attention: the draft block's launches (four per draft position)
+    "draft": {"src": "markov.hip", "kernels": ("md_hidden", "md_first", "md_tile", "md_stats"),
+              "bound": "hbm"},
 }
 
 
@@ -111,12 +117,16 @@ def attn_path(w, bf16: bool) -> str:
 
 
 def path_of_workload(name: str) -> str:
+    if name == "draft":
+        return "draft"
     import paper_2607_05147_amd.synth as synth
     w = synth.WORKLOADS[name]
     return attn_path(w, w.kv_elem_bytes == 2)
 
 
 def traffic_file(workload: str) -> str:
+    if workload == "draft":
+        return os.path.join(HERE, "profiles", "markov_draft_serving_traffic.json")
     return os.path.join(HERE, "profiles", f"verify_attn_{workload}_traffic.json")
 
 
@@ -151,9 +161,12 @@ def traffic_from(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, workload=
     def per_call(path):
         rows = _counter_rows(path)
         calls = sum(1 for name, _ in rows if kernels[1] in name)
+        if workload == "draft":  # one md_first launch per call
+            calls = sum(1 for name, _ in rows if "md_first" in name)
         tot = {k: sum(v for name, v in rows if k in name) for k in kernels}
         return {k: tot[k] / calls * 1024.0 for k in kernels}, calls
 
+    sel = "--stage draft" if workload == "draft" else f"--workload {workload}"
     sf, sw = copy_scale(copy_fetch_csv), copy_scale(copy_write_csv)
     fetch, calls = per_call(fetch_csv)
     write, _ = per_call(write_csv)
@@ -168,12 +181,12 @@ def traffic_from(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, workload=
         "source_sha256": source_sha(os.path.join(CSRC, path["src"])),
         "commands": [
             f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d <dir> -o pmc -- python bench.py "
-            f"--workload {workload} --steps 5 --warmup 1 --no-cpu-baseline",
+            f"{sel} --steps 5 --warmup 1 --no-cpu-baseline",
             f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d <dir> -o pmc -- python bench.py "
-            f"--workload {workload} --steps 5 --warmup 1 --no-cpu-baseline",
+            f"{sel} --steps 5 --warmup 1 --no-cpu-baseline",
             "rocprofv3 --pmc FETCH_SIZE --output-format csv -d <dir> -o pmc -- python bench.py --copy-probe",
             "rocprofv3 --pmc WRITE_SIZE --output-format csv -d <dir> -o pmc -- python bench.py --copy-probe",
-            f"python bench.py --workload {workload} --traffic-from <the four pmc_counter_collection.csv files>",
+            f"python bench.py {sel} --traffic-from <the four pmc_counter_collection.csv files>",
         ],
     }
     os.makedirs(os.path.dirname(traffic_file(workload)), exist_ok=True)
@@ -215,7 +228,7 @@ def copy_probe():
 def main():
     args = parse()
     if args.traffic_from:
-        traffic_from(*args.traffic_from, workload=args.workload)
+        traffic_from(*args.traffic_from, workload="draft" if args.stage == "draft" else args.workload)
         return
     if args.copy_probe:
         copy_probe()
@@ -232,6 +245,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py: no ROCm GPU visible", file=sys.stderr)
         sys.exit(1)
+    if args.stage == "draft":
+        draft_bench(args)
+        return
     dev = torch.device("cuda:0")
     w = synth.WORKLOADS[args.workload]
     seed = args.seed
@@ -375,6 +391,120 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, seed, conf, sps, ln, kv, q, logits, dr,
                                               args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+def draft_bytes(w, rank: int, d: int, base_bytes: int) -> int:
+    """Algorithmic HBM bytes of one draft-block call: per position the base
+    logits and the projection read once and the draft distribution written
+    once, plus the embedding rows, hidden states and small per-row values."""
+    per_pos = w.R * w.V * base_bytes + w.V * rank * 2 + w.R * w.V * 4
+    return w.K * per_pos + w.R * w.K * (d * 2 + rank * 2 + 16) + (d + rank) * 4
+
+
+def draft_bench(args):
+    """Times dspark_markov_draft on the workload's shape (R requests, K draft
+    positions, its vocabulary and logit dtype, rank 256, 4096-wide hidden
+    states) and prints one JSON line."""
+    import torch
+    import oracle
+    from paper_2607_05147_amd import dspark, synth
+
+    dev = torch.device("cuda:0")
+    w = synth.WORKLOADS[args.workload]
+    rank, d = synth.MARKOV_RANK, synth.MARKOV_HIDDEN
+    t0 = time.time()
+    inp = synth.markov_inputs(w, args.seed, rank=rank, d=d)
+
+    def to_dev(a):
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(a).to(dev)
+
+    args_d = dict(anchor=to_dev(inp.anchor), base=to_dev(inp.base), W1=to_dev(inp.W1),
+                  W2t=to_dev(inp.W2t), w_conf=to_dev(inp.w_conf), u=to_dev(inp.u),
+                  hidden=to_dev(inp.hidden), sts=to_dev(inp.sts_temp))
+    tok = torch.empty((w.R, w.K), dtype=torch.int32, device=dev)
+    dp = torch.empty((w.R, w.K, w.V), dtype=torch.float32, device=dev)
+    conf = torch.empty((w.R, w.K), dtype=torch.float32, device=dev)
+    ws = torch.empty(dspark.dspark_markov_draft_workspace_size(w.R, w.K, w.V, rank), dtype=torch.uint8,
+                     device=dev)
+    torch.cuda.synchronize()
+    log(f"draft inputs ready in {time.time() - t0:.1f}s: base logits {inp.base.nbytes / 1e6:.0f} MB, "
+        f"W1 + W2t {2 * inp.W1.nbytes / 1e6:.0f} MB")
+
+    def call():
+        dspark.dspark_markov_draft(args_d["anchor"], args_d["base"], args_d["W1"], args_d["W2t"],
+                                   args_d["w_conf"], args_d["u"], w.K, hidden=args_d["hidden"],
+                                   sts_temp=args_d["sts"], draft_tok=tok, draft_p=dp, conf=conf,
+                                   ws=ws)
+
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    t_start = time.perf_counter()
+    for e in evs:
+        e[0].record(stream)
+        call()
+        e[1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    ms_per = wall * 1e3 / args.steps
+    nbytes = draft_bytes(w, rank, d, w.logit_elem_bytes)
+    gbps = nbytes / (ms.mean() / 1e3) / 1e9
+    log(f"draft block: {ms.mean() * 1e3:.1f} us per call ({ms.mean() * 1e3 / w.K:.1f} us per position), "
+        f"{gbps:.0f} GB/s = {gbps / HBM_PEAK_GBPS:.1%} of HBM peak")
+    result = {
+        "metric": "draft tokens/s and achieved HBM GB/s (% of peak), Markov-head draft block on 1 MI355X",
+        "value": w.R * w.K / (ms_per / 1e3),
+        "unit": "draft tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded; shapes and distributions of the workload)",
+        "config": {"workload": f"markov draft ({w.name} shape): R={w.R} requests, K={w.K} positions, "
+                               f"V={w.V}, rank {rank}, hidden {d}, {w.logit_dtype} base logits",
+                   "seed": args.seed},
+        "roofline": {"kernel": "dspark_markov_draft: md_hidden + md_first, then md_tile<0> + md_stats + "
+                               "md_tile<1> per position",
+                     "bound": "hbm", "achieved": gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": gbps / HBM_PEAK_GBPS, "bytes_per_launch": nbytes,
+                     "traffic": measured_traffic("draft")},
+    }
+    if not args.no_cpu_baseline:
+        # the oracle on the first n requests, n sized to about --cpu-seconds
+        base = inp.base.reshape(w.R, w.K, -1)
+
+        def run(n):
+            s = time.perf_counter()
+            oracle.markov_draft(inp.anchor[:n], base[:n].reshape(n * w.K, -1), w.logit_dtype, inp.W1,
+                                inp.W2t, inp.w_conf, inp.u[:n], w.K, w.V, hidden=inp.hidden[:n],
+                                sts_temp=inp.sts_temp, want_p=False)
+            return time.perf_counter() - s
+
+        th = oracle.threads()
+        t1 = run(min(th, w.R))
+        n = int(min(w.R, max(th, th * round(args.cpu_seconds / max(t1, 1e-3)))))
+        tn = run(n) if n > min(th, w.R) else t1
+        n = max(n, min(th, w.R))
+        reps = 1
+        while tn * reps < 0.66 * args.cpu_seconds:  # the whole block is quick: repeat it
+            tn += run(n)
+            reps += 1
+        result["cpu_baseline"] = {"value": reps * n * w.K / tn, "unit": "draft tokens/s", "cores": th,
+                                  "kind": "oracle", "sample": f"requests 0..{n - 1} of the same block "
+                                  f"({n * w.K} draft tokens), {reps} times", "seconds": tn}
+        log(f"oracle baseline: {n} requests x {reps} in {tn:.1f}s on {th} threads")
     print(json.dumps(result), flush=True)
 
 

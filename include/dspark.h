@@ -218,12 +218,12 @@ dspark_status dspark_accept(const int32_t* draft_tok, const float* draft_p, cons
  *   An anchor outside [0, V) marks its request invalid: its draft_tok row is
  *   -1 and its conf row NaN (its draft_p rows hold finite values computed
  *   with embedding row 0).
- *   Limits: 1 <= R <= 8192, 1 <= K <= 64, 1 <= V <= 2^20, 0 <= d <= 2^16,
+ *   Limits: 1 <= R <= 8192, 1 <= K <= 64, 1 <= V <= 262144, 0 <= d <= 2^16,
  *   inv_temperature > 0; W1, W2t 16-byte aligned.  The base logits and
  *   draft_p are read and written four entries at a time when V and ld are
  *   multiples of 4 and the rows are aligned, else one at a time.
  * ---------------------------------------------------------------------- */
-size_t dspark_markov_draft_workspace_size(int R, int V, int rank);
+size_t dspark_markov_draft_workspace_size(int R, int K, int V, int rank);
 
 dspark_status dspark_markov_draft(const int32_t* anchor, const void* base_logits,
                                   dspark_dtype base_dt, int64_t ld, const uint16_t* W1,

@@ -249,9 +249,11 @@ dspark_status dspark_accept(const int32_t* draft_tok, const float* draft_p, cons
     return hip_status(dspark::launch_accept(a, ws, (hipStream_t)stream), "dspark_accept");
 }
 
-size_t dspark_markov_draft_workspace_size(int R, int V, int rank) {
-    if (R < 1 || R > kMaxR || V < 1 || V > kMaxV || !dspark::markov_rank_supported(rank)) return 0;
-    return dspark::markov_workspace(R, V, rank);
+size_t dspark_markov_draft_workspace_size(int R, int K, int V, int rank) {
+    if (R < 1 || R > kMaxR || K < 1 || K > kMaxK || V < 1 || V > dspark::markov_max_vocab() ||
+        !dspark::markov_rank_supported(rank))
+        return 0;
+    return dspark::markov_workspace(R, K, V, rank);
 }
 
 dspark_status dspark_markov_draft(const int32_t* anchor, const void* base_logits,
@@ -267,6 +269,8 @@ dspark_status dspark_markov_draft(const int32_t* anchor, const void* base_logits
     if (K < 1 || K > kMaxK) return fail(DSPARK_EINVAL, "K=%d outside [1, %d]", K, kMaxK);
     if (V < 1 || V > kMaxV) return fail(DSPARK_EINVAL, "V=%d outside [1, %d]", V, kMaxV);
     if (ld < V) return fail(DSPARK_ESHAPE, "ld=%lld smaller than V=%d", (long long)ld, V);
+    if (V > dspark::markov_max_vocab())
+        return fail(DSPARK_EUNSUPPORTED, "V=%d above %d", V, dspark::markov_max_vocab());
     if (!dspark::markov_rank_supported(rank))
         return fail(DSPARK_EUNSUPPORTED, "rank=%d (32, 64, 128 or 256)", rank);
     if (d < 0 || d > (1 << 16)) return fail(DSPARK_EINVAL, "d=%d outside [0, 65536]", d);
@@ -282,7 +286,7 @@ dspark_status dspark_markov_draft(const int32_t* anchor, const void* base_logits
         !aligned(w_conf, 4) || !aligned(sts_temp, 4) || !aligned(u, 4) ||
         !aligned(draft_tok, 4) || !aligned(draft_p, 4) || !aligned(conf, 4))
         return fail(DSPARK_EINVAL, "misaligned pointer");
-    const size_t need = dspark::markov_workspace(R, V, rank);
+    const size_t need = dspark::markov_workspace(R, K, V, rank);
     if (ws_bytes < need || !ws || !aligned(ws, 256))
         return fail(DSPARK_EWORKSPACE, "workspace of %zu bytes (256-aligned) needed, got %zu",
                     need, ws_bytes);

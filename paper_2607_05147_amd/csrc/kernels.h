@@ -81,8 +81,9 @@ struct MarkovArgs {
     float* draft_p;      // [R, K, V]
     float* conf;         // [R, K]
 };
-size_t markov_workspace(int R, int V, int rank);
+size_t markov_workspace(int R, int K, int V, int rank);
 bool markov_rank_supported(int rank);
+int markov_max_vocab();  // per-tile statistics of one request fit one workgroup
 hipError_t launch_markov(const MarkovArgs& a, void* ws, hipStream_t s);
 
 }  // namespace dspark

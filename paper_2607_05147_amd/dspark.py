@@ -61,7 +61,7 @@ def lib():
         L.dspark_accept.restype = i32
         L.dspark_accept.argtypes = [p, p, p, i32, i64, p, p, i32, i32, i32, f32, p, p, p, p, sz, p]
         L.dspark_markov_draft_workspace_size.restype = sz
-        L.dspark_markov_draft_workspace_size.argtypes = [i32, i32, i32]
+        L.dspark_markov_draft_workspace_size.argtypes = [i32, i32, i32, i32]
         L.dspark_markov_draft.restype = i32
         L.dspark_markov_draft.argtypes = [p, p, i32, i64, p, p, i32, p, p, i32, p, p, f32, i32, i32,
                                           i32, p, p, p, p, sz, p]
@@ -247,8 +247,8 @@ def dspark_accept(draft_tok: torch.Tensor, logits: torch.Tensor, cu_q: torch.Ten
     return accepted_len, next_tok, accept_rate
 
 
-def dspark_markov_draft_workspace_size(R: int, V: int, rank: int) -> int:
-    return int(lib().dspark_markov_draft_workspace_size(R, V, rank))
+def dspark_markov_draft_workspace_size(R: int, K: int, V: int, rank: int) -> int:
+    return int(lib().dspark_markov_draft_workspace_size(R, K, V, rank))
 
 
 def dspark_markov_draft(anchor: torch.Tensor, base_logits: torch.Tensor, W1: torch.Tensor,
@@ -290,7 +290,7 @@ def dspark_markov_draft(anchor: torch.Tensor, base_logits: torch.Tensor, W1: tor
     _dev(draft_tok, "draft_tok", torch.int32, (R, K))
     _dev(draft_p, "draft_p", torch.float32, (R, K, V))
     _dev(conf, "conf", torch.float32, (R, K))
-    need = dspark_markov_draft_workspace_size(R, V, rank)
+    need = dspark_markov_draft_workspace_size(R, K, V, rank)
     if need == 0:
         raise DSparkError(f"unsupported shape: R={R} V={V} rank={rank}")
     ws, ws_bytes = _workspace(need, dev, ws)

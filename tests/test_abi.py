@@ -158,6 +158,7 @@ def test_markov_draft_validation(L):
     assert _draft(L, V=0) == EINVAL
     assert _draft(L, ld=1000) == ESHAPE
     assert _draft(L, rank=96) == EUNSUPPORTED
+    assert _draft(L, V=262145, ld=262145) == EUNSUPPORTED  # tile statistics of a row fit one workgroup
     assert _draft(L, d=-1) == EINVAL
     assert _draft(L, it=0.0) == EINVAL
     assert _draft(L, it=float("inf")) == EINVAL
@@ -169,10 +170,11 @@ def test_markov_draft_validation(L):
 
 
 def test_markov_draft_workspace_size(L):
-    n = L.dspark_markov_draft_workspace_size(128, 129280, 256)
-    # embeddings, per-tile statistics (505 tiles of 256 entries), per-row statistics
-    assert n >= 128 * 256 * 2 + 128 * 505 * 8 + 128 * 8
-    assert L.dspark_markov_draft_workspace_size(128, 129280, 96) == 0
+    n = L.dspark_markov_draft_workspace_size(128, 16, 129280, 256)
+    # two embedding buffers, per-tile statistics (1010 tiles of 128 entries),
+    # per-row state, the hidden part of every confidence logit
+    assert n >= 2 * 128 * 256 * 2 + 128 * 1010 * 8 + 128 * 24 + 128 * 16 * 4
+    assert L.dspark_markov_draft_workspace_size(128, 16, 129280, 96) == 0
 
 
 def test_binding_rejects_host_tensors():
