@@ -4,12 +4,11 @@
 // Steps, all on the device so the verification step needs no host round trip:
 //   1. survival a[r][j] = prod_{i<=j} c[r][i] (fp64, multiplied in increasing j;
 //      the same sequence of roundings on every implementation);
-//   2. bitonic sort of the R*K candidates, descending a, ties by (r, j): the
-//      key is the bit pattern of a (non-negative doubles order like their
-//      bits) plus the flat index r*K + j.  Each thread keeps E = N/1024
-//      consecutive keys in registers: partners closer than E are swapped in
-//      registers, partners in the same wave through lane shuffles, and only
-//      partners in other waves go through LDS (with barriers);
+//   2. sort of the R*K candidates, descending a, ties by (r, j): the key is the
+//      bit pattern of a (non-negative doubles order like their bits) plus the
+//      flat index r*K + j.  A merge sort by rank: each request's candidates
+//      already form a sorted run, and each level merges runs pairwise with
+//      one binary search per candidate (E = Np/1024 candidates per thread);
 //   3. block-wide fp64 inclusive scan of the sorted a: tau_n = R + sum_{m<=n} a_m;
 //   4. Theta_n = tau_n * SPS(R + n + 1); mode 0 stops at the first n whose Theta
 //      does not exceed its predecessor's (Theta_{-1} = R * SPS(R)), mode 1 takes
@@ -61,22 +60,6 @@ __device__ __forceinline__ bool before(const SKey& x, const SKey& y) {
     if (x.hi != y.hi) return x.hi > y.hi;
     if (x.lo != y.lo) return x.lo > y.lo;
     return x.idx < y.idx;
-}
-
-// compare-exchange of the pair (e, e ^ J) inside a thread, for every e with bit
-// J clear; i0 is the thread's first flat position
-template <int E, int J>
-__device__ __forceinline__ void sort_in_thread(SKey (&v)[E], int i0, int k) {
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-        if (e & J) continue;
-        const bool up = ((i0 + e) & k) == 0;
-        if (before(v[e ^ J], v[e]) == up) {
-            const SKey t = v[e];
-            v[e] = v[e ^ J];
-            v[e ^ J] = t;
-        }
-    }
 }
 
 template <int E>
@@ -136,70 +119,55 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
     }
     for (int i = N + tid; i < Np; i += kSchedThreads) {
         key[i] = 0;
-        idx[i] = 0xFFFF;
+        idx[i] = (uint16_t)i;  // unique, after every real candidate of equal key
     }
     if (my_cand) atomicAdd(&s_ncand, my_cand);
     __syncthreads();
 
-    // 2. bitonic sort with the keys in registers
-    const bool active = i0 < Np;
+    // 2. merge sort by rank.  Runs of S sorted candidates are merged pairwise:
+    // a candidate at in-run index li moves to (run pair start) + li + (the
+    // number of the partner run's candidates that come before it), found by a
+    // branchless binary search of the partner run.  "before" is a strict total
+    // order (the flat index breaks every tie; padding slots carry their own
+    // position as index), so the new positions form a permutation.  Each
+    // request's K candidates are sorted already (a is non-increasing in j), so
+    // for a power-of-two K the merging starts at runs of K.
     SKey v[E];
+    int pos[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-        const uint64_t kk = active ? key[i0 + e] : 0;
-        v[e] = SKey{(uint32_t)(kk >> 32), (uint32_t)kk, active ? (int)idx[i0 + e] : 0xFFFF};
+        const int i = i0 + e;
+        const bool in = i < Np;
+        const uint64_t kk = in ? key[i] : 0;
+        v[e] = SKey{(uint32_t)(kk >> 32), (uint32_t)kk, in ? (int)idx[i] : 0};
+        pos[e] = i;
     }
-    for (int k = 2; k <= Np; k <<= 1) {
-        for (int j = k >> 1; j > 0; j >>= 1) {
-            if (j < E) {
-                if (E > 4 && j == 4) sort_in_thread<E, (E > 4 ? 4 : 1)>(v, i0, k);
-                else if (E > 2 && j == 2) sort_in_thread<E, (E > 2 ? 2 : 1)>(v, i0, k);
-                else sort_in_thread<E, 1>(v, i0, k);
-            } else if (j < DSPARK_WAVE * E) {
-                // partner element e of lane ^ (j / E)
-                const int m = j / E;
+    // (K = 0 has no candidates; S must start at 1 or more for the loop to end)
+    for (int S = K > 0 && (K & (K - 1)) == 0 ? K : 1; S < Np; S <<= 1) {
+        int cnt[E];
 #pragma unroll
-                for (int e = 0; e < E; ++e) {
-                    const SKey o{(uint32_t)__shfl_xor((int)v[e].hi, m, DSPARK_WAVE),
-                                 (uint32_t)__shfl_xor((int)v[e].lo, m, DSPARK_WAVE),
-                                 __shfl_xor(v[e].idx, m, DSPARK_WAVE)};
-                    const int i = i0 + e;
-                    const bool first = ((i & j) == 0) == ((i & k) == 0);  // keep the earlier one
-                    if (before(o, v[e]) == first) v[e] = o;
-                }
-            } else {
-                // partner in another wave: exchange through LDS
-                __syncthreads();  // everyone has read the previous exchange
-                if (active) {
+        for (int e = 0; e < E; ++e) cnt[e] = 0;
+        for (int b = S; b > 0; b >>= 1) {
 #pragma unroll
-                    for (int e = 0; e < E; ++e) {
-                        key[i0 + e] = ((uint64_t)v[e].hi << 32) | v[e].lo;
-                        idx[i0 + e] = (uint16_t)v[e].idx;
-                    }
-                }
-                __syncthreads();
-                if (active) {
-#pragma unroll
-                    for (int e = 0; e < E; ++e) {
-                        const int i = i0 + e;
-                        const uint64_t kk = key[i ^ j];
-                        const SKey o{(uint32_t)(kk >> 32), (uint32_t)kk, (int)idx[i ^ j]};
-                        const bool first = ((i & j) == 0) == ((i & k) == 0);
-                        if (before(o, v[e]) == first) v[e] = o;
-                    }
-                }
+            for (int e = 0; e < E; ++e) {
+                if (pos[e] >= Np || cnt[e] + b > S) continue;
+                const int pb = (pos[e] & ~(S - 1)) ^ S;  // the partner run's first position
+                const int t = pb + cnt[e] + b - 1;
+                const uint64_t kk = key[t];
+                const SKey o{(uint32_t)(kk >> 32), (uint32_t)kk, (int)idx[t]};
+                if (before(o, v[e])) cnt[e] += b;
             }
         }
-    }
-    __syncthreads();
-    if (active) {
+        __syncthreads();  // every read of this level is done
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-            key[i0 + e] = ((uint64_t)v[e].hi << 32) | v[e].lo;
-            idx[i0 + e] = (uint16_t)v[e].idx;
+            if (pos[e] >= Np) continue;
+            pos[e] = (pos[e] & ~(2 * S - 1)) + (pos[e] & (S - 1)) + cnt[e];
+            key[pos[e]] = ((uint64_t)v[e].hi << 32) | v[e].lo;
+            idx[pos[e]] = (uint16_t)v[e].idx;
         }
+        __syncthreads();  // the merged runs are visible
     }
-    __syncthreads();
     const int ncand = s_ncand;
 
     // 3. inclusive scan of the sorted survival probabilities (fp64); thread t
