@@ -304,6 +304,8 @@ def main():
         dtype=torch.uint8, device=dev)
     ws_acc = torch.empty(dspark.dspark_accept_workspace_size(w.R, w.K, w.V), dtype=torch.uint8,
                          device=dev)
+    ws_sched = torch.empty(dspark.dspark_schedule_workspace_size(w.R, w.K), dtype=torch.uint8,
+                           device=dev)
     torch.cuda.synchronize()
     log(f"device inputs ready ({NCOPY} copies), {time.time() - t0:.1f}s")
 
@@ -312,7 +314,8 @@ def main():
     def step(d, ev=None):
         if ev is not None:
             ev[0].record(stream)
-        dspark.dspark_schedule(d["conf"], d["sps"], 0, len_out=d["len"], cu_q=d["cu"])
+        dspark.dspark_schedule(d["conf"], d["sps"], 0, len_out=d["len"], cu_q=d["cu"],
+                               ws=ws_sched)
         if ev is not None:
             ev[1].record(stream)
         dspark.dspark_verify_attn(d["q"], d["k"], d["v"], kv.k_strides, kv.v_strides, d["bt"],

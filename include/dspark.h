@@ -86,8 +86,15 @@ const char* dspark_last_error(void);
  *                          cu_q[r] .. cu_q[r+1]-1 of the flattened batch.
  *   tok_req  [R*(K+1)] int32 out (nullable) request id of every flattened
  *                          verify token; slots >= cu_q[R] are set to -1.
+ *   ws       workspace of dspark_schedule_workspace_size(R, K) bytes
+ *                          (16 + 12*R*K, rounded up to 256), 256-aligned:
+ *                          the candidates' admission positions and running
+ *                          tau = R + sum of admitted a, passed from the
+ *                          ranking kernel to the selection kernel.  Missing,
+ *                          small or misaligned -> DSPARK_EWORKSPACE.
  *   The candidates (r, j) with a_{r,j} > 0 are admitted in descending a,
  *   ties by r then j.  Limits: 1 <= R, 0 <= K <= 64, R*K <= 8192.
+ *   dspark_schedule_workspace_size returns 0 for sizes outside the limits.
  * ---------------------------------------------------------------------- */
 size_t dspark_schedule_workspace_size(int R, int K);
 

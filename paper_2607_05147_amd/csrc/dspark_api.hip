@@ -107,16 +107,13 @@ const char* dspark_last_error(void) { return g_err.c_str(); }
 // ------------------------------------------------------------------ schedule
 
 size_t dspark_schedule_workspace_size(int R, int K) {
-    (void)R;
-    (void)K;
-    return 0;  // the scheduler works entirely in LDS
+    if (R < 1 || R > kMaxR || K < 0 || K > kMaxK || (int64_t)R * K > kMaxSchedCand) return 0;
+    return dspark::schedule_workspace(R, K);
 }
 
 dspark_status dspark_schedule(const float* conf, int R, int K, const double* sps, int64_t sps_len,
                               int mode, int32_t* len, int32_t* cu_q, int32_t* tok_req, void* ws,
                               size_t ws_bytes, dspark_stream stream) {
-    (void)ws;
-    (void)ws_bytes;
     if (R < 1 || R > kMaxR) return fail(DSPARK_EINVAL, "R=%d outside [1, %d]", R, kMaxR);
     if (K < 0 || K > kMaxK) return fail(DSPARK_EINVAL, "K=%d outside [0, %d]", K, kMaxK);
     if ((int64_t)R * K > kMaxSchedCand)
@@ -130,7 +127,11 @@ dspark_status dspark_schedule(const float* conf, int R, int K, const double* sps
     if (!aligned(conf, 4) || !aligned(sps, 8) || !aligned(len, 4) || !aligned(cu_q, 4) ||
         !aligned(tok_req, 4))
         return fail(DSPARK_EINVAL, "misaligned pointer");
-    return hip_status(dspark::launch_schedule(conf, R, K, sps, mode, len, cu_q, tok_req,
+    const size_t need = dspark::schedule_workspace(R, K);
+    if (ws_bytes < need || !ws || !aligned(ws, 256))
+        return fail(DSPARK_EWORKSPACE, "workspace of %zu bytes (256-aligned) needed, got %zu",
+                    need, ws_bytes);
+    return hip_status(dspark::launch_schedule(conf, R, K, sps, mode, len, cu_q, tok_req, ws,
                                               (hipStream_t)stream),
                       "dspark_schedule");
 }

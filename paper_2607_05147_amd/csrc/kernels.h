@@ -8,9 +8,10 @@
 namespace dspark {
 
 // ---- scheduler --------------------------------------------------------------
-size_t schedule_lds_bytes(int R, int K);
+size_t schedule_workspace(int R, int K);
 hipError_t launch_schedule(const float* conf, int R, int K, const double* sps, int mode,
-                           int32_t* len, int32_t* cu_q, int32_t* tok_req, hipStream_t s);
+                           int32_t* len, int32_t* cu_q, int32_t* tok_req, void* ws,
+                           hipStream_t s);
 
 // ---- verify attention ---------------------------------------------------------
 struct AttnArgs {

@@ -1,21 +1,27 @@
 // Hardware-aware prefix scheduler (Algorithm 1 of the section on
-// confidence-scheduled verification) as one gfx950 workgroup.
+// confidence-scheduled verification) as two gfx950 kernels, so the
+// verification step needs no host round trip.
 //
-// Steps, all on the device so the verification step needs no host round trip:
-//   1. survival a[r][j] = prod_{i<=j} c[r][i] (fp64, multiplied in increasing j;
-//      the same sequence of roundings on every implementation);
-//   2. sort of the R*K candidates, descending a, ties by (r, j): the key is the
-//      bit pattern of a (non-negative doubles order like their bits) plus the
-//      flat index r*K + j.  A merge sort by rank: each request's candidates
-//      already form a sorted run, and each level merges runs pairwise with
-//      one binary search per candidate (E = Np/1024 candidates per thread);
-//   3. block-wide fp64 inclusive scan of the sorted a: tau_n = R + sum_{m<=n} a_m;
-//   4. Theta_n = tau_n * SPS(R + n + 1); mode 0 stops at the first n whose Theta
-//      does not exceed its predecessor's (Theta_{-1} = R * SPS(R)), mode 1 takes
-//      the first maximum;
+// sched_rank (one workgroup per 16 candidates, the whole GPU):
+//   1. survival a[r][j] = prod_{i<=j} c[r][i] in fp64, multiplied in
+//      increasing j (the same sequence of roundings on every implementation),
+//      recomputed by every workgroup into LDS;
+//   2. the admission order is descending a, ties by the flat index r*K + j.
+//      Instead of sorting, every candidate (a > 0) counts the candidates that
+//      come before it in that order -- its position n -- and sums their a in
+//      the same pass, which gives tau_n = R + sum_{m<=n} a_(m) directly.
+//      Sixteen lanes share a candidate, each taking every 16th key, so a
+//      wave's LDS reads are sixteen consecutive doubles (no bank conflicts)
+//      broadcast to the four candidates of the wave;
+//   3. tau and the flat index are written at position n; workgroup 0 writes
+//      the candidate count.
+// sched_select (one workgroup):
+//   4. Theta_n = tau_n * SPS(R + n + 1); mode 0 stops at the first n whose
+//      Theta does not exceed its predecessor's (Theta_{-1} = R * SPS(R)),
+//      mode 1 takes the first maximum;
 //   5. len[r] = the largest admitted position of r (admission follows each
-//      request's prefix order, since a is non-increasing in j), then cu_q and the
-//      token -> request marker.
+//      request's prefix order, since a is non-increasing in j), then cu_q and
+//      the token -> request marker.
 #include "device_common.h"
 #include "kernels.h"
 
@@ -23,24 +29,20 @@
 
 namespace dspark {
 
-constexpr int kSchedThreads = 1024;
-constexpr int kSchedWaves = kSchedThreads / DSPARK_WAVE;
+constexpr int kRankThreads = 256;
+constexpr int kRankSlices = 16;  // lanes per candidate
+constexpr int kRankCand = kRankThreads / kRankSlices;
+constexpr int kSelThreads = 1024;
+constexpr int kSelWaves = kSelThreads / DSPARK_WAVE;
 
-static int next_pow2(int n) {
-    int p = 1;
-    while (p < n) p <<= 1;
-    return p;
-}
+// workspace: [candidate count | pad to 16 B][tau fp64 x N][flat index int32 x N]
+__host__ __device__ constexpr size_t ws_tau_off() { return 16; }
+__host__ __device__ constexpr size_t ws_idx_off(int N) { return 16 + (size_t)N * 8; }
 
-size_t schedule_lds_bytes(int R, int K) {
-    const int N = R * K;
-    const int Np = next_pow2(N > 0 ? N : 1);
-    size_t b = (size_t)Np * 8 + (size_t)Np * 2;
-    b = (b + 15) & ~(size_t)15;
-    b += (size_t)R * 4;
-    b = (b + 15) & ~(size_t)15;
-    b += (size_t)(N > 0 ? N : 1) * 4;  // staged confidences
-    return b;
+size_t schedule_workspace(int R, int K) {
+    const size_t N = (size_t)R * (K > 0 ? K : 0);
+    const size_t b = 16 + N * 12;
+    return (b + 255) & ~(size_t)255;
 }
 
 __device__ __forceinline__ double sched_conf(float c) {
@@ -49,164 +51,128 @@ __device__ __forceinline__ double sched_conf(float c) {
     return (double)c;
 }
 
-// A sort element: the survival probability's bits (hi, lo) and the flat index.
-struct SKey {
-    uint32_t hi, lo;
-    int idx;
-};
+__global__ __launch_bounds__(kRankThreads) void sched_rank(const float* __restrict__ conf, int R,
+                                                           int K, unsigned char* __restrict__ ws) {
+    extern __shared__ __align__(16) double a_l[];  // [N] survival, then [N] staged confidences
+    float* conf_l = reinterpret_cast<float*>(a_l + (R * K > 0 ? R * K : 1));
+    __shared__ int s_ncand;
+    const int tid = threadIdx.x;
+    const int N = R * K;
+    if (tid == 0) s_ncand = 0;
 
-// "x comes before y": larger a first, equal a by smaller flat index
-__device__ __forceinline__ bool before(const SKey& x, const SKey& y) {
-    if (x.hi != y.hi) return x.hi > y.hi;
-    if (x.lo != y.lo) return x.lo > y.lo;
-    return x.idx < y.idx;
+    // the confidences, staged with coalesced loads: every load of a chunk is
+    // issued before the first is used (indices clamped instead of guarded, so
+    // no load waits behind a branch)
+    for (int base = 0; base < N; base += kRankThreads * 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = conf[min(base + u * kRankThreads + tid, N - 1)];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int i = base + u * kRankThreads + tid;
+            if (i < N) conf_l[i] = v[u];
+        }
+    }
+    __syncthreads();
+
+    // 1. survival products, one request per thread
+    int my_cand = 0;
+    for (int r = tid; r < R; r += kRankThreads) {
+        double p = 1.0;
+#pragma unroll 4
+        for (int j = 0; j < K; ++j) {
+            p = p * sched_conf(conf_l[r * K + j]);
+            a_l[r * K + j] = p;
+            my_cand += p > 0.0;
+        }
+    }
+    if (blockIdx.x == 0 && my_cand) atomicAdd(&s_ncand, my_cand);
+    __syncthreads();
+
+    // 2. position of each candidate in the admission order, and the sum of
+    // the a admitted before it
+    const int s = tid % kRankSlices;
+    const int x = blockIdx.x * kRankCand + tid / kRankSlices;
+    const double ax = x < N ? a_l[x] : 0.0;
+    // y comes before x iff a_y > a_x, or a_y == a_x and y < x: over y < x
+    // the test is a_y >= a_x, over y > x it is a_y > a_x
+    int cnt = 0;
+    double sum = 0.0;
+    if (ax > 0.0) {
+#pragma unroll 8
+        for (int i = s; i < x; i += kRankSlices) {
+            const double ay = a_l[i];
+            const bool b = ay >= ax;
+            cnt += b;
+            sum = sum + (b ? ay : 0.0);
+        }
+        const int i1 = x + 1 + ((s - (x + 1)) & (kRankSlices - 1));  // first i > x with i % 16 == s
+#pragma unroll 8
+        for (int i = i1; i < N; i += kRankSlices) {
+            const double ay = a_l[i];
+            const bool b = ay > ax;
+            cnt += b;
+            sum = sum + (b ? ay : 0.0);
+        }
+    }
+#pragma unroll
+    for (int o = kRankSlices / 2; o > 0; o >>= 1) {
+        cnt += __shfl_xor(cnt, o, DSPARK_WAVE);
+        sum = sum + __shfl_xor(sum, o, DSPARK_WAVE);
+    }
+
+    // 3. scatter by position
+    double* tau = reinterpret_cast<double*>(ws + ws_tau_off());
+    int32_t* idx = reinterpret_cast<int32_t*>(ws + ws_idx_off(N));
+    if (s == 0 && ax > 0.0) {
+        tau[cnt] = (double)R + (sum + ax);
+        idx[cnt] = x;
+    }
+    if (blockIdx.x == 0 && tid == 0) *reinterpret_cast<int32_t*>(ws) = s_ncand;
 }
 
 template <int E>
-__global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
-    const float* __restrict__ conf, int R, int K, const double* __restrict__ sps, int mode,
-    int Np, int32_t* __restrict__ len_out, int32_t* __restrict__ cu_q,
-    int32_t* __restrict__ tok_req) {
-    extern __shared__ __align__(16) unsigned char smem[];
-    uint64_t* key = reinterpret_cast<uint64_t*>(smem);
-    uint16_t* idx = reinterpret_cast<uint16_t*>(key + Np);
-    const size_t len_off = (((size_t)Np * 10) + 15) & ~(size_t)15;
-    int32_t* lenl = reinterpret_cast<int32_t*>(smem + len_off);
-    float* confl = reinterpret_cast<float*>(smem + ((len_off + (size_t)R * 4 + 15) & ~(size_t)15));
-
-    __shared__ double s_wave_tot[kSchedWaves];
+__global__ __launch_bounds__(kSelThreads) void sched_select(
+    const unsigned char* __restrict__ ws, int R, int K, const double* __restrict__ sps, int mode,
+    int32_t* __restrict__ len_out, int32_t* __restrict__ cu_q, int32_t* __restrict__ tok_req) {
+    extern __shared__ int32_t lenl[];  // [R]
     __shared__ int s_first;
-    __shared__ int s_ncand;
-    __shared__ double s_best_v[kSchedWaves];
-    __shared__ int s_best_n[kSchedWaves];
-    __shared__ int s_wave_int[kSchedWaves];
+    __shared__ double s_best_v[kSelWaves];
+    __shared__ int s_best_n[kSelWaves];
+    __shared__ int s_wave_int[kSelWaves];
 
     const int tid = threadIdx.x;
     const int lane = tid & (DSPARK_WAVE - 1);
     const int wave = tid / DSPARK_WAVE;
     const int N = R * K;
-    const int i0 = tid * E;  // this thread's sorted positions i0 .. i0 + E - 1
+    const double* tau_s = reinterpret_cast<const double*>(ws + ws_tau_off());
+    const int32_t* idx_s = reinterpret_cast<const int32_t*>(ws + ws_idx_off(N));
 
-    // the throughput table at the positions this thread will examine (sorted
-    // position n needs SPS(R + n) and SPS(R + n + 1)), loaded while sorting
-    double spsv[E + 1];
-#pragma unroll
-    for (int e = 0; e <= E; ++e) spsv[e] = (i0 + e <= N) ? sps[R + i0 + e] : 0.0;
-    const double sps_r = sps[R];
-
-    if (tid == 0) s_ncand = 0;
-    // 1. survival products, one request per thread; the confidences are first
-    // staged in LDS with coalesced loads
-    for (int i = tid; i < N; i += kSchedThreads) confl[i] = conf[i];
-    __syncthreads();
-    int my_cand = 0;
-    for (int r = tid; r < R; r += kSchedThreads) {
-        double p = 1.0;
-        for (int j0 = 0; j0 < K; j0 += 16) {
-            float c[16];
-#pragma unroll
-            for (int jj = 0; jj < 16; ++jj) c[jj] = j0 + jj < K ? confl[r * K + j0 + jj] : 1.0f;
-#pragma unroll
-            for (int jj = 0; jj < 16; ++jj) {
-                if (j0 + jj >= K) break;
-                p = p * sched_conf(c[jj]);
-                key[r * K + j0 + jj] = (uint64_t)__double_as_longlong(p);
-                idx[r * K + j0 + jj] = (uint16_t)(r * K + j0 + jj);
-                my_cand += p > 0.0;
-            }
-        }
-        lenl[r] = 0;
-    }
-    for (int i = N + tid; i < Np; i += kSchedThreads) {
-        key[i] = 0;
-        idx[i] = (uint16_t)i;  // unique, after every real candidate of equal key
-    }
-    if (my_cand) atomicAdd(&s_ncand, my_cand);
-    __syncthreads();
-
-    // 2. merge sort by rank.  Runs of S sorted candidates are merged pairwise:
-    // a candidate at in-run index li moves to (run pair start) + li + (the
-    // number of the partner run's candidates that come before it), found by a
-    // branchless binary search of the partner run.  "before" is a strict total
-    // order (the flat index breaks every tie; padding slots carry their own
-    // position as index), so the new positions form a permutation.  Each
-    // request's K candidates are sorted already (a is non-increasing in j), so
-    // for a power-of-two K the merging starts at runs of K.
-    SKey v[E];
-    int pos[E];
+    // every load up front (positions past the candidate count are read but
+    // never used): this thread's positions i0 .. i0 + E - 1, tau at i0 - 1,
+    // and SPS(R + n + 1) at each position n, SPS(R + i0) before them
+    // (indices are clamped, not guarded, so that no load waits behind a
+    // branch; the workspace holds at least 256 bytes and sps at least R + N + 1
+    // entries, so every clamped index is in bounds, N = 0 included)
+    const int i0 = tid * E;
+    const int nmax = N > 0 ? N - 1 : 0;
+    double tv[E], sv[E];
+    int iv[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-        const int i = i0 + e;
-        const bool in = i < Np;
-        const uint64_t kk = in ? key[i] : 0;
-        v[e] = SKey{(uint32_t)(kk >> 32), (uint32_t)kk, in ? (int)idx[i] : 0};
-        pos[e] = i;
+        const int n = min(i0 + e, nmax);
+        tv[e] = tau_s[n];
+        sv[e] = sps[min(R + i0 + e + 1, R + N)];
+        iv[e] = idx_s[n];
     }
-    // (K = 0 has no candidates; S must start at 1 or more for the loop to end)
-    for (int S = K > 0 && (K & (K - 1)) == 0 ? K : 1; S < Np; S <<= 1) {
-        int cnt[E];
-#pragma unroll
-        for (int e = 0; e < E; ++e) cnt[e] = 0;
-        for (int b = S; b > 0; b >>= 1) {
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-                if (pos[e] >= Np || cnt[e] + b > S) continue;
-                const int pb = (pos[e] & ~(S - 1)) ^ S;  // the partner run's first position
-                const int t = pb + cnt[e] + b - 1;
-                const uint64_t kk = key[t];
-                const SKey o{(uint32_t)(kk >> 32), (uint32_t)kk, (int)idx[t]};
-                if (before(o, v[e])) cnt[e] += b;
-            }
-        }
-        __syncthreads();  // every read of this level is done
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-            if (pos[e] >= Np) continue;
-            pos[e] = (pos[e] & ~(2 * S - 1)) + (pos[e] & (S - 1)) + cnt[e];
-            key[pos[e]] = ((uint64_t)v[e].hi << 32) | v[e].lo;
-            idx[pos[e]] = (uint16_t)v[e].idx;
-        }
-        __syncthreads();  // the merged runs are visible
-    }
-    const int ncand = s_ncand;
+    const double tprev = tau_s[min(max(i0 - 1, 0), nmax)];
+    const double sprev = sps[min(R + i0, R + N)];
+    const double theta0 = (double)R * sps[R];
+    const int ncand = *reinterpret_cast<const int32_t*>(ws);  // written by sched_rank, N = 0 too
 
-    // 3. inclusive scan of the sorted survival probabilities (fp64); thread t
-    // owns positions i0 .. i0 + E - 1 (E = 1 covers all when Np <= 1024)
-    double loc[E];
-    double run = 0.0;
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-        const int n = i0 + e;
-        const double a = (n < ncand) ? __longlong_as_double((long long)key[n]) : 0.0;
-        run = run + a;
-        loc[e] = run;
-    }
-    // wave inclusive scan of the per-thread totals
-    double incl = run;
-#pragma unroll
-    for (int o = 1; o < DSPARK_WAVE; o <<= 1) {
-        const double t = __shfl_up(incl, o, DSPARK_WAVE);
-        if (lane >= o) incl = incl + t;
-    }
-    if (lane == DSPARK_WAVE - 1) s_wave_tot[wave] = incl;
-    __syncthreads();
-    double wave_off = 0.0;
-    for (int w = 0; w < wave; ++w) wave_off = wave_off + s_wave_tot[w];
-    const double excl = wave_off + (incl - run);
-    const double Rd = (double)R;
-    // tau at this thread's positions, and at the position before them
-    double tau[E];
-#pragma unroll
-    for (int e = 0; e < E; ++e) tau[e] = Rd + (excl + loc[e]);
-    // Theta of position n - 1 for the first position of each thread: the
-    // previous thread's last tau (theta0 for position 0)
-    const double tau_prev_last = __shfl_up(tau[E - 1], 1, DSPARK_WAVE);
-    __shared__ double s_wave_last_tau[kSchedWaves];
-    if (lane == DSPARK_WAVE - 1) s_wave_last_tau[wave] = tau[E - 1];
+    for (int r = tid; r < R; r += kSelThreads) lenl[r] = 0;
     if (tid == 0) s_first = ncand;
     __syncthreads();
-    const double theta0 = Rd * sps_r;
-    double prev_tau = lane > 0 ? tau_prev_last : (wave > 0 ? s_wave_last_tau[wave - 1] : 0.0);
 
     // 4. throughput along the greedy path and the stop rule
     int n_adm;
@@ -216,9 +182,12 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
         for (int e = 0; e < E; ++e) {
             const int n = i0 + e;
             if (n >= ncand) break;
-            const double th = tau[e] * spsv[e + 1];
-            const double prev = n == 0 ? theta0 : (e == 0 ? prev_tau : tau[e - 1]) * spsv[e];
-            if (!(th > prev)) { first = n; break; }
+            const double th = tv[e] * sv[e];
+            const double prev = n == 0 ? theta0 : (e == 0 ? tprev * sprev : tv[e - 1] * sv[e - 1]);
+            if (!(th > prev)) {
+                first = n;
+                break;
+            }
         }
         if (first < ncand) atomicMin(&s_first, first);
         __syncthreads();
@@ -230,22 +199,31 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
         for (int e = 0; e < E; ++e) {
             const int n = i0 + e;
             if (n >= ncand) break;
-            const double th = tau[e] * spsv[e + 1];
-            if (th > bv) { bv = th; bn = n; }
+            const double th = tv[e] * sv[e];
+            if (th > bv) {
+                bv = th;
+                bn = n;
+            }
         }
         if (tid != 0 && bn == -1) bn = 0x7fffffff;
 #pragma unroll
         for (int o = 1; o < DSPARK_WAVE; o <<= 1) {
             const double ov = __shfl_xor(bv, o, DSPARK_WAVE);
             const int on = __shfl_xor(bn, o, DSPARK_WAVE);
-            if (ov > bv || (ov == bv && on < bn)) { bv = ov; bn = on; }
+            if (ov > bv || (ov == bv && on < bn)) {
+                bv = ov;
+                bn = on;
+            }
         }
-        if (lane == 0) { s_best_v[wave] = bv; s_best_n[wave] = bn; }
+        if (lane == 0) {
+            s_best_v[wave] = bv;
+            s_best_n[wave] = bn;
+        }
         __syncthreads();
         if (tid == 0) {
             double v = s_best_v[0];
             int n = s_best_n[0];
-            for (int w = 1; w < kSchedWaves; ++w)
+            for (int w = 1; w < kSelWaves; ++w)
                 if (s_best_v[w] > v || (s_best_v[w] == v && s_best_n[w] < n)) {
                     v = s_best_v[w];
                     n = s_best_n[w];
@@ -257,14 +235,15 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
     }
 
     // 5. lengths: the largest admitted position of each request
-    for (int n = tid; n < n_adm; n += kSchedThreads) {
-        const int i = idx[n];
-        atomicMax(&lenl[i / K], i % K + 1);
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int n = i0 + e;
+        if (n < n_adm) atomicMax(&lenl[iv[e] / K], iv[e] % K + 1);
     }
     __syncthreads();
 
     // cu_q: exclusive scan of 1 + len over requests (contiguous ranges per thread)
-    const int per = (R + kSchedThreads - 1) / kSchedThreads;
+    const int per = (R + kSelThreads - 1) / kSelThreads;
     const int r0 = tid * per;
     const int r1 = min(R, r0 + per);
     int tot = 0;
@@ -291,41 +270,44 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
     if (r1 == R && r0 < r1) {
         if (cu_q) cu_q[R] = off;
     }
-    if (R == 0 && tid == 0 && cu_q) cu_q[0] = 0;
     if (tok_req) {
         // total = sum(1 + len) from the scan totals, so every thread can clear the tail
         int total = 0;
-        for (int w = 0; w < kSchedWaves; ++w) total += s_wave_int[w];
-        for (int i = total + tid; i < R * (K + 1); i += kSchedThreads) tok_req[i] = -1;
+        for (int w = 0; w < kSelWaves; ++w) total += s_wave_int[w];
+        for (int i = total + tid; i < R * (K + 1); i += kSelThreads) tok_req[i] = -1;
     }
 }
 
 template <int E>
-static hipError_t launch_e(const float* conf, int R, int K, const double* sps, int mode, int Np,
-                           size_t lds, int32_t* len, int32_t* cu_q, int32_t* tok_req,
-                           hipStream_t s) {
-    if (lds > 64 * 1024) {
-        hipError_t e = hipFuncSetAttribute((const void*)schedule_kernel<E>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return e;
-    }
-    hipLaunchKernelGGL(schedule_kernel<E>, dim3(1), dim3(kSchedThreads), lds, s, conf, R, K, sps,
-                       mode, Np, len, cu_q, tok_req);
+static hipError_t launch_select(const unsigned char* ws, int R, int K, const double* sps,
+                                int mode, int32_t* len, int32_t* cu_q, int32_t* tok_req,
+                                hipStream_t s) {
+    hipLaunchKernelGGL(sched_select<E>, dim3(1), dim3(kSelThreads), (size_t)R * 4, s, ws, R, K,
+                       sps, mode, len, cu_q, tok_req);
     return hipGetLastError();
 }
 
 hipError_t launch_schedule(const float* conf, int R, int K, const double* sps, int mode,
-                           int32_t* len, int32_t* cu_q, int32_t* tok_req, hipStream_t s) {
+                           int32_t* len, int32_t* cu_q, int32_t* tok_req, void* ws,
+                           hipStream_t s) {
     const int N = R * K;
-    const int Np = next_pow2(N > 0 ? N : 1);
-    const size_t lds = schedule_lds_bytes(R, K);
-    // keys per thread (N <= 8192)
-    switch (Np <= kSchedThreads ? 1 : Np / kSchedThreads) {
-        case 1: return launch_e<1>(conf, R, K, sps, mode, Np, lds, len, cu_q, tok_req, s);
-        case 2: return launch_e<2>(conf, R, K, sps, mode, Np, lds, len, cu_q, tok_req, s);
-        case 4: return launch_e<4>(conf, R, K, sps, mode, Np, lds, len, cu_q, tok_req, s);
-        default: return launch_e<8>(conf, R, K, sps, mode, Np, lds, len, cu_q, tok_req, s);
+    unsigned char* w = static_cast<unsigned char*>(ws);
+    const size_t lds = (size_t)(N > 0 ? N : 1) * 12;
+    if (lds >= 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute((const void*)sched_rank,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
     }
+    const int grid = N > 0 ? (N + kRankCand - 1) / kRankCand : 1;
+    hipLaunchKernelGGL(sched_rank, dim3(grid), dim3(kRankThreads), lds, s, conf, R, K, w);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    // positions per thread of the selection (N <= 8192)
+    const int per = (N + kSelThreads - 1) / kSelThreads;
+    if (per <= 1) return launch_select<1>(w, R, K, sps, mode, len, cu_q, tok_req, s);
+    if (per <= 2) return launch_select<2>(w, R, K, sps, mode, len, cu_q, tok_req, s);
+    if (per <= 4) return launch_select<4>(w, R, K, sps, mode, len, cu_q, tok_req, s);
+    return launch_select<8>(w, R, K, sps, mode, len, cu_q, tok_req, s);
 }
 
 }  // namespace dspark

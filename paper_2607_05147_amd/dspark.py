@@ -128,7 +128,7 @@ def dspark_schedule_workspace_size(R: int, K: int) -> int:
 def dspark_schedule(conf: torch.Tensor, sps: torch.Tensor, mode: int = 0,
                     len_out: Optional[torch.Tensor] = None, cu_q: Optional[torch.Tensor] = None,
                     tok_req: Optional[torch.Tensor] = None, want_tok_req: bool = False,
-                    stream=None):
+                    ws: Optional[torch.Tensor] = None, stream=None):
     """conf fp32 [R, K], sps fp64 [> R*(K+1)] -> (len int32 [R], cu_q int32 [R+1], tok_req|None)."""
     _dev(conf, "conf", torch.float32)
     if conf.dim() != 2:
@@ -145,8 +145,9 @@ def dspark_schedule(conf: torch.Tensor, sps: torch.Tensor, mode: int = 0,
     _dev(len_out, "len", torch.int32, (R,))
     _dev(cu_q, "cu_q", torch.int32, (R + 1,))
     _dev(tok_req, "tok_req", torch.int32, (R * (K + 1),), optional=True)
+    ws, ws_bytes = _workspace(dspark_schedule_workspace_size(R, K), dev, ws)
     st = lib().dspark_schedule(_p(conf), R, K, _p(sps), sps.numel(), mode, _p(len_out), _p(cu_q),
-                               _p(tok_req), None, 0, _stream(stream))
+                               _p(tok_req), _p(ws), ws_bytes, _stream(stream))
     _raise(st, "dspark_schedule")
     return len_out, cu_q, tok_req
 

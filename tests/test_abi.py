@@ -51,8 +51,11 @@ def test_abi_version_matches_header(L):
     assert L.dspark_abi_version() == int(m.group(1))
 
 
-def _sched(L, conf=FAKE, R=4, K=8, sps=FAKE, sps_len=100, mode=0, ln=FAKE):
-    return L.dspark_schedule(conf, R, K, sps, sps_len, mode, ln, None, None, None, 0, None)
+def _sched(L, conf=FAKE, R=4, K=8, sps=FAKE, sps_len=100, mode=0, ln=FAKE, ws=FAKE,
+           ws_bytes=None):
+    if ws_bytes is None:
+        ws_bytes = L.dspark_schedule_workspace_size(R, K)
+    return L.dspark_schedule(conf, R, K, sps, sps_len, mode, ln, None, None, ws, ws_bytes, None)
 
 
 def test_schedule_validation(L):
@@ -66,6 +69,15 @@ def test_schedule_validation(L):
     assert _sched(L, sps_len=36) == ESHAPE  # must exceed R*(K+1) = 36
     assert _sched(L, R=8192, K=2, sps_len=10**6) == EUNSUPPORTED
     assert _sched(L, conf=C.c_void_p((1 << 20) + 2)) == EINVAL  # misaligned
+
+
+def test_schedule_workspace(L):
+    need = L.dspark_schedule_workspace_size(4, 8)
+    assert need >= 16 + 12 * 32 and need % 256 == 0
+    assert L.dspark_schedule_workspace_size(0, 8) == 0
+    assert _sched(L, ws=None) == EWORKSPACE
+    assert _sched(L, ws_bytes=need - 1) == EWORKSPACE
+    assert _sched(L, ws=C.c_void_p((1 << 20) + 64)) == EWORKSPACE  # not 256-aligned
 
 
 def test_last_error_describes_failure(L):
