@@ -333,13 +333,20 @@ def main():
     torch.cuda.synchronize()
     accepted = copies[0]["acc"].cpu().numpy()
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    # the timed region: exactly K steps and nothing else on the stream
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for i in range(args.steps):
-        step(copies[i % NCOPY], evs[i])
+        step(copies[i % NCOPY])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
+    # per-stage times from a second, separate pass with events between the
+    # stages (each event record leaves the GPU idle for a few microseconds,
+    # so these passes are kept out of the timed region)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    for i in range(args.steps):
+        step(copies[i % NCOPY], evs[i])
+    torch.cuda.synchronize()
     sched_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
     attn_ms = np.array([e[1].elapsed_time(e[2]) for e in evs])
     acc_ms = np.array([e[2].elapsed_time(e[3]) for e in evs])
