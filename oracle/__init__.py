@@ -48,9 +48,12 @@ def _load():
         lib.oracle_accept.argtypes = [p, p, p, i32, i64, p, p, i32, i32, i32, f64, p, p, p, p]
         lib.oracle_markov_draft.argtypes = [p, p, i32, i64, p, p, i32, p, p, i32, p, p, f64, i32,
                                             i32, i32, p, p, p, p]
+        lib.oracle_rnn_draft.argtypes = [p, p, i32, i64, p, p, p, i32, p, p, i32, p, p, f64, i32,
+                                         i32, i32, p, p, p, p]
         lib.oracle_threads.argtypes = []
         for f in (lib.oracle_survival, lib.oracle_schedule, lib.oracle_verify_attn,
-                  lib.oracle_accept, lib.oracle_markov_draft, lib.oracle_threads):
+                  lib.oracle_accept, lib.oracle_markov_draft, lib.oracle_rnn_draft,
+                  lib.oracle_threads):
             f.restype = C.c_int
         _lib = lib
     return _lib
@@ -206,4 +209,41 @@ def markov_draft(anchor, U, u_dtype: str, W1, W2t, w_conf, u, K: int, V: int,
                                      _ptr(hid), _ptr(wc), d, _ptr(st), _ptr(uu), it, R, K, V,
                                      _ptr(tok), _ptr(dp), _ptr(conf), _ptr(mg))
     _check(rc, "markov_draft")
+    return tok, dp, conf, mg
+
+
+def rnn_draft(anchor, U, u_dtype: str, W1, W2t, Wrnn, w_conf, u, K: int, V: int,
+              hidden=None, sts_temp=None, inv_temperature: float = 1.0,
+              ld: Optional[int] = None, want_p: bool = True):
+    """RNN-head draft block.  As markov_draft, plus Wrnn: [3 rank, 2 rank + d]
+    bf16 bits (gate, candidate and output rows; columns [s; e; h]).  Returns
+    (draft_tok int32[R, K], draft_p f64[R, K, V] or None, conf f64[R, K],
+    margin f64[R, K])."""
+    dt = 0 if u_dtype == "f32" else 1
+    store = np.float32 if dt == 0 else np.uint16
+    U = _c(U, store)
+    if ld is None:
+        ld = U.shape[-1]
+    anc = _c(anchor, np.int32)
+    R = len(anc)
+    W1 = _c(W1, np.uint16)
+    W2t = _c(W2t, np.uint16)
+    Wr = _c(Wrnn, np.uint16)
+    rank = W1.shape[1]
+    hid = None if hidden is None else _c(hidden, np.uint16)
+    d = 0 if hid is None else hid.shape[-1]
+    if Wr.shape != (3 * rank, 2 * rank + d):
+        raise ValueError(f"Wrnn must be [{3 * rank}, {2 * rank + d}], got {Wr.shape}")
+    wc = _c(w_conf, np.float32)
+    st = None if sts_temp is None else _c(sts_temp, np.float32)
+    uu = _c(u, np.float32)
+    tok = np.zeros((R, K), dtype=np.int32)
+    dp = np.empty((R, K, V), dtype=np.float64) if want_p else None
+    conf = np.zeros((R, K), dtype=np.float64)
+    mg = np.zeros((R, K), dtype=np.float64)
+    it = float(np.float32(inv_temperature))
+    rc = _load().oracle_rnn_draft(_ptr(anc), _ptr(U), dt, ld, _ptr(W1), _ptr(W2t), _ptr(Wr), rank,
+                                  _ptr(hid), _ptr(wc), d, _ptr(st), _ptr(uu), it, R, K, V,
+                                  _ptr(tok), _ptr(dp), _ptr(conf), _ptr(mg))
+    _check(rc, "rnn_draft")
     return tok, dp, conf, mg

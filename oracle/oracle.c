@@ -13,8 +13,8 @@
  *   - acceptance is the left-to-right speculative acceptance rule of the
  *     background section on speculative decoding, with the conventions listed
  *     at each function;
- *   - the Markov-head draft block follows the left-to-right factorisation of
- *     the semi-autoregressive stage, one position at a time.
+ *   - the Markov-head and RNN-head draft blocks follow the left-to-right
+ *     factorisation of the semi-autoregressive stage, one position at a time.
  * All arithmetic is fp64; bf16 inputs are widened exactly.  OpenMP only runs
  * independent rows side by side; no row's arithmetic is reordered.
  *
@@ -489,6 +489,102 @@ int oracle_markov_draft(const int32_t* anchor, const void* U, int u_dtype, int64
         }
         free(z);
         free(e);
+    }
+    return bad ? ORACLE_EINVAL : ORACLE_OK;
+}
+
+/* --------------------------------------------------- RNN-head draft block */
+
+static double sigmoid(double x) { return 1.0 / (1.0 + exp(-x)); }
+
+/*
+ * The sequential stage with the RNN head (section on semi-autoregressive
+ * generation, the RNN-head item, eq. rnn): the same left-to-right
+ * factorisation as the Markov head, with the transition bias read from a
+ * recurrent state that sees the whole prefix of the block.
+ *
+ * For every request r, with x_0 = anchor[r], s_0 = 0 and k = 1 .. K:
+ *   e_k    = W1[x_{k-1}]
+ *   z_k    = [s_{k-1}; e_k; h_k]                     (2 rank + d values)
+ *   a_k    = W z_k, W = [W_g; W_c; W_o]              (3 rank values)
+ *   s_k    = sigmoid(a_g) * s_{k-1} + (1 - sigmoid(a_g)) * tanh(a_c)
+ *   B_k(v) = sum_j W2[j, v] * tanh(a_o)[j]
+ *   p_k    = softmax(inv_temp * (U_k + B_k)),   x_k = inverse CDF at u[r, k-1]
+ *   c_k    = sigmoid((w_h . h_k + w_e . e_k) / T_k)  (eq. confidence)
+ * Storage as oracle_markov_draft, plus Wrnn [3 rank, 2 rank + d] bf16
+ * row-major: rows 0 .. rank-1 the gate, then the candidate, then the output
+ * component; columns in the order of z_k.  The equation has no bias terms.
+ */
+int oracle_rnn_draft(const int32_t* anchor, const void* U, int u_dtype, int64_t ld,
+                     const uint16_t* W1, const uint16_t* W2t, const uint16_t* Wrnn, int rank,
+                     const uint16_t* hidden, const float* w_conf, int d,
+                     const float* sts_temp, const float* u, double inv_temp, int R, int K,
+                     int V, int32_t* draft_tok, double* draft_p, double* conf,
+                     double* margin) {
+    if (!anchor || !U || !W1 || !W2t || !Wrnn || !w_conf || !u || !draft_tok || !conf)
+        return ORACLE_EINVAL;
+    if (R < 0 || K < 1 || V < 1 || rank < 1 || d < 0 || ld < V || (d > 0 && !hidden))
+        return ORACLE_EINVAL;
+    for (int r = 0; r < R; ++r)
+        if (anchor[r] < 0 || anchor[r] >= V) return ORACLE_EINVAL;
+    const int nz = 2 * rank + d;
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(|| : bad)
+    for (int r = 0; r < R; ++r) {
+        double* zl = (double*)malloc(sizeof(double) * (size_t)V);
+        double* zin = (double*)malloc(sizeof(double) * (size_t)nz);
+        double* act = (double*)malloc(sizeof(double) * (size_t)(3 * rank));
+        double* st = (double*)calloc((size_t)rank, sizeof(double));
+        double* o = (double*)malloc(sizeof(double) * (size_t)rank);
+        if (!zl || !zin || !act || !st || !o) {
+            bad = 1;
+            free(zl); free(zin); free(act); free(st); free(o);
+            continue;
+        }
+        int prev = anchor[r];
+        for (int k = 1; k <= K; ++k) {
+            const int64_t row = (int64_t)r * K + (k - 1);
+            /* z_k = [s_{k-1}; W1[x_{k-1}]; h_k] */
+            for (int j = 0; j < rank; ++j) zin[j] = st[j];
+            for (int j = 0; j < rank; ++j) zin[rank + j] = bf16_to_f64(W1[(int64_t)prev * rank + j]);
+            for (int i = 0; i < d; ++i) zin[2 * rank + i] = bf16_to_f64(hidden[row * d + i]);
+            /* the single projection, split into gate, candidate and output */
+            for (int i = 0; i < 3 * rank; ++i) {
+                double acc = 0.0;
+                for (int j = 0; j < nz; ++j) acc += bf16_to_f64(Wrnn[(int64_t)i * nz + j]) * zin[j];
+                act[i] = acc;
+            }
+            /* gated state update (uses s_{k-1} through zin only) and the head's output */
+            for (int j = 0; j < rank; ++j) {
+                const double g = sigmoid(act[j]);
+                st[j] = g * st[j] + (1.0 - g) * tanh(act[rank + j]);
+                o[j] = tanh(act[2 * rank + j]);
+            }
+            /* B_k = W2^T o, then the softmax of inv_temp * (U_k + B_k) */
+            double m = -INFINITY;
+            for (int v = 0; v < V; ++v) {
+                double b = 0.0;
+                for (int j = 0; j < rank; ++j) b += bf16_to_f64(W2t[(int64_t)v * rank + j]) * o[j];
+                zl[v] = inv_temp * (elem(U, row * ld + v, u_dtype) + b);
+                if (zl[v] > m) m = zl[v];
+            }
+            double S = 0.0;
+            for (int v = 0; v < V; ++v) { zl[v] = exp(zl[v] - m); S += zl[v]; }
+            for (int v = 0; v < V; ++v) zl[v] = zl[v] / S;
+            if (draft_p) memcpy(draft_p + row * (int64_t)V, zl, sizeof(double) * (size_t)V);
+            double mg;
+            const int x = inverse_cdf(zl, V, (double)u[row], &mg);
+            if (margin) margin[row] = mg;
+            draft_tok[row] = x;
+            /* confidence: the backbone state and the embedding of x_{k-1} */
+            double sacc = 0.0;
+            for (int i = 0; i < d; ++i) sacc += (double)w_conf[i] * zin[2 * rank + i];
+            for (int j = 0; j < rank; ++j) sacc += (double)w_conf[d + j] * zin[rank + j];
+            const double T = sts_temp ? (double)sts_temp[k - 1] : 1.0;
+            conf[row] = sigmoid(sacc / T);
+            prev = x;
+        }
+        free(zl); free(zin); free(act); free(st); free(o);
     }
     return bad ? ORACLE_EINVAL : ORACLE_OK;
 }
