@@ -45,7 +45,9 @@ def parse():
     ap.add_argument("--workload", default="serving")
     ap.add_argument("--stage", default="step", choices=["step", "draft"],
                     help="step: the verification step (schedule, attention, acceptance); "
-                         "draft: the Markov-head draft block that produces its inputs")
+                         "draft: the draft block that produces its inputs")
+    ap.add_argument("--head", default="markov", choices=["markov", "rnn"],
+                    help="the draft block's sequential head (--stage draft)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample")
@@ -99,9 +101,12 @@ ATTN_PATHS = {
                "bound": "mfma"},
     "generic": {"src": "attn_generic.hip", "kernels": ("attn_generic_kernel", "attn_generic_merge"),
                 "bound": "hbm"},
-    # not attention: the draft block's launches (four per draft position)
+    # not attention: the draft blocks' launches
     "draft": {"src": "markov.hip", "kernels": ("md_hidden", "md_first", "md_tile", "md_stats"),
               "bound": "hbm"},
+    "rnn_draft": {"src": "markov.hip", "kernels": ("md_hidden", "rnn_hproj", "md_first", "rnn_state",
+                                                   "md_tile", "md_stats"),
+                  "bound": "hbm"},
 }
 
 
@@ -117,8 +122,8 @@ def attn_path(w, bf16: bool) -> str:
 
 
 def path_of_workload(name: str) -> str:
-    if name == "draft":
-        return "draft"
+    if name in ("draft", "rnn_draft"):
+        return name
     import paper_2607_05147_amd.synth as synth
     w = synth.WORKLOADS[name]
     return attn_path(w, w.kv_elem_bytes == 2)
@@ -127,6 +132,8 @@ def path_of_workload(name: str) -> str:
 def traffic_file(workload: str) -> str:
     if workload == "draft":
         return os.path.join(HERE, "profiles", "markov_draft_serving_traffic.json")
+    if workload == "rnn_draft":
+        return os.path.join(HERE, "profiles", "rnn_draft_serving_traffic.json")
     return os.path.join(HERE, "profiles", f"verify_attn_{workload}_traffic.json")
 
 
@@ -161,12 +168,13 @@ def traffic_from(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, workload=
     def per_call(path):
         rows = _counter_rows(path)
         calls = sum(1 for name, _ in rows if kernels[1] in name)
-        if workload == "draft":  # one md_first launch per call
+        if workload in ("draft", "rnn_draft"):  # one md_first launch per call
             calls = sum(1 for name, _ in rows if "md_first" in name)
         tot = {k: sum(v for name, v in rows if k in name) for k in kernels}
         return {k: tot[k] / calls * 1024.0 for k in kernels}, calls
 
-    sel = "--stage draft" if workload == "draft" else f"--workload {workload}"
+    sel = {"draft": "--stage draft", "rnn_draft": "--stage draft --head rnn"}.get(
+        workload, f"--workload {workload}")
     sf, sw = copy_scale(copy_fetch_csv), copy_scale(copy_write_csv)
     fetch, calls = per_call(fetch_csv)
     write, _ = per_call(write_csv)
@@ -181,9 +189,9 @@ def traffic_from(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, workload=
         "source_sha256": source_sha(os.path.join(CSRC, path["src"])),
         "commands": [
             f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d <dir> -o pmc -- python bench.py "
-            f"{sel} --steps 5 --warmup 1 --no-cpu-baseline",
+            f"{sel} --steps 2 --warmup 1 --no-cpu-baseline",
             f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d <dir> -o pmc -- python bench.py "
-            f"{sel} --steps 5 --warmup 1 --no-cpu-baseline",
+            f"{sel} --steps 2 --warmup 1 --no-cpu-baseline",
             "rocprofv3 --pmc FETCH_SIZE --output-format csv -d <dir> -o pmc -- python bench.py --copy-probe",
             "rocprofv3 --pmc WRITE_SIZE --output-format csv -d <dir> -o pmc -- python bench.py --copy-probe",
             f"python bench.py {sel} --traffic-from <the four pmc_counter_collection.csv files>",
@@ -228,7 +236,7 @@ def copy_probe():
 def main():
     args = parse()
     if args.traffic_from:
-        traffic_from(*args.traffic_from, workload="draft" if args.stage == "draft" else args.workload)
+        traffic_from(*args.traffic_from, workload=draft_key(args) if args.stage == "draft" else args.workload)
         return
     if args.copy_probe:
         copy_probe()
@@ -412,10 +420,25 @@ def draft_bytes(w, rank: int, d: int, base_bytes: int) -> int:
     return w.K * per_pos + w.R * w.K * (d * 2 + rank * 2 + 16) + (d + rank) * 4
 
 
+def rnn_draft_bytes(w, rank: int, d: int, base_bytes: int) -> int:
+    """Algorithmic HBM bytes of one RNN-head draft-block call: the Markov
+    head's, plus the projection's hidden columns read once and its product
+    written once, and per position the state and embedding columns of the
+    projection, that product's row, and the state read and written."""
+    once = 3 * rank * d * 2 + w.R * w.K * 3 * rank * 4
+    per_pos = 3 * rank * 2 * rank * 2 + w.R * 3 * rank * 4 + 2 * w.R * rank * 4
+    return draft_bytes(w, rank, d, base_bytes) + once + w.K * per_pos
+
+
+def draft_key(args) -> str:
+    return "rnn_draft" if args.head == "rnn" else "draft"
+
+
 def draft_bench(args):
-    """Times dspark_markov_draft on the workload's shape (R requests, K draft
-    positions, its vocabulary and logit dtype, rank 256, 4096-wide hidden
-    states) and prints one JSON line."""
+    """Times the draft block (dspark_markov_draft, or dspark_rnn_draft with
+    --head rnn) on the workload's shape (R requests, K draft positions, its
+    vocabulary and logit dtype, rank 256, 4096-wide hidden states) and prints
+    one JSON line."""
     import torch
     import oracle
     from paper_2607_05147_amd import dspark, synth
@@ -423,8 +446,9 @@ def draft_bench(args):
     dev = torch.device("cuda:0")
     w = synth.WORKLOADS[args.workload]
     rank, d = synth.MARKOV_RANK, synth.MARKOV_HIDDEN
+    rnn = args.head == "rnn"
     t0 = time.time()
-    inp = synth.markov_inputs(w, args.seed, rank=rank, d=d)
+    inp = synth.markov_inputs(w, args.seed, rank=rank, d=d, rnn=rnn)
 
     def to_dev(a):
         a = np.ascontiguousarray(a)
@@ -434,43 +458,60 @@ def draft_bench(args):
 
     args_d = dict(anchor=to_dev(inp.anchor), base=to_dev(inp.base), W1=to_dev(inp.W1),
                   W2t=to_dev(inp.W2t), w_conf=to_dev(inp.w_conf), u=to_dev(inp.u),
-                  hidden=to_dev(inp.hidden), sts=to_dev(inp.sts_temp))
+                  hidden=to_dev(inp.hidden), sts=to_dev(inp.sts_temp),
+                  Wrnn=to_dev(inp.Wrnn) if rnn else None)
     tok = torch.empty((w.R, w.K), dtype=torch.int32, device=dev)
     dp = torch.empty((w.R, w.K, w.V), dtype=torch.float32, device=dev)
     conf = torch.empty((w.R, w.K), dtype=torch.float32, device=dev)
-    ws = torch.empty(dspark.dspark_markov_draft_workspace_size(w.R, w.K, w.V, rank), dtype=torch.uint8,
-                     device=dev)
+    ws_size = (dspark.dspark_rnn_draft_workspace_size if rnn else
+               dspark.dspark_markov_draft_workspace_size)(w.R, w.K, w.V, rank)
+    ws = torch.empty(ws_size, dtype=torch.uint8, device=dev)
     torch.cuda.synchronize()
     log(f"draft inputs ready in {time.time() - t0:.1f}s: base logits {inp.base.nbytes / 1e6:.0f} MB, "
         f"W1 + W2t {2 * inp.W1.nbytes / 1e6:.0f} MB")
 
     def call():
-        dspark.dspark_markov_draft(args_d["anchor"], args_d["base"], args_d["W1"], args_d["W2t"],
-                                   args_d["w_conf"], args_d["u"], w.K, hidden=args_d["hidden"],
-                                   sts_temp=args_d["sts"], draft_tok=tok, draft_p=dp, conf=conf,
-                                   ws=ws)
+        if rnn:
+            dspark.dspark_rnn_draft(args_d["anchor"], args_d["base"], args_d["W1"], args_d["W2t"],
+                                    args_d["Wrnn"], args_d["w_conf"], args_d["u"], w.K,
+                                    hidden=args_d["hidden"], sts_temp=args_d["sts"], draft_tok=tok,
+                                    draft_p=dp, conf=conf, ws=ws)
+        else:
+            dspark.dspark_markov_draft(args_d["anchor"], args_d["base"], args_d["W1"], args_d["W2t"],
+                                       args_d["w_conf"], args_d["u"], w.K, hidden=args_d["hidden"],
+                                       sts_temp=args_d["sts"], draft_tok=tok, draft_p=dp, conf=conf,
+                                       ws=ws)
 
     for _ in range(args.warmup):
         call()
     torch.cuda.synchronize()
+    # the timed region: exactly the calls; events in a second pass
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        call()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
     stream = torch.cuda.current_stream()
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in range(args.steps)]
-    t_start = time.perf_counter()
     for e in evs:
         e[0].record(stream)
         call()
         e[1].record(stream)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t_start
     ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
     ms_per = wall * 1e3 / args.steps
-    nbytes = draft_bytes(w, rank, d, w.logit_elem_bytes)
+    nbytes = (rnn_draft_bytes if rnn else draft_bytes)(w, rank, d, w.logit_elem_bytes)
     gbps = nbytes / (ms.mean() / 1e3) / 1e9
-    log(f"draft block: {ms.mean() * 1e3:.1f} us per call ({ms.mean() * 1e3 / w.K:.1f} us per position), "
-        f"{gbps:.0f} GB/s = {gbps / HBM_PEAK_GBPS:.1%} of HBM peak")
+    head = "RNN-head" if rnn else "Markov-head"
+    log(f"{head} draft block: {ms.mean() * 1e3:.1f} us per call ({ms.mean() * 1e3 / w.K:.1f} us per "
+        f"position), {gbps:.0f} GB/s = {gbps / HBM_PEAK_GBPS:.1%} of HBM peak")
+    kernels = ("dspark_rnn_draft: md_hidden + rnn_hproj + md_first, then rnn_state + md_tile<0> + "
+               "md_stats + md_tile<1> per position" if rnn else
+               "dspark_markov_draft: md_hidden + md_first, then md_tile<0> + md_stats + md_tile<1> "
+               "per position")
     result = {
-        "metric": "draft tokens/s and achieved HBM GB/s (% of peak), Markov-head draft block on 1 MI355X",
+        "metric": f"draft tokens/s and achieved HBM GB/s (% of peak), {head} draft block on 1 MI355X",
         "value": w.R * w.K / (ms_per / 1e3),
         "unit": "draft tokens/s",
         "n_gpus": 1,
@@ -482,14 +523,13 @@ def draft_bench(args):
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded; shapes and distributions of the workload)",
-        "config": {"workload": f"markov draft ({w.name} shape): R={w.R} requests, K={w.K} positions, "
-                               f"V={w.V}, rank {rank}, hidden {d}, {w.logit_dtype} base logits",
+        "config": {"workload": f"{args.head} draft ({w.name} shape): R={w.R} requests, K={w.K} "
+                               f"positions, V={w.V}, rank {rank}, hidden {d}, {w.logit_dtype} base logits",
                    "seed": args.seed},
-        "roofline": {"kernel": "dspark_markov_draft: md_hidden + md_first, then md_tile<0> + md_stats + "
-                               "md_tile<1> per position",
+        "roofline": {"kernel": kernels,
                      "bound": "hbm", "achieved": gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": gbps / HBM_PEAK_GBPS, "bytes_per_launch": nbytes,
-                     "traffic": measured_traffic("draft")},
+                     "traffic": measured_traffic(draft_key(args))},
     }
     if not args.no_cpu_baseline:
         # the oracle on the first n requests, n sized to about --cpu-seconds
@@ -497,9 +537,14 @@ def draft_bench(args):
 
         def run(n):
             s = time.perf_counter()
-            oracle.markov_draft(inp.anchor[:n], base[:n].reshape(n * w.K, -1), w.logit_dtype, inp.W1,
-                                inp.W2t, inp.w_conf, inp.u[:n], w.K, w.V, hidden=inp.hidden[:n],
-                                sts_temp=inp.sts_temp, want_p=False)
+            if rnn:
+                oracle.rnn_draft(inp.anchor[:n], base[:n].reshape(n * w.K, -1), w.logit_dtype, inp.W1,
+                                 inp.W2t, inp.Wrnn, inp.w_conf, inp.u[:n], w.K, w.V,
+                                 hidden=inp.hidden[:n], sts_temp=inp.sts_temp, want_p=False)
+            else:
+                oracle.markov_draft(inp.anchor[:n], base[:n].reshape(n * w.K, -1), w.logit_dtype,
+                                    inp.W1, inp.W2t, inp.w_conf, inp.u[:n], w.K, w.V,
+                                    hidden=inp.hidden[:n], sts_temp=inp.sts_temp, want_p=False)
             return time.perf_counter() - s
 
         th = oracle.threads()

@@ -240,6 +240,39 @@ dspark_status dspark_markov_draft(const int32_t* anchor, const void* base_logits
                                   int32_t* draft_tok, float* draft_p, float* conf, void* ws,
                                   size_t ws_bytes, dspark_stream stream);
 
+/* ------------------------------------------------------------------------
+ * Drafter, RNN head: the same draft block with the RNN head of the section on
+ * semi-autoregressive generation (eq. rnn) in place of the Markov head.  A
+ * recurrent state carries the whole prefix of the block.  For every request
+ * r, with x_0 = anchor[r], s_0 = 0 and k = 1 .. K, left to right:
+ *     e_k = W1[x_{k-1}],   z_k = [s_{k-1}; e_k; h_k]        (2 rank + d values)
+ *     a_k = Wrnn z_k = [a_g; a_c; a_o]                      (3 rank values)
+ *     s_k = sigmoid(a_g) * s_{k-1} + (1 - sigmoid(a_g)) * tanh(a_c)
+ *     p_k = softmax(inv_temperature * (U_k + W2^T tanh(a_o)))
+ *     x_k, c_k as for dspark_markov_draft (c_k reads [h_k; e_k]).
+ *
+ *   Wrnn  [3 rank, 2 rank + d] bf16 row-major, 16-byte aligned: the single
+ *         projection of the equation, rows 0 .. rank-1 the gate, then the
+ *         candidate, then the output component; columns in the order of z_k.
+ *         The equation has no bias terms.
+ *   Every other argument, output, limit and the invalid-anchor rule are those
+ *   of dspark_markov_draft, and in addition d % 8 == 0 and hidden 16-byte
+ *   aligned when d > 0 (the backbone part of the projection, Wrnn[:, 2 rank:]
+ *   h_k, runs on the matrix cores once for every position).  The state and
+ *   the head's output are fp32; the output enters the bf16 vocabulary product
+ *   as three bf16 terms whose sum is its fp32 value.
+ *   ws    dspark_rnn_draft_workspace_size(R, K, V, rank) bytes, 256-aligned.
+ * ---------------------------------------------------------------------- */
+size_t dspark_rnn_draft_workspace_size(int R, int K, int V, int rank);
+
+dspark_status dspark_rnn_draft(const int32_t* anchor, const void* base_logits,
+                               dspark_dtype base_dt, int64_t ld, const uint16_t* W1,
+                               const uint16_t* W2t, const uint16_t* Wrnn, int rank,
+                               const uint16_t* hidden, const float* w_conf, int d,
+                               const float* sts_temp, const float* u, float inv_temperature,
+                               int R, int K, int V, int32_t* draft_tok, float* draft_p,
+                               float* conf, void* ws, size_t ws_bytes, dspark_stream stream);
+
 #ifdef __cplusplus
 }
 #endif

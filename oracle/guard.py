@@ -142,14 +142,15 @@ class DraftCase:
 
 
 def draft_case(w: synth.Workload, seed: int, rank: int, d: int, reqs: Optional[List[int]] = None,
-               inv_temperature: float = 1.0, want_p: bool = True, max_tries: int = 64) -> DraftCase:
+               inv_temperature: float = 1.0, want_p: bool = True, max_tries: int = 64,
+               head: str = "markov") -> DraftCase:
     """Inputs of the draft block and the oracle's outputs for ``reqs`` (all by
     default), with each request's uniforms redrawn draw by draw, left to right,
     until every draw is at least ACCEPT_GUARD (units of the total mass) from
     its bucket's edges.  A redraw of draw k takes element k of the request's
     next uniform sub-stream and changes every later draw, which is checked
     again."""
-    inp = synth.markov_inputs(w, seed, rank=rank, d=d)
+    inp = synth.markov_inputs(w, seed, rank=rank, d=d, rnn=head == "rnn")
     R, K, V = w.R, w.K, w.V
     reqs = list(range(R)) if reqs is None else list(reqs)
     tries = {r: np.zeros(K, dtype=np.int64) for r in reqs}
@@ -159,6 +160,11 @@ def draft_case(w: synth.Workload, seed: int, rank: int, d: int, reqs: Optional[L
     def run(want):
         base = inp.base.reshape(R, K, -1)[sub].reshape(len(sub) * K, -1)
         hid = None if d == 0 else inp.hidden[sub]
+        if head == "rnn":
+            return oracle.rnn_draft(inp.anchor[sub], base, w.logit_dtype, inp.W1, inp.W2t,
+                                    inp.Wrnn, inp.w_conf, inp.u[sub], K, V, hidden=hid,
+                                    sts_temp=inp.sts_temp, inv_temperature=inv_temperature,
+                                    want_p=want)
         return oracle.markov_draft(inp.anchor[sub], base, w.logit_dtype, inp.W1, inp.W2t,
                                    inp.w_conf, inp.u[sub], K, V, hidden=hid,
                                    sts_temp=inp.sts_temp, inv_temperature=inv_temperature,

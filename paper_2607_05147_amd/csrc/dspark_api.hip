@@ -311,7 +311,77 @@ dspark_status dspark_markov_draft(const int32_t* anchor, const void* base_logits
     a.draft_tok = draft_tok;
     a.draft_p = draft_p;
     a.conf = conf;
+    a.Wrnn = nullptr;
     return hip_status(dspark::launch_markov(a, ws, (hipStream_t)stream), "dspark_markov_draft");
+}
+
+size_t dspark_rnn_draft_workspace_size(int R, int K, int V, int rank) {
+    if (R < 1 || R > kMaxR || K < 1 || K > kMaxK || V < 1 || V > dspark::markov_max_vocab() ||
+        !dspark::markov_rank_supported(rank))
+        return 0;
+    return dspark::rnn_workspace(R, K, V, rank);
+}
+
+dspark_status dspark_rnn_draft(const int32_t* anchor, const void* base_logits,
+                               dspark_dtype base_dt, int64_t ld, const uint16_t* W1,
+                               const uint16_t* W2t, const uint16_t* Wrnn, int rank,
+                               const uint16_t* hidden, const float* w_conf, int d,
+                               const float* sts_temp, const float* u, float inv_temperature,
+                               int R, int K, int V, int32_t* draft_tok, float* draft_p,
+                               float* conf, void* ws, size_t ws_bytes, dspark_stream stream) {
+    if (base_dt != DSPARK_F32 && base_dt != DSPARK_BF16)
+        return fail(DSPARK_EDTYPE, "base logit dtype %d", (int)base_dt);
+    if (R < 1 || R > kMaxR) return fail(DSPARK_EINVAL, "R=%d outside [1, %d]", R, kMaxR);
+    if (K < 1 || K > kMaxK) return fail(DSPARK_EINVAL, "K=%d outside [1, %d]", K, kMaxK);
+    if (V < 1 || V > kMaxV) return fail(DSPARK_EINVAL, "V=%d outside [1, %d]", V, kMaxV);
+    if (ld < V) return fail(DSPARK_ESHAPE, "ld=%lld smaller than V=%d", (long long)ld, V);
+    if (V > dspark::markov_max_vocab())
+        return fail(DSPARK_EUNSUPPORTED, "V=%d above %d", V, dspark::markov_max_vocab());
+    if (!dspark::markov_rank_supported(rank))
+        return fail(DSPARK_EUNSUPPORTED, "rank=%d (32, 64, 128 or 256)", rank);
+    if (d < 0 || d > (1 << 16)) return fail(DSPARK_EINVAL, "d=%d outside [0, 65536]", d);
+    if (d % 8) return fail(DSPARK_EUNSUPPORTED, "d=%d (the RNN head needs a multiple of 8)", d);
+    if ((int64_t)R * K > ((int64_t)1 << 24))
+        return fail(DSPARK_EUNSUPPORTED, "R*K=%lld too large", (long long)R * K);
+    if (!(inv_temperature > 0.0f) || !isfinite(inv_temperature))
+        return fail(DSPARK_EINVAL, "inv_temperature must be positive and finite");
+    if (!anchor || !base_logits || !W1 || !W2t || !Wrnn || !w_conf || !u || !draft_tok ||
+        !draft_p || !conf || (d > 0 && !hidden))
+        return fail(DSPARK_EINVAL, "null argument");
+    const size_t esz = base_dt == DSPARK_BF16 ? 2 : 4;
+    if (!aligned(W1, 16) || !aligned(W2t, 16) || !aligned(Wrnn, 16) ||
+        (d > 0 && !aligned(hidden, 16)))
+        return fail(DSPARK_EUNSUPPORTED, "W1, W2t, Wrnn and hidden must be 16-byte aligned");
+    if (!aligned(anchor, 4) || !aligned(base_logits, esz) || !aligned(w_conf, 4) ||
+        !aligned(sts_temp, 4) || !aligned(u, 4) || !aligned(draft_tok, 4) ||
+        !aligned(draft_p, 4) || !aligned(conf, 4))
+        return fail(DSPARK_EINVAL, "misaligned pointer");
+    const size_t need = dspark::rnn_workspace(R, K, V, rank);
+    if (ws_bytes < need || !ws || !aligned(ws, 256))
+        return fail(DSPARK_EWORKSPACE, "workspace of %zu bytes (256-aligned) needed, got %zu",
+                    need, ws_bytes);
+    dspark::MarkovArgs a;
+    a.anchor = anchor;
+    a.base = base_logits;
+    a.base_bf16 = base_dt == DSPARK_BF16;
+    a.ld = ld;
+    a.W1 = W1;
+    a.W2t = W2t;
+    a.rank = rank;
+    a.hidden = d > 0 ? hidden : nullptr;
+    a.w_conf = w_conf;
+    a.d = d;
+    a.sts_temp = sts_temp;
+    a.u = u;
+    a.inv_temp = inv_temperature;
+    a.R = R;
+    a.K = K;
+    a.V = V;
+    a.draft_tok = draft_tok;
+    a.draft_p = draft_p;
+    a.conf = conf;
+    a.Wrnn = Wrnn;
+    return hip_status(dspark::launch_rnn(a, ws, (hipStream_t)stream), "dspark_rnn_draft");
 }
 
 }  // extern "C"

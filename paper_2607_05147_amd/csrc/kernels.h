@@ -81,8 +81,11 @@ struct MarkovArgs {
     int32_t* draft_tok;  // [R, K]
     float* draft_p;      // [R, K, V]
     float* conf;         // [R, K]
+    const uint16_t* Wrnn;  // RNN head only: [3 rank, 2 rank + d] bf16 (gate, candidate, output)
 };
 size_t markov_workspace(int R, int K, int V, int rank);
+size_t rnn_workspace(int R, int K, int V, int rank);
+hipError_t launch_rnn(const MarkovArgs& a, void* ws, hipStream_t s);
 bool markov_rank_supported(int rank);
 int markov_max_vocab();  // per-tile statistics of one request fit one workgroup
 hipError_t launch_markov(const MarkovArgs& a, void* ws, hipStream_t s);

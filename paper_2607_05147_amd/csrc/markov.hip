@@ -103,10 +103,6 @@ __device__ __forceinline__ double block_scan(double v, double* s, double* total)
     return before + incl;
 }
 
-__device__ __forceinline__ float load_base(const MarkovArgs& a, int64_t i) {
-    return a.base_bf16 ? bf16_to_f32(((const uint16_t*)a.base)[i]) : ((const float*)a.base)[i];
-}
-
 // token of position k - 1 (the anchor for k = 1); -1 when it is not a valid token
 __device__ __forceinline__ int prev_token(const MarkovArgs& a, int r, int k) {
     const int x = k == 1 ? a.anchor[r] : a.draft_tok[(int64_t)r * a.K + (k - 2)];
@@ -205,14 +201,24 @@ __global__ __launch_bounds__(kThreads) void md_first(MarkovArgs a, const float* 
 //   embedding E_next[r] = W1[x_k] and the confidence c_{k+1}.
 // VEC: 4 consecutive entries per lane are loaded / stored as one vector
 // (V, ld multiples of 4, aligned rows).
-template <int KS, int PASS, bool VEC>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 4))) void md_tile(MarkovArgs a, const uint16_t* E,
+// NT: bf16 terms of the B operand per request (1: the embedding itself; 3:
+// an fp32 vector split as hi + mid + lo, each term a bf16 rounding of what the
+// previous ones leave, so the products reproduce the fp32 vector's to fp32
+// accuracy); E row r holds the NT terms one after the other.
+// BF16: the base logits' type.  Their loads are branch-free (clamped
+// indices; entries past V are masked with the rest of the tile), so they issue
+// back to back and stay in flight during the products.  Occupancy: three
+// waves per SIMD for the one-term statistics pass; two for the pass that
+// draws and writes p, and for three terms (three times the staged embedding
+// loads), which leaves their loads room without spilling (measured faster).
+template <int KS, int NT, int PASS, bool VEC, bool BF16>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 1 && PASS == 0 ? 3 : 2, 4))) void md_tile(MarkovArgs a, const uint16_t* E,
                                                     float2* stats, const RowInfo* info,
                                                     uint16_t* E_next, const float* sh,
                                                     int ntiles, int k) {
     constexpr int kNch = 4 * KS;  // 16-byte chunks per embedding row
     constexpr int kRank = 32 * KS;
-    __shared__ __align__(16) uint16_t se[kChunkR * kRank];
+    __shared__ __align__(16) uint16_t se[NT * kChunkR * kRank];
     __shared__ float2 sst[kWaves][kChunkR];
     __shared__ float smass[kTileV];
     const int tid = threadIdx.x;
@@ -240,14 +246,17 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 4))
         // the chunk's embeddings first, then its base logits: the LDS stores
         // below wait only for the embeddings (loads complete in order), and the
         // base logits stay in flight during the products
-        constexpr int kCopy = ceil_div(kChunkR * kNch, kThreads);
+        // (measured: this guarded form schedules better than clamped, unguarded
+        // loads, by 1.4x on the three-term product)
+        constexpr int kCopy = ceil_div(NT * kChunkR * kNch, kThreads);
         uint4 ev[kCopy];
 #pragma unroll
         for (int i = 0; i < kCopy; ++i) {
-            const int idx = tid + i * kThreads;
-            const int t = idx / kNch, c = idx - t * kNch;
-            ev[i] = idx < kChunkR * kNch && c0 + t < a.R ? *(const uint4*)(E + (int64_t)(c0 + t) * kRank + 8 * c)
-                                                          : uint4{0u, 0u, 0u, 0u};
+            const int idx = tid + i * kThreads;  // (request t, term, chunk)
+            const int t = idx / (NT * kNch);
+            ev[i] = idx < NT * kChunkR * kNch && c0 + t < a.R
+                        ? *(const uint4*)(E + (int64_t)(c0 + t) * (NT * kRank) + 8 * (idx % (NT * kNch)))
+                        : uint4{0u, 0u, 0u, 0u};
         }
         float ub[kRT][kVT][4];
 #pragma unroll
@@ -257,30 +266,38 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 4))
 #pragma unroll
             for (int vt = 0; vt < kVT; ++vt) {
                 const int vb = v0 + 16 * vt + 4 * lq;
-                if (VEC && vb + 3 < a.V) {
-                    if (a.base_bf16) {
-                        const uint2 w = *(const uint2*)((const uint16_t*)a.base + row * a.ld + vb);
+                if (VEC) {
+                    // V % 4 == 0: a group below V lies wholly inside the row
+                    const int vc = min(vb, a.V - 4);
+                    if (BF16) {
+                        const uint2 w = *(const uint2*)((const uint16_t*)a.base + row * a.ld + vc);
                         ub[rt][vt][0] = __uint_as_float(w.x << 16);
                         ub[rt][vt][1] = __uint_as_float(w.x & 0xffff0000u);
                         ub[rt][vt][2] = __uint_as_float(w.y << 16);
                         ub[rt][vt][3] = __uint_as_float(w.y & 0xffff0000u);
                     } else {
-                        const float4 w = *(const float4*)((const float*)a.base + row * a.ld + vb);
+                        const float4 w = *(const float4*)((const float*)a.base + row * a.ld + vc);
                         ub[rt][vt][0] = w.x, ub[rt][vt][1] = w.y, ub[rt][vt][2] = w.z, ub[rt][vt][3] = w.w;
                     }
                 } else {
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        ub[rt][vt][e] = vb + e < a.V ? load_base(a, row * a.ld + vb + e) : 0.0f;
+                    for (int e = 0; e < 4; ++e) {
+                        const int64_t i = row * a.ld + min(vb + e, a.V - 1);
+                        ub[rt][vt][e] = BF16 ? bf16_to_f32(((const uint16_t*)a.base)[i]) : ((const float*)a.base)[i];
+                    }
                 }
             }
         }
         lds_barrier();  // the previous chunk's LDS reads are done (global loads stay in flight)
+        // (no guard when the copy divides evenly: a branch here would make the
+        // stores wait for the base logits as well)
+        constexpr bool kExact = NT * kChunkR * kNch % kThreads == 0;
 #pragma unroll
         for (int i = 0; i < kCopy; ++i) {
             const int idx = tid + i * kThreads;
-            const int t = idx / kNch, c = idx - t * kNch;
-            if (idx < kChunkR * kNch) *(uint4*)(se + (t * kNch + eslot(t, c, kNch)) * 8) = ev[i];
+            const int t = idx / (NT * kNch), nt = (idx / kNch) % NT, c = idx % kNch;
+            if (kExact || idx < NT * kChunkR * kNch)
+                *(uint4*)(se + ((nt * kChunkR + t) * kNch + eslot(t, c, kNch)) * 8) = ev[i];
         }
         lds_barrier();
 
@@ -294,12 +311,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 4))
         for (int rt = 0; rt < kRT; ++rt) {
             const int t = 16 * rt + lr;
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const bf16x8 b = *(const bf16x8*)(se + (t * kNch + eslot(t, 4 * ks + lq, kNch)) * 8);
+            for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-                for (int vt = 0; vt < kVT; ++vt)
-                    acc[vt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[vt][ks], b, acc[vt][rt], 0, 0, 0);
-            }
+                for (int ks = 0; ks < KS; ++ks) {
+                    const bf16x8 b =
+                        *(const bf16x8*)(se + ((nt * kChunkR + t) * kNch + eslot(t, 4 * ks + lq, kNch)) * 8);
+#pragma unroll
+                    for (int vt = 0; vt < kVT; ++vt)
+                        acc[vt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[vt][ks], b, acc[vt][rt], 0, 0, 0);
+                }
         }
 
 #pragma unroll
@@ -501,6 +521,196 @@ __global__ __launch_bounds__(kThreads) void md_stats(MarkovArgs a, const float2*
     }
 }
 
+// One launch of md_tile over every vocabulary tile, instantiated for the
+// base logits' type and vector access.
+template <int KS, int NT, int PASS>
+void tile_pass(const MarkovArgs& a, const uint16_t* E, float2* stats, const RowInfo* info,
+               uint16_t* En, const float* shp, int ntiles, int k, bool vec, hipStream_t s) {
+    const dim3 g(ntiles), b(kThreads);
+    if (vec && a.base_bf16) hipLaunchKernelGGL((md_tile<KS, NT, PASS, true, true>), g, b, 0, s, a, E, stats, info, En, shp, ntiles, k);
+    else if (vec) hipLaunchKernelGGL((md_tile<KS, NT, PASS, true, false>), g, b, 0, s, a, E, stats, info, En, shp, ntiles, k);
+    else if (a.base_bf16) hipLaunchKernelGGL((md_tile<KS, NT, PASS, false, true>), g, b, 0, s, a, E, stats, info, En, shp, ntiles, k);
+    else hipLaunchKernelGGL((md_tile<KS, NT, PASS, false, false>), g, b, 0, s, a, E, stats, info, En, shp, ntiles, k);
+}
+
+// ------------------------------------------------------------ RNN head
+
+// The backbone part of the RNN head's projection (eq. rnn), once for every
+// (request, position) since it does not depend on the drawn tokens:
+// Hp[row, i] = sum_{j < d} Wrnn[i, 2 rank + j] h[row, j], row = r K + k - 1,
+// i < 3 rank.  v_mfma_f32_16x16x32_bf16 with both operands read straight
+// from memory (a lane's 8 consecutive inputs are one 16-byte load); a
+// workgroup computes 64 rows x 64 outputs, wave w rows 16 w .. 16 w + 15, and
+// keeps kHpDepth steps of 32 inputs in flight.  d % 8 == 0, so a lane's 8
+// inputs are either all inside the row or all past its end.
+constexpr int kHpRows = 64, kHpCols = 64, kHpDepth = 4, kHpNt = kHpCols / 16;
+__global__ __launch_bounds__(kThreads) void rnn_hproj(MarkovArgs a, float* Hp) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lr = lane & 15, lq = lane >> 4;
+    const int nrows = a.R * a.K, ncols = 3 * a.rank, nz = 2 * a.rank + a.d;
+    const int m0 = blockIdx.x * kHpRows + 16 * wave;
+    const int n0 = blockIdx.y * kHpCols;
+    const uint16_t* ap = a.hidden + (int64_t)min(m0 + lr, nrows - 1) * a.d + 8 * lq;
+    const uint16_t* bp[kHpNt];
+#pragma unroll
+    for (int nt = 0; nt < kHpNt; ++nt)
+        bp[nt] = a.Wrnn + (int64_t)min(n0 + 16 * nt + lr, ncols - 1) * nz + 2 * a.rank + 8 * lq;
+    const int nsteps = ceil_div(a.d, 32);
+    bf16x8 af[kHpDepth], bfr[kHpDepth][kHpNt];
+    auto load = [&](int st, int slot) {
+        const bool in = st < nsteps && 32 * st + 8 * lq < a.d;
+        const int off = in ? 32 * st : 0;  // past the end: a valid address, zeroed below
+        af[slot] = *(const bf16x8*)(ap + off);
+#pragma unroll
+        for (int nt = 0; nt < kHpNt; ++nt) bfr[slot][nt] = *(const bf16x8*)(bp[nt] + off);
+        if (!in) af[slot] = bf16x8{};
+    };
+    f32x4 acc[kHpNt];
+#pragma unroll
+    for (int nt = 0; nt < kHpNt; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int u = 0; u < kHpDepth; ++u) load(u, u);
+    for (int st0 = 0; st0 < nsteps; st0 += kHpDepth) {
+#pragma unroll
+        for (int u = 0; u < kHpDepth; ++u) {
+#pragma unroll
+            for (int nt = 0; nt < kHpNt; ++nt)
+                acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[u], bfr[u][nt], acc[nt], 0, 0, 0);
+            load(st0 + kHpDepth + u, u);
+        }
+    }
+    // lane holds rows m0 + 4 lq + e, output n0 + 16 nt + lr
+#pragma unroll
+    for (int nt = 0; nt < kHpNt; ++nt) {
+        const int col = n0 + 16 * nt + lr;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int row = m0 + 4 * lq + e;
+            if (row < nrows && col < ncols) Hp[(int64_t)row * ncols + col] = acc[nt][e];
+        }
+    }
+}
+
+// Position k of the RNN head: a = Hp[r, k] + Wrnn[:, :2 rank] [s_{k-1}; e_k]
+// (e_k = W1[x_{k-1}], gathered by the previous position's draw), the gated
+// state update s_k = g s_{k-1} + (1 - g) tanh(a_c) with g = sigmoid(a_g), and
+// the head's output o_k = tanh(a_o), written for md_tile as three bf16 terms
+// (hi, mid, lo: each the rounding of what the previous ones leave, so their
+// sum is o_k to fp32 accuracy).  A workgroup owns 16 state dims j and 16
+// requests, with its weight rows (gate, candidate and output rows of those
+// dims) and the requests' [s_{k-1}; e_k] in LDS; thread (j, request) computes
+// the three rows' dot products over 2 rank inputs in fp32.  The state is
+// double-buffered (s_prev is read by every workgroup of a request block while
+// others write s_next); s_0 = 0.
+constexpr int kStJ = 16, kStR = 16;
+static_assert(kStJ * kStR == kThreads, "one thread per (dim, request)");
+__host__ __device__ constexpr int st_wpitch(int rank) { return 2 * rank + 8; }  // bf16 elements
+__host__ __device__ constexpr int st_zpitch(int rank) { return 2 * rank + 4; }  // fp32 elements
+static size_t rnn_state_lds(int rank) {
+    return (size_t)3 * kStJ * st_wpitch(rank) * 2 + (size_t)kStR * st_zpitch(rank) * 4;
+}
+
+__global__ __launch_bounds__(kThreads) void rnn_state(MarkovArgs a, const float* Hp,
+                                                      const float* s_prev, float* s_next,
+                                                      const uint16_t* Ee, uint16_t* E3, int k) {
+    extern __shared__ __align__(16) unsigned char st_smem[];
+    const int rank = a.rank, n2 = 2 * rank;
+    const int wp = st_wpitch(rank), zp = st_zpitch(rank);
+    uint16_t* Wl = reinterpret_cast<uint16_t*>(st_smem);                    // [3 * kStJ][wp]
+    float* Zl = reinterpret_cast<float*>(st_smem + (size_t)3 * kStJ * wp * 2);  // [kStR][zp]
+    const int tid = threadIdx.x;
+    const int j0 = blockIdx.x * kStJ, r0 = blockIdx.y * kStR;
+    const int nz = n2 + a.d;
+    // weight rows: part p, dim j0 + jj -> LDS row p * kStJ + jj, the 2 rank state and embedding columns
+    const int wch = n2 / 8;  // 16-byte chunks per row
+    for (int i = tid; i < 3 * kStJ * wch; i += kThreads) {
+        const int lrow = i / wch, c = i - lrow * wch;
+        const int p = lrow / kStJ, jj = lrow - p * kStJ;
+        *(uint4*)(Wl + lrow * wp + 8 * c) =
+            *(const uint4*)(a.Wrnn + (int64_t)(p * rank + j0 + jj) * nz + 8 * c);
+    }
+    // [s_{k-1}; e_k] of the block's requests (zero past R; s_0 = 0)
+    for (int i = tid; i < kStR * n2; i += kThreads) {
+        const int rr = i / n2, c = i - rr * n2, r = r0 + rr;
+        float v = 0.0f;
+        if (r < a.R) {
+            if (c < rank) v = k > 1 ? s_prev[(int64_t)r * rank + c] : 0.0f;
+            else v = bf16_to_f32(Ee[(int64_t)r * rank + (c - rank)]);
+        }
+        Zl[rr * zp + c] = v;
+    }
+    __syncthreads();
+    const int jj = tid / kStR, rr = tid % kStR;
+    const int j = j0 + jj, r = r0 + rr;
+    const uint16_t* wg = Wl + (0 * kStJ + jj) * wp;
+    const uint16_t* wc = Wl + (1 * kStJ + jj) * wp;
+    const uint16_t* wo = Wl + (2 * kStJ + jj) * wp;
+    const float* z = Zl + rr * zp;
+    float ag = 0.0f, ac = 0.0f, ao = 0.0f;
+    for (int c = 0; c < n2; c += 8) {
+        const float4 z0 = *(const float4*)(z + c), z1 = *(const float4*)(z + c + 4);
+        const float zz[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
+        const uint4 g8 = *(const uint4*)(wg + c), c8 = *(const uint4*)(wc + c), o8 = *(const uint4*)(wo + c);
+        const uint32_t gw[4] = {g8.x, g8.y, g8.z, g8.w}, cw[4] = {c8.x, c8.y, c8.z, c8.w},
+                       ow[4] = {o8.x, o8.y, o8.z, o8.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            ag = __builtin_fmaf(__uint_as_float(gw[q] << 16), zz[2 * q], ag);
+            ag = __builtin_fmaf(__uint_as_float(gw[q] & 0xffff0000u), zz[2 * q + 1], ag);
+            ac = __builtin_fmaf(__uint_as_float(cw[q] << 16), zz[2 * q], ac);
+            ac = __builtin_fmaf(__uint_as_float(cw[q] & 0xffff0000u), zz[2 * q + 1], ac);
+            ao = __builtin_fmaf(__uint_as_float(ow[q] << 16), zz[2 * q], ao);
+            ao = __builtin_fmaf(__uint_as_float(ow[q] & 0xffff0000u), zz[2 * q + 1], ao);
+        }
+    }
+    if (r >= a.R) return;
+    if (Hp) {
+        const float* hp = Hp + ((int64_t)r * a.K + (k - 1)) * (3 * rank);
+        ag += hp[j];
+        ac += hp[rank + j];
+        ao += hp[2 * rank + j];
+    }
+    const float g = 1.0f / (1.0f + expf(-ag));
+    const float sp = z[j];  // s_{k-1}[j]
+    s_next[(int64_t)r * rank + j] = g * sp + (1.0f - g) * tanhf(ac);
+    const float o = tanhf(ao);
+    const uint16_t hi = f32_to_bf16(o);
+    const float r1 = o - bf16_to_f32(hi);
+    const uint16_t mid = f32_to_bf16(r1);
+    const uint16_t lo = f32_to_bf16(r1 - bf16_to_f32(mid));
+    uint16_t* e3 = E3 + (int64_t)r * 3 * rank;
+    e3[j] = hi;
+    e3[rank + j] = mid;
+    e3[2 * rank + j] = lo;
+}
+
+template <int KS>
+hipError_t launch_rnn_ks(const MarkovArgs& a, uint16_t* Ee, uint16_t* E3, float* S0, float* S1,
+                         float* Hp, float2* stats, RowInfo* info, float* sh, int ntiles, bool vec,
+                         hipStream_t s) {
+    const int64_t rows = (int64_t)a.R * a.K;
+    if (a.d > 0) {
+        hipLaunchKernelGGL(md_hidden, dim3((unsigned)ceil_div((int)rows, kWaves)), dim3(kThreads), 0, s, a, sh);
+        hipLaunchKernelGGL(rnn_hproj, dim3((unsigned)ceil_div((int)rows, kHpRows), ceil_div(3 * a.rank, kHpCols)),
+                           dim3(kThreads), 0, s, a, Hp);
+    }
+    const float* shp = a.d > 0 ? sh : nullptr;
+    const float* hpp = a.d > 0 ? Hp : nullptr;
+    hipLaunchKernelGGL(md_first, dim3(ceil_div(a.R, kWaves)), dim3(kThreads), 0, s, a, shp, Ee);
+    const size_t lds = rnn_state_lds(a.rank);
+    for (int k = 1; k <= a.K; ++k) {
+        const float* sp = (k & 1) ? S1 : S0;  // s_{k-1} (unread at k = 1)
+        float* sn = (k & 1) ? S0 : S1;
+        hipLaunchKernelGGL(rnn_state, dim3(a.rank / kStJ, ceil_div(a.R, kStR)), dim3(kThreads), lds, s, a, hpp,
+                           sp, sn, (const uint16_t*)Ee, E3, k);
+        tile_pass<KS, 3, 0>(a, E3, stats, info, Ee, shp, ntiles, k, vec, s);
+        hipLaunchKernelGGL(md_stats, dim3(a.R), dim3(kThreads), 0, s, a, stats, info, ntiles, k);
+        // the draw gathers W1[x_k] into Ee: the embedding input of position k + 1
+        tile_pass<KS, 3, 1>(a, E3, stats, info, Ee, shp, ntiles, k, vec, s);
+    }
+    return hipGetLastError();
+}
+
 template <int KS>
 hipError_t launch_ks(const MarkovArgs& a, uint16_t* E0, uint16_t* E1, float2* stats, RowInfo* info,
                      float* sh, int ntiles, bool vec, hipStream_t s) {
@@ -511,11 +721,9 @@ hipError_t launch_ks(const MarkovArgs& a, uint16_t* E0, uint16_t* E1, float2* st
     for (int k = 1; k <= a.K; ++k) {
         uint16_t* Ek = (k & 1) ? E0 : E1;
         uint16_t* En = (k & 1) ? E1 : E0;
-        if (vec) hipLaunchKernelGGL((md_tile<KS, 0, true>), dim3(ntiles), dim3(kThreads), 0, s, a, Ek, stats, info, En, shp, ntiles, k);
-        else hipLaunchKernelGGL((md_tile<KS, 0, false>), dim3(ntiles), dim3(kThreads), 0, s, a, Ek, stats, info, En, shp, ntiles, k);
+        tile_pass<KS, 1, 0>(a, Ek, stats, info, En, shp, ntiles, k, vec, s);
         hipLaunchKernelGGL(md_stats, dim3(a.R), dim3(kThreads), 0, s, a, stats, info, ntiles, k);
-        if (vec) hipLaunchKernelGGL((md_tile<KS, 1, true>), dim3(ntiles), dim3(kThreads), 0, s, a, Ek, stats, info, En, shp, ntiles, k);
-        else hipLaunchKernelGGL((md_tile<KS, 1, false>), dim3(ntiles), dim3(kThreads), 0, s, a, Ek, stats, info, En, shp, ntiles, k);
+        tile_pass<KS, 1, 1>(a, Ek, stats, info, En, shp, ntiles, k, vec, s);
     }
     return hipGetLastError();
 }
@@ -541,6 +749,58 @@ WsLayout ws_layout(int R, int K, int V, int rank) {
 }  // namespace
 
 size_t markov_workspace(int R, int K, int V, int rank) { return ws_layout(R, K, V, rank).total; }
+
+namespace {
+// RNN head: the embedding input Ee, the three-term output E3, two state
+// buffers, the backbone part of the projection, then what the Markov head uses
+struct RnnLayout {
+    size_t ee, e3, st, hp, stats, info, sh, total;
+};
+RnnLayout rnn_layout(int R, int K, int V, int rank) {
+    const int ntiles = mkd::ceil_div(V, mkd::kTileV);
+    RnnLayout l;
+    l.ee = align256((size_t)R * rank * 2);
+    l.e3 = align256((size_t)R * 3 * rank * 2);
+    l.st = align256((size_t)R * rank * 4);
+    l.hp = align256((size_t)R * K * 3 * rank * 4);
+    l.stats = align256((size_t)R * ntiles * sizeof(float2));
+    l.info = align256((size_t)R * sizeof(mkd::RowInfo));
+    l.sh = align256((size_t)R * K * sizeof(float));
+    l.total = l.ee + l.e3 + 2 * l.st + l.hp + l.stats + l.info + l.sh;
+    return l;
+}
+}  // namespace
+
+size_t rnn_workspace(int R, int K, int V, int rank) { return rnn_layout(R, K, V, rank).total; }
+
+hipError_t launch_rnn(const MarkovArgs& a, void* ws, hipStream_t s) {
+    const int ntiles = mkd::ceil_div(a.V, mkd::kTileV);
+    const RnnLayout l = rnn_layout(a.R, a.K, a.V, a.rank);
+    char* p = (char*)ws;
+    uint16_t* Ee = (uint16_t*)p;                 p += l.ee;
+    uint16_t* E3 = (uint16_t*)p;                 p += l.e3;
+    float* S0 = (float*)p;                       p += l.st;
+    float* S1 = (float*)p;                       p += l.st;
+    float* Hp = (float*)p;                       p += l.hp;
+    float2* stats = (float2*)p;                  p += l.stats;
+    mkd::RowInfo* info = (mkd::RowInfo*)p;       p += l.info;
+    float* sh = (float*)p;
+    const size_t lds = mkd::rnn_state_lds(a.rank);
+    if (lds > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute((const void*)mkd::rnn_state,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+    }
+    const size_t eb = a.base_bf16 ? 2 : 4;
+    const bool vec = a.V % 4 == 0 && a.ld % 4 == 0 && ((uintptr_t)a.base % (4 * eb)) == 0 &&
+                     ((uintptr_t)a.draft_p % 16) == 0;
+    switch (a.rank) {
+        case 32: return mkd::launch_rnn_ks<1>(a, Ee, E3, S0, S1, Hp, stats, info, sh, ntiles, vec, s);
+        case 64: return mkd::launch_rnn_ks<2>(a, Ee, E3, S0, S1, Hp, stats, info, sh, ntiles, vec, s);
+        case 128: return mkd::launch_rnn_ks<4>(a, Ee, E3, S0, S1, Hp, stats, info, sh, ntiles, vec, s);
+        default: return mkd::launch_rnn_ks<8>(a, Ee, E3, S0, S1, Hp, stats, info, sh, ntiles, vec, s);
+    }
+}
 
 bool markov_rank_supported(int rank) { return rank == 32 || rank == 64 || rank == 128 || rank == 256; }
 

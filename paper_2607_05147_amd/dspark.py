@@ -65,6 +65,11 @@ def lib():
         L.dspark_markov_draft.restype = i32
         L.dspark_markov_draft.argtypes = [p, p, i32, i64, p, p, i32, p, p, i32, p, p, f32, i32, i32,
                                           i32, p, p, p, p, sz, p]
+        L.dspark_rnn_draft_workspace_size.restype = sz
+        L.dspark_rnn_draft_workspace_size.argtypes = [i32, i32, i32, i32]
+        L.dspark_rnn_draft.restype = i32
+        L.dspark_rnn_draft.argtypes = [p, p, i32, i64, p, p, p, i32, p, p, i32, p, p, f32, i32, i32,
+                                       i32, p, p, p, p, sz, p]
         _lib = L
     return _lib
 
@@ -301,4 +306,60 @@ def dspark_markov_draft(anchor: torch.Tensor, base_logits: torch.Tensor, W1: tor
                                    K, V, _p(draft_tok), _p(draft_p), _p(conf), _p(ws), ws_bytes,
                                    _stream(stream))
     _raise(st, "dspark_markov_draft")
+    return draft_tok, draft_p, conf
+
+
+def dspark_rnn_draft_workspace_size(R: int, K: int, V: int, rank: int) -> int:
+    return int(lib().dspark_rnn_draft_workspace_size(R, K, V, rank))
+
+
+def dspark_rnn_draft(anchor: torch.Tensor, base_logits: torch.Tensor, W1: torch.Tensor,
+                     W2t: torch.Tensor, Wrnn: torch.Tensor, w_conf: torch.Tensor, u: torch.Tensor,
+                     K: int, hidden: Optional[torch.Tensor] = None,
+                     sts_temp: Optional[torch.Tensor] = None, inv_temperature: float = 1.0,
+                     draft_tok: Optional[torch.Tensor] = None,
+                     draft_p: Optional[torch.Tensor] = None, conf: Optional[torch.Tensor] = None,
+                     ws: Optional[torch.Tensor] = None, stream=None):
+    """As dspark_markov_draft, plus Wrnn bf16 [3 rank, 2 rank + d] (gate,
+    candidate and output rows; columns [s; e; h]).
+    Returns (draft_tok int32 [R, K], draft_p fp32 [R, K, V], conf fp32 [R, K])."""
+    _dev(anchor, "anchor", torch.int32)
+    R = anchor.shape[0]
+    if base_logits.dtype not in _DT or base_logits.dim() != 2 or base_logits.device.type != "cuda":
+        raise DSparkError("base_logits must be a 2-D float32/bfloat16 ROCm tensor")
+    if base_logits.stride(1) != 1 or base_logits.shape[0] != R * K:
+        raise DSparkError("base_logits must be [R*K, V] with contiguous rows")
+    V = base_logits.shape[1]
+    ld = base_logits.stride(0)
+    _dev(W1, "W1", torch.bfloat16)
+    rank = W1.shape[1]
+    _dev(W2t, "W2t", torch.bfloat16, (V, rank))
+    if W1.shape != (V, rank):
+        raise DSparkError("W1 must be [V, rank]")
+    d = 0 if hidden is None else hidden.shape[-1]
+    _dev(hidden, "hidden", torch.bfloat16, (R, K, d), optional=True)
+    _dev(Wrnn, "Wrnn", torch.bfloat16, (3 * rank, 2 * rank + d))
+    _dev(w_conf, "w_conf", torch.float32, (d + rank,))
+    _dev(sts_temp, "sts_temp", torch.float32, (K,), optional=True)
+    _dev(u, "u", torch.float32, (R, K))
+    dev = anchor.device
+    if draft_tok is None:
+        draft_tok = torch.empty((R, K), dtype=torch.int32, device=dev)
+    if draft_p is None:
+        draft_p = torch.empty((R, K, V), dtype=torch.float32, device=dev)
+    if conf is None:
+        conf = torch.empty((R, K), dtype=torch.float32, device=dev)
+    _dev(draft_tok, "draft_tok", torch.int32, (R, K))
+    _dev(draft_p, "draft_p", torch.float32, (R, K, V))
+    _dev(conf, "conf", torch.float32, (R, K))
+    need = dspark_rnn_draft_workspace_size(R, K, V, rank)
+    if need == 0:
+        raise DSparkError(f"unsupported shape: R={R} V={V} rank={rank}")
+    ws, ws_bytes = _workspace(need, dev, ws)
+    st = lib().dspark_rnn_draft(_p(anchor), C.c_void_p(base_logits.data_ptr()),
+                                _DT[base_logits.dtype], ld, _p(W1), _p(W2t), _p(Wrnn), rank,
+                                _p(hidden), _p(w_conf), d, _p(sts_temp), _p(u),
+                                float(inv_temperature), R, K, V, _p(draft_tok), _p(draft_p),
+                                _p(conf), _p(ws), ws_bytes, _stream(stream))
+    _raise(st, "dspark_rnn_draft")
     return draft_tok, draft_p, conf

@@ -47,6 +47,7 @@ _STREAM = {
     "mk_hidden": 15,
     "mk_wconf": 16,
     "mk_uniform": 17,
+    "rnn_w": 18,
 }
 
 _KV_CHUNK_PAGES = 64  # pages per generator chunk of the KV pool
@@ -454,6 +455,7 @@ class MarkovInputs:
     w_conf: np.ndarray  # fp32 [d + rank]
     sts_temp: np.ndarray  # fp32 [K] per-position temperatures
     u: np.ndarray  # fp32 [R, K] uniforms of the draws
+    Wrnn: Optional[np.ndarray] = None  # uint16 bf16 bits [3 rank, 2 rank + d] (RNN head only)
 
 
 def markov_uniforms(seed: int, r: int, K: int, attempt: int = 0) -> np.ndarray:
@@ -461,8 +463,22 @@ def markov_uniforms(seed: int, r: int, K: int, attempt: int = 0) -> np.ndarray:
     return _rng(seed, "mk_uniform", r, attempt).random(K, dtype=np.float32)
 
 
+def rnn_weights(seed: int, rank: int, d: int) -> np.ndarray:
+    """Seeded RNN-head projection [3 rank, 2 rank + d] (bf16 bits): rows are
+    gate, candidate and output; columns [s; e; h].  Column blocks ~ N(0, 1/rank),
+    N(0, 1) and N(0, 1/d) for the state, the unit-norm embedding and the
+    N(0, 1) hidden state, so each pre-activation is about N(0, 2); the output
+    rows are scaled by 1/sqrt(rank), which keeps tanh near linear and the bias
+    W2^T o about N(0, 2), like the Markov head's."""
+    g = _rng(seed, "rnn_w").standard_normal((3 * rank, 2 * rank + d), dtype=np.float32)
+    col = np.concatenate([np.full(rank, 1.0 / math.sqrt(rank)), np.ones(rank),
+                          np.full(d, 1.0 / math.sqrt(max(d, 1)))]).astype(np.float32)
+    row = np.concatenate([np.ones(2 * rank), np.full(rank, 1.0 / math.sqrt(rank))]).astype(np.float32)
+    return f32_to_bf16_bits(g * col[None, :] * row[:, None])
+
+
 def markov_inputs(w: Workload, seed: int, rank: int = MARKOV_RANK, d: int = MARKOV_HIDDEN,
-                  u_attempts: Optional[np.ndarray] = None) -> MarkovInputs:
+                  u_attempts: Optional[np.ndarray] = None, rnn: bool = False) -> MarkovInputs:
     """Seeded synthetic inputs of the Markov-head draft block for workload w:
     base logits logit_scale * N(0, 1) in the logit dtype; W1 ~ N(0, 1/rank)
     (unit-norm embeddings) and W2 ~ N(0, 1), so the transition bias is about
@@ -488,4 +504,5 @@ def markov_inputs(w: Workload, seed: int, rank: int = MARKOV_RANK, d: int = MARK
         u_attempts = np.zeros(R, dtype=np.int64)
     u = np.stack([markov_uniforms(seed, r, K, int(u_attempts[r])) for r in range(R)])
     return MarkovInputs(anchor=anchor, base=base, W1=f32_to_bf16_bits(g1), W2t=f32_to_bf16_bits(g2),
-                        hidden=hidden, w_conf=w_conf, sts_temp=sts, u=np.ascontiguousarray(u))
+                        hidden=hidden, w_conf=w_conf, sts_temp=sts, u=np.ascontiguousarray(u),
+                        Wrnn=rnn_weights(seed, rank, d) if rnn else None)

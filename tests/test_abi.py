@@ -189,6 +189,45 @@ def test_markov_draft_workspace_size(L):
     assert L.dspark_markov_draft_workspace_size(128, 16, 129280, 96) == 0
 
 
+def _rnn(L, **kw):
+    a = dict(anchor=FAKE, base=FAKE, dt=1, ld=1024, W1=FAKE, W2t=FAKE, Wr=FAKE, rank=256,
+             hidden=FAKE, wc=FAKE, d=64, sts=None, u=FAKE, it=1.0, R=4, K=8, V=1024, tok=FAKE,
+             dp=FAKE, conf=FAKE, ws=FAKE, ws_bytes=0)
+    a.update(kw)
+    return L.dspark_rnn_draft(a["anchor"], a["base"], a["dt"], a["ld"], a["W1"], a["W2t"], a["Wr"],
+                              a["rank"], a["hidden"], a["wc"], a["d"], a["sts"], a["u"], a["it"],
+                              a["R"], a["K"], a["V"], a["tok"], a["dp"], a["conf"], a["ws"],
+                              a["ws_bytes"], None)
+
+
+def test_rnn_draft_validation(L):
+    assert _rnn(L, dt=7) == EDTYPE
+    assert _rnn(L, K=0) == EINVAL
+    assert _rnn(L, R=0) == EINVAL
+    assert _rnn(L, V=0) == EINVAL
+    assert _rnn(L, ld=1000) == ESHAPE
+    assert _rnn(L, rank=96) == EUNSUPPORTED
+    assert _rnn(L, d=-1) == EINVAL
+    assert _rnn(L, d=60) == EUNSUPPORTED  # the hidden projection reads 8 inputs at a time
+    assert _rnn(L, it=0.0) == EINVAL
+    assert _rnn(L, Wr=None) == EINVAL
+    assert _rnn(L, hidden=None) == EINVAL
+    assert _rnn(L, Wr=C.c_void_p((1 << 20) + 8)) == EUNSUPPORTED  # not 16-byte aligned
+    assert _rnn(L, hidden=C.c_void_p((1 << 20) + 8)) == EUNSUPPORTED
+    assert _rnn(L) == EWORKSPACE
+    need = L.dspark_rnn_draft_workspace_size(4, 8, 1024, 256)
+    assert _rnn(L, ws_bytes=need - 1) == EWORKSPACE
+    assert _rnn(L, hidden=None, d=0, ws=C.c_void_p((1 << 20) + 64), ws_bytes=need) == EWORKSPACE
+
+
+def test_rnn_draft_workspace_size(L):
+    n = L.dspark_rnn_draft_workspace_size(128, 16, 129280, 256)
+    # the Markov head's buffers plus the three-term output, two states and the
+    # hidden part of the projection for every position
+    assert n >= L.dspark_markov_draft_workspace_size(128, 16, 129280, 256) + 128 * 16 * 768 * 4
+    assert L.dspark_rnn_draft_workspace_size(128, 16, 129280, 96) == 0
+
+
 def test_binding_rejects_host_tensors():
     import torch
     with pytest.raises(dspark.DSparkError):

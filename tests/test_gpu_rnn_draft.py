@@ -1,0 +1,141 @@
+"""GPU parity of the RNN-head draft block against the fp64 oracle.
+
+Draft tokens are compared exactly, on uniforms guarded draw by draw (every
+draw at least 1e-4 of the total mass from its bucket's edges).
+
+Distributions: the head's pre-activations are fp32 sums of 2 rank + d
+products of bf16 weights with fp32 inputs (the hidden part on the matrix
+cores), so each carries a relative error of a few 2^-24 per term in the
+worst case and ~sqrt(n) 2^-24 typically; tanh and sigmoid add a few ulp, and
+the state recursion carries the error from position to position without
+amplifying it (|ds_k/ds_{k-1}| <= max g < 1 plus the candidate's bounded
+slope).  The output enters the vocabulary product as three bf16 terms whose
+sum is its fp32 value, so the bias W2^T o has the Markov head's error
+(rank 2^-24 sum_j |W2[j, v] o_j|) plus that of o, ~1e-5 relative at
+rank 256, d 4096.  Entries of p are compared at P_RTOL = 2e-4 relative, the
+Markov head's bound; confidences at C_ATOL = 2e-5 (their path is the Markov
+head's).
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import guard
+from paper_2607_05147_amd import dspark, synth
+
+from gpu_helpers import log, to_dev
+
+pytestmark = pytest.mark.gpu
+
+P_RTOL = 2e-4
+C_ATOL = 2e-5
+
+
+def _run_gpu(w, case, d, inv_temperature=1.0, anchor=None):
+    inp = case.inp
+    tok, p, conf = dspark.dspark_rnn_draft(
+        to_dev(inp.anchor if anchor is None else anchor), to_dev(inp.base), to_dev(inp.W1),
+        to_dev(inp.W2t), to_dev(inp.Wrnn), to_dev(inp.w_conf), to_dev(inp.u), w.K,
+        hidden=None if d == 0 else to_dev(inp.hidden), sts_temp=to_dev(inp.sts_temp),
+        inv_temperature=inv_temperature)
+    torch.cuda.synchronize()
+    return tok, p, conf
+
+
+def _compare(w, case, tok, p, conf, label):
+    reqs = [r for r in case.reqs if r not in case.unguarded]
+    idx = [case.reqs.index(r) for r in reqs]
+    got_tok = tok[reqs].cpu().numpy()
+    got_p = p[reqs].double().cpu().numpy()
+    ref_p = case.p[idx]
+    rel = np.abs(got_p - ref_p) / np.maximum(ref_p, 1e-300)
+    rel[ref_p < 1e-30] = 0.0
+    got_c = conf[reqs].double().cpu().numpy()
+    cerr = np.abs(got_c - case.conf[idx]).max()
+    log(f"[rnn draft] {label}: R={w.R} K={w.K} V={w.V} | {len(reqs)} requests compared, "
+        f"{len(case.unguarded)} unguarded, min margin {case.margin.min():.2e}; "
+        f"max p rel err {rel.max():.2e}, max conf err {cerr:.2e}")
+    np.testing.assert_array_equal(got_tok, case.tok[idx])
+    assert rel.max() <= P_RTOL
+    assert cerr <= C_ATOL
+    np.testing.assert_allclose(got_p.sum(axis=-1), 1.0, rtol=0, atol=1e-5)
+
+
+def test_rnn_draft_reduced_unaligned_vocabulary():
+    # V not a multiple of 4, a ragged last tile, rank 64, hidden states with
+    # d = 40 (a partial 32-wide step of the hidden projection), bf16 base logits
+    w = synth.scaled(synth.WORKLOADS["serving"], R=6, K=4, V=3001)
+    case = guard.draft_case(w, 1, rank=64, d=40, head="rnn")
+    tok, p, conf = _run_gpu(w, case, 40)
+    _compare(w, case, tok, p, conf, "reduced")
+
+
+def test_rnn_draft_vector_path_fp32_base_no_hidden():
+    # V, ld multiples of 4, fp32 base logits, rank 256, no hidden part (the
+    # projection reads only [s; e]), inverse temperature 0.8
+    w = synth.scaled(synth.WORKLOADS["mid"], R=5, K=3, V=4096)
+    case = guard.draft_case(w, 2, rank=256, d=0, inv_temperature=0.8, head="rnn")
+    tok, p, conf = _run_gpu(w, case, 0, inv_temperature=0.8)
+    _compare(w, case, tok, p, conf, "vector fp32, d = 0")
+
+
+@pytest.mark.parametrize("rank", [32, 128])
+def test_rnn_draft_other_ranks(rank):
+    w = synth.scaled(synth.WORKLOADS["serving"], R=3, K=3, V=1000)
+    case = guard.draft_case(w, 3, rank=rank, d=16, head="rnn")
+    tok, p, conf = _run_gpu(w, case, 16)
+    _compare(w, case, tok, p, conf, f"rank {rank}")
+
+
+def test_rnn_draft_several_request_blocks():
+    # 150 requests: ten state blocks (the last one partial), five LDS chunks
+    # of the vocabulary product, 150 * 2 = 300 hidden rows (a partial 64-row
+    # block of the projection)
+    w = synth.scaled(synth.WORKLOADS["serving"], R=150, K=2, V=1024)
+    case = guard.draft_case(w, 4, rank=64, d=8, head="rnn")
+    tok, p, conf = _run_gpu(w, case, 8)
+    _compare(w, case, tok, p, conf, "150 requests")
+
+
+def test_rnn_draft_long_block():
+    # 16 positions: the state recursion carries its rounding through the block
+    w = synth.scaled(synth.WORKLOADS["serving"], R=4, K=16, V=2048)
+    case = guard.draft_case(w, 6, rank=128, d=64, head="rnn")
+    tok, p, conf = _run_gpu(w, case, 64)
+    _compare(w, case, tok, p, conf, "16 positions")
+
+
+def test_rnn_draft_invalid_anchor():
+    w = synth.scaled(synth.WORKLOADS["serving"], R=5, K=3, V=777)
+    case = guard.draft_case(w, 5, rank=64, d=8, head="rnn")
+    anchor = case.inp.anchor.copy()
+    anchor[1], anchor[3] = -1, w.V
+    tok, p, conf = _run_gpu(w, case, 8, anchor=anchor)
+    t = tok.cpu().numpy()
+    c = conf.cpu().numpy()
+    assert (t[[1, 3]] == -1).all() and np.isnan(c[[1, 3]]).all()
+    assert np.isfinite(p[[1, 3]].cpu().numpy()).all()
+    keep = [0, 2, 4]
+    np.testing.assert_array_equal(t[keep], case.tok[keep])
+    assert np.abs(c[keep] - case.conf[keep]).max() <= C_ATOL
+
+
+def test_rnn_draft_repeated_calls_are_identical():
+    # the state buffers are rewritten every call (s_0 = 0 is not read from memory)
+    w = synth.scaled(synth.WORKLOADS["serving"], R=7, K=4, V=1500)
+    case = guard.draft_case(w, 7, rank=64, d=16, head="rnn")
+    a = _run_gpu(w, case, 16)
+    b = _run_gpu(w, case, 16)
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+    _compare(w, case, *a, "repeat")
+
+
+def test_rnn_draft_full_size_sampled():
+    # the serving shape: 128 requests, 16 positions, V = 129280, rank 256,
+    # 4096-wide hidden states; the oracle checks three requests in full
+    w = synth.WORKLOADS["serving"]
+    case = guard.draft_case(w, 0, rank=256, d=4096, reqs=[0, 61, 127], head="rnn")
+    tok, p, conf = _run_gpu(w, case, 4096)
+    _compare(w, case, tok, p, conf, "full size")
+    assert ((tok >= 0) & (tok < w.V)).all().item()
