@@ -186,18 +186,24 @@ __device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
 // workgroup.  Groups (request, KV head, split) are dealt to the queues round
 // robin in request order; inside a queue the items are counting-sorted by
 // length, longest first, with the row blocks of a group kept together.
+// Every loop is spread over (request, split) or (request, merge item) pairs,
+// so no thread runs a long chain of dependent LDS operations.
 constexpr int kPlanThreads = 1024;
+constexpr int kPlanMaxR = 8192;                                  // the ABI's limit on R
+constexpr int kBinsPerLane = (kBins + DSPARK_WAVE - 1) / DSPARK_WAVE;
+constexpr int kMergePerBlock = kRows / kMergeRows;               // merge items of a full row block
+static_assert(kQueues <= kPlanThreads / DSPARK_WAVE, "one wave per queue");
 __global__ __launch_bounds__(kPlanThreads) void mla_plan(Params p) {
     const AttnArgs& a = p.a;
     __shared__ int s_bin[kQueues][kBins];
-    __shared__ int s_qtot[kQueues];
-    __shared__ int s_wave[kPlanThreads / DSPARK_WAVE];
-    __shared__ int s_merge;
+    __shared__ int s_qstart[kQueues];
+    __shared__ int s_wave[2][kPlanThreads / DSPARK_WAVE];
+    __shared__ int s_gid0[kPlanMaxR];  // first group id of each request
+    __shared__ int s_mb0[kPlanMaxR];   // first merge item of each request
     const int tid = threadIdx.x;
     const int lane = tid & (DSPARK_WAVE - 1);
     const int wave = tid / DSPARK_WAVE;
     for (int i = tid; i < kQueues * kBins; i += kPlanThreads) (&s_bin[0][0])[i] = 0;
-    if (tid == 0) s_merge = 0;
     auto shape = [&](int r, int& q0, int& ql, int& kv, int& ns, int& nrb) {
         q0 = a.cu_q[r];
         ql = a.cu_q[r + 1] - q0;
@@ -212,89 +218,121 @@ __global__ __launch_bounds__(kPlanThreads) void mla_plan(Params p) {
         split_range(kv, s, st, en);
         return min((en - st + kStep - 1) / kStep, kBins - 1);
     };
-    // group ids: exclusive scan of the groups of each request (contiguous ranges)
+    // merge items of one KV head of a request: 16 per full row block, the last block's rows / 4
+    auto merges_of = [&](int ql, int ns, int nrb) {
+        if (ns <= 1) return 0;
+        const int last = ql * p.group - (nrb - 1) * kRows;
+        return (nrb - 1) * kMergePerBlock + (last + kMergeRows - 1) / kMergeRows;
+    };
+    // group ids and merge offsets: exclusive scans over requests (contiguous ranges per thread)
     const int per = (a.R + kPlanThreads - 1) / kPlanThreads;
     const int r0 = min(a.R, tid * per), r1 = min(a.R, r0 + per);
-    int mine = 0;
+    int mg = 0, mm = 0;
     for (int r = r0; r < r1; ++r) {
         int q0, ql, kv, ns, nrb;
-        if (shape(r, q0, ql, kv, ns, nrb)) mine += a.Hkv * ns;
+        if (shape(r, q0, ql, kv, ns, nrb)) {
+            mg += a.Hkv * ns;
+            mm += a.Hkv * merges_of(ql, ns, nrb);
+        }
     }
-    int incl = mine;
+    int ig = mg, im = mm;
     for (int o = 1; o < DSPARK_WAVE; o <<= 1) {
-        const int t = __shfl_up(incl, o, DSPARK_WAVE);
-        if (lane >= o) incl += t;
+        const int tg = __shfl_up(ig, o, DSPARK_WAVE), tm = __shfl_up(im, o, DSPARK_WAVE);
+        if (lane >= o) ig += tg, im += tm;
     }
-    if (lane == DSPARK_WAVE - 1) s_wave[wave] = incl;
+    if (lane == DSPARK_WAVE - 1) s_wave[0][wave] = ig, s_wave[1][wave] = im;
     __syncthreads();
-    int gid0 = incl - mine;
-    for (int w = 0; w < wave; ++w) gid0 += s_wave[w];
-    // histogram per queue and length
-    {
-        int gid = gid0;
-        for (int r = r0; r < r1; ++r) {
-            int q0, ql, kv, ns, nrb;
-            if (!shape(r, q0, ql, kv, ns, nrb)) continue;
-            for (int g = 0; g < a.Hkv; ++g)
-                for (int s = 0; s < ns; ++s, ++gid) atomicAdd(&s_bin[gid % kQueues][steps_of(kv, s)], nrb);
+    int g0 = ig - mg, m0 = im - mm, mtot = 0;
+    for (int w = 0; w < kPlanThreads / DSPARK_WAVE; ++w) {
+        if (w < wave) g0 += s_wave[0][w], m0 += s_wave[1][w];
+        mtot += s_wave[1][w];
+    }
+    for (int r = r0; r < r1; ++r) {
+        int q0, ql, kv, ns, nrb;
+        s_gid0[r] = g0;
+        s_mb0[r] = m0;
+        if (shape(r, q0, ql, kv, ns, nrb)) {
+            g0 += a.Hkv * ns;
+            m0 += a.Hkv * merges_of(ql, ns, nrb);
         }
     }
     __syncthreads();
-    if (tid < kQueues) {  // per queue: bin offsets, longest first
-        int off = 0;
-        for (int b = kBins - 1; b >= 0; --b) {
-            const int c = s_bin[tid][b];
-            s_bin[tid][b] = off;
-            off += c;
+    // histogram per queue and length: one thread per (request, split)
+    const int S = p.max_splits;
+    for (int u = tid; u < a.R * S; u += kPlanThreads) {
+        const int r = u / S, sp = u - r * S;
+        int q0, ql, kv, ns, nrb;
+        if (!shape(r, q0, ql, kv, ns, nrb) || sp >= ns) continue;
+        for (int g = 0; g < a.Hkv; ++g)
+            atomicAdd(&s_bin[(s_gid0[r] + g * ns + sp) % kQueues][steps_of(kv, sp)], nrb);
+    }
+    __syncthreads();
+    if (wave < kQueues) {
+        // bin offsets of queue `wave`, longest first: lane l owns the bins at
+        // descending positions kBinsPerLane * l .. kBinsPerLane * (l + 1) - 1
+        int cnt[kBinsPerLane], mine = 0;
+#pragma unroll
+        for (int k = 0; k < kBinsPerLane; ++k) {
+            const int bb = kBins - 1 - (kBinsPerLane * lane + k);
+            cnt[k] = bb >= 0 ? s_bin[wave][bb] : 0;
+            mine += cnt[k];
         }
-        s_qtot[tid] = off;
+        int incl = mine;
+        for (int o = 1; o < DSPARK_WAVE; o <<= 1) {
+            const int t = __shfl_up(incl, o, DSPARK_WAVE);
+            if (lane >= o) incl += t;
+        }
+        int run = incl - mine;
+#pragma unroll
+        for (int k = 0; k < kBinsPerLane; ++k) {
+            const int bb = kBins - 1 - (kBinsPerLane * lane + k);
+            if (bb >= 0) s_bin[wave][bb] = run;
+            run += cnt[k];
+        }
+        if (lane == DSPARK_WAVE - 1) s_qstart[wave] = incl;  // the queue's length, for now
     }
     __syncthreads();
     if (tid == 0) {
         int base = 0;
         for (int q = 0; q < kQueues; ++q) {
+            const int len = s_qstart[q];
             p.head[q] = 0;
             p.head[kQueues + q] = base;
-            base += s_qtot[q];
-            p.head[2 * kQueues + q] = base;
-            s_qtot[q] = p.head[kQueues + q];  // now the queue's start
+            p.head[2 * kQueues + q] = base + len;
+            s_qstart[q] = base;
+            base += len;
         }
+        p.head[3 * kQueues] = mtot;
     }
     __syncthreads();
-    {
-        int gid = gid0;
-        for (int r = r0; r < r1; ++r) {
-            int q0, ql, kv, ns, nrb;
-            if (!shape(r, q0, ql, kv, ns, nrb)) continue;
-            const int4 meta = int4{q0, ql, kv, ns};
-            for (int g = 0; g < a.Hkv; ++g)
-                for (int s = 0; s < ns; ++s, ++gid) {
-                    const int q = gid % kQueues;
-                    const int off = s_qtot[q] + atomicAdd(&s_bin[q][steps_of(kv, s)], nrb);
-                    for (int b = 0; b < nrb; ++b) {
-                        p.list[2 * (off + b)] = int4{r, g, b, s};
-                        p.list[2 * (off + b) + 1] = meta;
-                    }
-                }
-            if (ns > 1) {
-                const int rows = ql * p.group;
-                int cnt = 0;
-                for (int b = 0; b < nrb; ++b)
-                    cnt += (min(kRows, rows - b * kRows) + kMergeRows - 1) / kMergeRows;
-                int off = atomicAdd(&s_merge, a.Hkv * cnt);
-                for (int g = 0; g < a.Hkv; ++g)
-                    for (int b = 0; b < nrb; ++b) {
-                        const int nrows = min(kRows, rows - b * kRows);
-                        for (int m0 = 0; m0 < nrows; m0 += kMergeRows, ++off) {
-                            p.mlist[2 * off] = int4{r, g, b, m0};
-                            p.mlist[2 * off + 1] = meta;
-                        }
-                    }
+    // items: one thread per (request, split), the row blocks of a group together
+    for (int u = tid; u < a.R * S; u += kPlanThreads) {
+        const int r = u / S, sp = u - r * S;
+        int q0, ql, kv, ns, nrb;
+        if (!shape(r, q0, ql, kv, ns, nrb) || sp >= ns) continue;
+        const int4 meta = int4{q0, ql, kv, ns};
+        for (int g = 0; g < a.Hkv; ++g) {
+            const int q = (s_gid0[r] + g * ns + sp) % kQueues;
+            const int off = s_qstart[q] + atomicAdd(&s_bin[q][steps_of(kv, sp)], nrb);
+            for (int b = 0; b < nrb; ++b) {
+                p.list[2 * (off + b)] = int4{r, g, b, sp};
+                p.list[2 * (off + b) + 1] = meta;
             }
         }
     }
-    __syncthreads();
-    if (tid == 0) p.head[3 * kQueues] = s_merge;
+    // merge items: one thread per (request, item); KV head, then row block, then rows
+    const int M = a.Hkv * (p.rb_max * kMergePerBlock);  // items of a request, at most
+    for (int u = tid; u < a.R * M; u += kPlanThreads) {
+        const int r = u / M, j = u - r * M;
+        int q0, ql, kv, ns, nrb;
+        if (!shape(r, q0, ql, kv, ns, nrb)) continue;
+        const int cnt = merges_of(ql, ns, nrb);
+        if (j >= a.Hkv * cnt) continue;
+        const int g = j / cnt, jj = j - g * cnt;
+        const int off = s_mb0[r] + j;
+        p.mlist[2 * off] = int4{r, g, jj / kMergePerBlock, kMergeRows * (jj % kMergePerBlock)};
+        p.mlist[2 * off + 1] = int4{q0, ql, kv, ns};
+    }
 }
 
 // ------------------------------------------------------------------ item
