@@ -538,46 +538,74 @@ void tile_pass(const MarkovArgs& a, const uint16_t* E, float2* stats, const RowI
 // The backbone part of the RNN head's projection (eq. rnn), once for every
 // (request, position) since it does not depend on the drawn tokens:
 // Hp[row, i] = sum_{j < d} Wrnn[i, 2 rank + j] h[row, j], row = r K + k - 1,
-// i < 3 rank.  v_mfma_f32_16x16x32_bf16 with both operands read straight
-// from memory (a lane's 8 consecutive inputs are one 16-byte load); a
-// workgroup computes 64 rows x 64 outputs, wave w rows 16 w .. 16 w + 15, and
-// keeps kHpDepth steps of 32 inputs in flight.  d % 8 == 0, so a lane's 8
+// i < 3 rank.  v_mfma_f32_16x16x32_bf16; a workgroup computes 64 rows x 128
+// outputs.  Wave w owns rows 16 w .. 16 w + 15 and reads its hidden-state
+// fragments straight from memory, one step ahead; the 128 weight rows of each
+// 32-input step are staged once per workgroup in an LDS double buffer (row
+// pitch 80 bytes) and shared by the four waves.  d % 8 == 0, so a lane's 8
 // inputs are either all inside the row or all past its end.
-constexpr int kHpRows = 64, kHpCols = 64, kHpDepth = 4, kHpNt = kHpCols / 16;
+constexpr int kHpRows = 64, kHpCols = 128, kHpNt = kHpCols / 16, kHpPitch = 40;
 __global__ __launch_bounds__(kThreads) void rnn_hproj(MarkovArgs a, float* Hp) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    __shared__ __align__(16) uint16_t sb[2][kHpCols * kHpPitch];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int lr = lane & 15, lq = lane >> 4;
     const int nrows = a.R * a.K, ncols = 3 * a.rank, nz = 2 * a.rank + a.d;
     const int m0 = blockIdx.x * kHpRows + 16 * wave;
     const int n0 = blockIdx.y * kHpCols;
-    const uint16_t* ap = a.hidden + (int64_t)min(m0 + lr, nrows - 1) * a.d + 8 * lq;
-    const uint16_t* bp[kHpNt];
+    // row starts (hidden row; a weight row's hidden columns): a lane's 8 inputs
+    // past the end of the row read the row's first 8 instead (always inside the
+    // row, d >= 8) and are zeroed
+    const uint16_t* arow = a.hidden + (int64_t)min(m0 + lr, nrows - 1) * a.d;
+    // this thread's two 16-byte pieces of a step's weight tile: piece c is row
+    // c / 4, input chunk c % 4
+    const uint16_t* brow[2];
+    int bdst[2], bpart[2];
 #pragma unroll
-    for (int nt = 0; nt < kHpNt; ++nt)
-        bp[nt] = a.Wrnn + (int64_t)min(n0 + 16 * nt + lr, ncols - 1) * nz + 2 * a.rank + 8 * lq;
+    for (int i = 0; i < 2; ++i) {
+        const int c = tid + kThreads * i;
+        bpart[i] = c & 3;
+        brow[i] = a.Wrnn + (int64_t)min(n0 + (c >> 2), ncols - 1) * nz + 2 * a.rank;
+        bdst[i] = (c >> 2) * kHpPitch + 8 * bpart[i];
+    }
     const int nsteps = ceil_div(a.d, 32);
-    bf16x8 af[kHpDepth], bfr[kHpDepth][kHpNt];
-    auto load = [&](int st, int slot) {
-        const bool in = st < nsteps && 32 * st + 8 * lq < a.d;
-        const int off = in ? 32 * st : 0;  // past the end: a valid address, zeroed below
-        af[slot] = *(const bf16x8*)(ap + off);
+    auto load_a = [&](int st) {
+        const int kk = 32 * st + 8 * lq;
+        const bool in = st < nsteps && kk < a.d;
+        const bf16x8 v = *(const bf16x8*)(arow + (in ? kk : 0));
+        return in ? v : bf16x8{};
+    };
+    auto load_b = [&](int st, uint4* v) {
 #pragma unroll
-        for (int nt = 0; nt < kHpNt; ++nt) bfr[slot][nt] = *(const bf16x8*)(bp[nt] + off);
-        if (!in) af[slot] = bf16x8{};
+        for (int i = 0; i < 2; ++i) {
+            const int kk = 32 * st + 8 * bpart[i];
+            const bool in = st < nsteps && kk < a.d;
+            const uint4 w = *(const uint4*)(brow[i] + (in ? kk : 0));
+            v[i] = in ? w : uint4{0u, 0u, 0u, 0u};
+        }
     };
     f32x4 acc[kHpNt];
 #pragma unroll
     for (int nt = 0; nt < kHpNt; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    uint4 vb[2];
+    load_b(0, vb);
+    bf16x8 a_cur = load_a(0), a_next = load_a(1);
 #pragma unroll
-    for (int u = 0; u < kHpDepth; ++u) load(u, u);
-    for (int st0 = 0; st0 < nsteps; st0 += kHpDepth) {
+    for (int i = 0; i < 2; ++i) *(uint4*)(&sb[0][bdst[i]]) = vb[i];
+    __syncthreads();
+    for (int st = 0; st < nsteps; ++st) {
+        load_b(st + 1, vb);  // the next step's tile stays in flight during the products
+        const uint16_t* cur = sb[st & 1];
 #pragma unroll
-        for (int u = 0; u < kHpDepth; ++u) {
-#pragma unroll
-            for (int nt = 0; nt < kHpNt; ++nt)
-                acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[u], bfr[u][nt], acc[nt], 0, 0, 0);
-            load(st0 + kHpDepth + u, u);
+        for (int nt = 0; nt < kHpNt; ++nt) {
+            const bf16x8 bfrag = *(const bf16x8*)(cur + (16 * nt + lr) * kHpPitch + 8 * lq);
+            acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_cur, bfrag, acc[nt], 0, 0, 0);
         }
+        a_cur = a_next;
+        a_next = load_a(st + 2);
+        // the other buffer was last read in step st - 1, before the barrier that ended it
+#pragma unroll
+        for (int i = 0; i < 2; ++i) *(uint4*)(&sb[(st + 1) & 1][bdst[i]]) = vb[i];
+        __syncthreads();
     }
     // lane holds rows m0 + 4 lq + e, output n0 + 16 nt + lr
 #pragma unroll
@@ -591,103 +619,109 @@ __global__ __launch_bounds__(kThreads) void rnn_hproj(MarkovArgs a, float* Hp) {
     }
 }
 
-// Position k of the RNN head: a = Hp[r, k] + Wrnn[:, :2 rank] [s_{k-1}; e_k]
-// (e_k = W1[x_{k-1}], gathered by the previous position's draw), the gated
-// state update s_k = g s_{k-1} + (1 - g) tanh(a_c) with g = sigmoid(a_g), and
-// the head's output o_k = tanh(a_o), written for md_tile as three bf16 terms
-// (hi, mid, lo: each the rounding of what the previous ones leave, so their
-// sum is o_k to fp32 accuracy).  A workgroup owns 16 state dims j and 16
-// requests, with its weight rows (gate, candidate and output rows of those
-// dims) and the requests' [s_{k-1}; e_k] in LDS; thread (j, request) computes
-// the three rows' dot products over 2 rank inputs in fp32.  The state is
-// double-buffered (s_prev is read by every workgroup of a request block while
-// others write s_next); s_0 = 0.
-constexpr int kStJ = 16, kStR = 16;
-static_assert(kStJ * kStR == kThreads, "one thread per (dim, request)");
-__host__ __device__ constexpr int st_wpitch(int rank) { return 2 * rank + 8; }  // bf16 elements
-__host__ __device__ constexpr int st_zpitch(int rank) { return 2 * rank + 4; }  // fp32 elements
-static size_t rnn_state_lds(int rank) {
-    return (size_t)3 * kStJ * st_wpitch(rank) * 2 + (size_t)kStR * st_zpitch(rank) * 4;
+// hi + mid + lo: each term the bf16 rounding of what the previous ones leave,
+// so that their sum is v to fp32 accuracy
+__device__ __forceinline__ void split3(float v, uint16_t* dst, int stride) {
+    const uint16_t hi = f32_to_bf16(v);
+    const float r1 = v - bf16_to_f32(hi);
+    const uint16_t mid = f32_to_bf16(r1);
+    dst[0] = hi;
+    dst[stride] = mid;
+    dst[2 * stride] = f32_to_bf16(r1 - bf16_to_f32(mid));
 }
 
+// Position k of the RNN head on the matrix cores: a = Hp[r, k] + Wrnn[:, :2 rank]
+// [s_{k-1}; e_k], e_k = W1[x_{k-1}] gathered by the previous position's draw.
+// The K dimension runs over 4 rank inputs: the fp32 state as three bf16 terms
+// (hi, mid, lo; written by the previous position) against the state columns
+// three times, then the exact bf16 embedding against the embedding columns.
+// The output columns of a workgroup are the gate, candidate and output rows of
+// 16 state dims, so a lane holds all three pre-activations of one (request,
+// dim) and applies the gated update in registers: s_k = g s_{k-1} + (1 - g)
+// tanh(a_c) with g = sigmoid(a_g), written in fp32 and as three terms, and the
+// head's output o_k = tanh(a_o) as three terms for md_tile.  A workgroup owns
+// 16 dims x 16 requests; its four waves take every fourth 32-input step (both
+// operands straight from memory, kStDepth steps ahead) and wave 0 adds the
+// four partial products in wave order.  The state is double-buffered (others
+// may still read s_{k-1}); at k = 1 it is zero and its steps are skipped.
+constexpr int kStJ = 16, kStR = 16, kStDepth = 4;
 __global__ __launch_bounds__(kThreads) void rnn_state(MarkovArgs a, const float* Hp,
-                                                      const float* s_prev, float* s_next,
+                                                      const float* s_prev, const uint16_t* S3_prev,
+                                                      float* s_next, uint16_t* S3_next,
                                                       const uint16_t* Ee, uint16_t* E3, int k) {
-    extern __shared__ __align__(16) unsigned char st_smem[];
-    const int rank = a.rank, n2 = 2 * rank;
-    const int wp = st_wpitch(rank), zp = st_zpitch(rank);
-    uint16_t* Wl = reinterpret_cast<uint16_t*>(st_smem);                    // [3 * kStJ][wp]
-    float* Zl = reinterpret_cast<float*>(st_smem + (size_t)3 * kStJ * wp * 2);  // [kStR][zp]
-    const int tid = threadIdx.x;
-    const int j0 = blockIdx.x * kStJ, r0 = blockIdx.y * kStR;
-    const int nz = n2 + a.d;
-    // weight rows: part p, dim j0 + jj -> LDS row p * kStJ + jj, the 2 rank state and embedding columns
-    const int wch = n2 / 8;  // 16-byte chunks per row
-    for (int i = tid; i < 3 * kStJ * wch; i += kThreads) {
-        const int lrow = i / wch, c = i - lrow * wch;
-        const int p = lrow / kStJ, jj = lrow - p * kStJ;
-        *(uint4*)(Wl + lrow * wp + 8 * c) =
-            *(const uint4*)(a.Wrnn + (int64_t)(p * rank + j0 + jj) * nz + 8 * c);
-    }
-    // [s_{k-1}; e_k] of the block's requests (zero past R; s_0 = 0)
-    for (int i = tid; i < kStR * n2; i += kThreads) {
-        const int rr = i / n2, c = i - rr * n2, r = r0 + rr;
-        float v = 0.0f;
-        if (r < a.R) {
-            if (c < rank) v = k > 1 ? s_prev[(int64_t)r * rank + c] : 0.0f;
-            else v = bf16_to_f32(Ee[(int64_t)r * rank + (c - rank)]);
+    __shared__ f32x4 part[kWaves - 1][3][DSPARK_WAVE];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lr = lane & 15, lq = lane >> 4;
+    const int rank = a.rank, nz = 2 * rank + a.d;
+    const int j0 = blockIdx.x * kStJ;
+    const int m0 = blockIdx.y * kStR;
+    const int ra = min(m0 + lr, a.R - 1);  // request of this lane's A fragment
+    const int ks_s = 3 * rank / 32, nst = ks_s + rank / 32;
+    const int st0 = (k > 1 ? 0 : ks_s) + wave;  // this wave's steps: st0, st0 + 4, ...
+    bf16x8 af[kStDepth], bfr[kStDepth][3];
+    auto load = [&](int i, int slot) {  // this wave's i-th step
+        const int kk = 32 * min(st0 + kWaves * i, nst - 1) + 8 * lq;  // past the end: unused
+        const bool state = kk < 3 * rank;                            // uniform over the wave
+        af[slot] = state ? *(const bf16x8*)(S3_prev + (int64_t)ra * 3 * rank + kk)
+                         : *(const bf16x8*)(Ee + (int64_t)ra * rank + (kk - 3 * rank));
+        const int col = state ? kk % rank : kk - 2 * rank;
+#pragma unroll
+        for (int p = 0; p < 3; ++p)
+            bfr[slot][p] = *(const bf16x8*)(a.Wrnn + (int64_t)(p * rank + j0 + lr) * nz + col);
+    };
+    const int nmine = st0 < nst ? (nst - st0 + kWaves - 1) / kWaves : 0;
+    f32x4 acc[3];
+#pragma unroll
+    for (int p = 0; p < 3; ++p) acc[p] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int u = 0; u < kStDepth; ++u) load(u, u);
+    for (int i0 = 0; i0 < nmine; i0 += kStDepth) {
+#pragma unroll
+        for (int u = 0; u < kStDepth; ++u) {
+            if (i0 + u < nmine) {
+#pragma unroll
+                for (int p = 0; p < 3; ++p)
+                    acc[p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[u], bfr[u][p], acc[p], 0, 0, 0);
+            }
+            load(i0 + kStDepth + u, u);
         }
-        Zl[rr * zp + c] = v;
+    }
+    if (wave > 0) {
+#pragma unroll
+        for (int p = 0; p < 3; ++p) part[wave - 1][p][lane] = acc[p];
     }
     __syncthreads();
-    const int jj = tid / kStR, rr = tid % kStR;
-    const int j = j0 + jj, r = r0 + rr;
-    const uint16_t* wg = Wl + (0 * kStJ + jj) * wp;
-    const uint16_t* wc = Wl + (1 * kStJ + jj) * wp;
-    const uint16_t* wo = Wl + (2 * kStJ + jj) * wp;
-    const float* z = Zl + rr * zp;
-    float ag = 0.0f, ac = 0.0f, ao = 0.0f;
-    for (int c = 0; c < n2; c += 8) {
-        const float4 z0 = *(const float4*)(z + c), z1 = *(const float4*)(z + c + 4);
-        const float zz[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
-        const uint4 g8 = *(const uint4*)(wg + c), c8 = *(const uint4*)(wc + c), o8 = *(const uint4*)(wo + c);
-        const uint32_t gw[4] = {g8.x, g8.y, g8.z, g8.w}, cw[4] = {c8.x, c8.y, c8.z, c8.w},
-                       ow[4] = {o8.x, o8.y, o8.z, o8.w};
+    if (wave > 0) return;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            ag = __builtin_fmaf(__uint_as_float(gw[q] << 16), zz[2 * q], ag);
-            ag = __builtin_fmaf(__uint_as_float(gw[q] & 0xffff0000u), zz[2 * q + 1], ag);
-            ac = __builtin_fmaf(__uint_as_float(cw[q] << 16), zz[2 * q], ac);
-            ac = __builtin_fmaf(__uint_as_float(cw[q] & 0xffff0000u), zz[2 * q + 1], ac);
-            ao = __builtin_fmaf(__uint_as_float(ow[q] << 16), zz[2 * q], ao);
-            ao = __builtin_fmaf(__uint_as_float(ow[q] & 0xffff0000u), zz[2 * q + 1], ao);
+    for (int w = 0; w < kWaves - 1; ++w)
+#pragma unroll
+        for (int p = 0; p < 3; ++p) acc[p] += part[w][p][lane];
+    // lane holds requests m0 + 4 lq + e, state dim j0 + lr
+    const int j = j0 + lr;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int r = m0 + 4 * lq + e;
+        if (r >= a.R) continue;
+        float ag = acc[0][e], ac = acc[1][e], ao = acc[2][e];
+        if (Hp) {
+            const float* hp = Hp + ((int64_t)r * a.K + (k - 1)) * (3 * rank);
+            ag += hp[j];
+            ac += hp[rank + j];
+            ao += hp[2 * rank + j];
         }
+        const float g = 1.0f / (1.0f + expf(-ag));
+        const float sp = k > 1 ? s_prev[(int64_t)r * rank + j] : 0.0f;
+        const float sn = g * sp + (1.0f - g) * tanhf(ac);
+        s_next[(int64_t)r * rank + j] = sn;
+        split3(sn, S3_next + (int64_t)r * 3 * rank + j, rank);
+        split3(tanhf(ao), E3 + (int64_t)r * 3 * rank + j, rank);
     }
-    if (r >= a.R) return;
-    if (Hp) {
-        const float* hp = Hp + ((int64_t)r * a.K + (k - 1)) * (3 * rank);
-        ag += hp[j];
-        ac += hp[rank + j];
-        ao += hp[2 * rank + j];
-    }
-    const float g = 1.0f / (1.0f + expf(-ag));
-    const float sp = z[j];  // s_{k-1}[j]
-    s_next[(int64_t)r * rank + j] = g * sp + (1.0f - g) * tanhf(ac);
-    const float o = tanhf(ao);
-    const uint16_t hi = f32_to_bf16(o);
-    const float r1 = o - bf16_to_f32(hi);
-    const uint16_t mid = f32_to_bf16(r1);
-    const uint16_t lo = f32_to_bf16(r1 - bf16_to_f32(mid));
-    uint16_t* e3 = E3 + (int64_t)r * 3 * rank;
-    e3[j] = hi;
-    e3[rank + j] = mid;
-    e3[2 * rank + j] = lo;
 }
 
 template <int KS>
 hipError_t launch_rnn_ks(const MarkovArgs& a, uint16_t* Ee, uint16_t* E3, float* S0, float* S1,
-                         float* Hp, float2* stats, RowInfo* info, float* sh, int ntiles, bool vec,
-                         hipStream_t s) {
+                         uint16_t* T0, uint16_t* T1, float* Hp, float2* stats, RowInfo* info,
+                         float* sh, int ntiles, bool vec, hipStream_t s) {
     const int64_t rows = (int64_t)a.R * a.K;
     if (a.d > 0) {
         hipLaunchKernelGGL(md_hidden, dim3((unsigned)ceil_div((int)rows, kWaves)), dim3(kThreads), 0, s, a, sh);
@@ -697,12 +731,14 @@ hipError_t launch_rnn_ks(const MarkovArgs& a, uint16_t* Ee, uint16_t* E3, float*
     const float* shp = a.d > 0 ? sh : nullptr;
     const float* hpp = a.d > 0 ? Hp : nullptr;
     hipLaunchKernelGGL(md_first, dim3(ceil_div(a.R, kWaves)), dim3(kThreads), 0, s, a, shp, Ee);
-    const size_t lds = rnn_state_lds(a.rank);
     for (int k = 1; k <= a.K; ++k) {
-        const float* sp = (k & 1) ? S1 : S0;  // s_{k-1} (unread at k = 1)
+        // s_{k-1} in fp32 and as three terms (unread at k = 1), and where s_k goes
+        const float* sp = (k & 1) ? S1 : S0;
         float* sn = (k & 1) ? S0 : S1;
-        hipLaunchKernelGGL(rnn_state, dim3(a.rank / kStJ, ceil_div(a.R, kStR)), dim3(kThreads), lds, s, a, hpp,
-                           sp, sn, (const uint16_t*)Ee, E3, k);
+        const uint16_t* tp = (k & 1) ? T1 : T0;
+        uint16_t* tn = (k & 1) ? T0 : T1;
+        hipLaunchKernelGGL(rnn_state, dim3(a.rank / kStJ, ceil_div(a.R, kStR)), dim3(kThreads), 0, s, a, hpp,
+                           sp, tp, sn, tn, (const uint16_t*)Ee, E3, k);
         tile_pass<KS, 3, 0>(a, E3, stats, info, Ee, shp, ntiles, k, vec, s);
         hipLaunchKernelGGL(md_stats, dim3(a.R), dim3(kThreads), 0, s, a, stats, info, ntiles, k);
         // the draw gathers W1[x_k] into Ee: the embedding input of position k + 1
@@ -754,7 +790,7 @@ namespace {
 // RNN head: the embedding input Ee, the three-term output E3, two state
 // buffers, the backbone part of the projection, then what the Markov head uses
 struct RnnLayout {
-    size_t ee, e3, st, hp, stats, info, sh, total;
+    size_t ee, e3, st, st3, hp, stats, info, sh, total;
 };
 RnnLayout rnn_layout(int R, int K, int V, int rank) {
     const int ntiles = mkd::ceil_div(V, mkd::kTileV);
@@ -762,11 +798,12 @@ RnnLayout rnn_layout(int R, int K, int V, int rank) {
     l.ee = align256((size_t)R * rank * 2);
     l.e3 = align256((size_t)R * 3 * rank * 2);
     l.st = align256((size_t)R * rank * 4);
+    l.st3 = align256((size_t)R * 3 * rank * 2);
     l.hp = align256((size_t)R * K * 3 * rank * 4);
     l.stats = align256((size_t)R * ntiles * sizeof(float2));
     l.info = align256((size_t)R * sizeof(mkd::RowInfo));
     l.sh = align256((size_t)R * K * sizeof(float));
-    l.total = l.ee + l.e3 + 2 * l.st + l.hp + l.stats + l.info + l.sh;
+    l.total = l.ee + l.e3 + 2 * l.st + 2 * l.st3 + l.hp + l.stats + l.info + l.sh;
     return l;
 }
 }  // namespace
@@ -781,24 +818,20 @@ hipError_t launch_rnn(const MarkovArgs& a, void* ws, hipStream_t s) {
     uint16_t* E3 = (uint16_t*)p;                 p += l.e3;
     float* S0 = (float*)p;                       p += l.st;
     float* S1 = (float*)p;                       p += l.st;
+    uint16_t* T0 = (uint16_t*)p;                 p += l.st3;
+    uint16_t* T1 = (uint16_t*)p;                 p += l.st3;
     float* Hp = (float*)p;                       p += l.hp;
     float2* stats = (float2*)p;                  p += l.stats;
     mkd::RowInfo* info = (mkd::RowInfo*)p;       p += l.info;
     float* sh = (float*)p;
-    const size_t lds = mkd::rnn_state_lds(a.rank);
-    if (lds > 64 * 1024) {
-        hipError_t e = hipFuncSetAttribute((const void*)mkd::rnn_state,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return e;
-    }
     const size_t eb = a.base_bf16 ? 2 : 4;
     const bool vec = a.V % 4 == 0 && a.ld % 4 == 0 && ((uintptr_t)a.base % (4 * eb)) == 0 &&
                      ((uintptr_t)a.draft_p % 16) == 0;
     switch (a.rank) {
-        case 32: return mkd::launch_rnn_ks<1>(a, Ee, E3, S0, S1, Hp, stats, info, sh, ntiles, vec, s);
-        case 64: return mkd::launch_rnn_ks<2>(a, Ee, E3, S0, S1, Hp, stats, info, sh, ntiles, vec, s);
-        case 128: return mkd::launch_rnn_ks<4>(a, Ee, E3, S0, S1, Hp, stats, info, sh, ntiles, vec, s);
-        default: return mkd::launch_rnn_ks<8>(a, Ee, E3, S0, S1, Hp, stats, info, sh, ntiles, vec, s);
+        case 32: return mkd::launch_rnn_ks<1>(a, Ee, E3, S0, S1, T0, T1, Hp, stats, info, sh, ntiles, vec, s);
+        case 64: return mkd::launch_rnn_ks<2>(a, Ee, E3, S0, S1, T0, T1, Hp, stats, info, sh, ntiles, vec, s);
+        case 128: return mkd::launch_rnn_ks<4>(a, Ee, E3, S0, S1, T0, T1, Hp, stats, info, sh, ntiles, vec, s);
+        default: return mkd::launch_rnn_ks<8>(a, Ee, E3, S0, S1, T0, T1, Hp, stats, info, sh, ntiles, vec, s);
     }
 }
 
