@@ -298,22 +298,21 @@ __global__ __launch_bounds__(kBlk) void acc_rowpass(
 
 // ---------------------------------------------------------------- resolve
 
-// Row statistics from the chunk statistics: one wave per row, lanes over chunks.
+// Row statistics from the chunk statistics: one wave per row, lanes over
+// chunks.  A lane folds its chunks in order (stat_absorb), then the wave
+// combines the lanes (stat_combine).
 template <bool GREEDY>
-__device__ __forceinline__ void row_stats(const ChunkStat* st, int nch, float& A, float& B,
-                                          int& arg) {
-    const int lane = threadIdx.x & (kLanes - 1);
-    float a = -__builtin_huge_valf(), b = 0.0f;
-    int i = 0x7fffffff;
-    for (int c = lane; c < nch; c += kLanes) {
-        const ChunkStat x = st[c];
-        if (GREEDY) {
-            if (x.a > a || (x.a == a && x.arg < i)) { a = x.a; i = x.arg; }
-        } else if (x.a > -__builtin_huge_valf()) {
-            if (x.a > a) { b = b * exp2f(a - x.a) + x.b; a = x.a; }
-            else b += x.b * exp2f(x.a - a);
-        }
+__device__ __forceinline__ void stat_absorb(const ChunkStat& x, float& a, float& b, int& i) {
+    if (GREEDY) {
+        if (x.a > a || (x.a == a && x.arg < i)) { a = x.a; i = x.arg; }
+    } else if (x.a > -__builtin_huge_valf()) {
+        if (x.a > a) { b = b * exp2f(a - x.a) + x.b; a = x.a; }
+        else b += x.b * exp2f(x.a - a);
     }
+}
+
+template <bool GREEDY>
+__device__ __forceinline__ void stat_combine(float& a, float& b, int& i) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
         const float oa = __shfl_xor(a, o, kLanes);
@@ -330,10 +329,22 @@ __device__ __forceinline__ void row_stats(const ChunkStat* st, int nch, float& A
             b = nb;
         }
     }
+}
+
+template <bool GREEDY>
+__device__ __forceinline__ void row_stats(const ChunkStat* st, int nch, float& A, float& B,
+                                          int& arg) {
+    const int lane = threadIdx.x & (kLanes - 1);
+    float a = -__builtin_huge_valf(), b = 0.0f;
+    int i = 0x7fffffff;
+    for (int c = lane; c < nch; c += kLanes) stat_absorb<GREEDY>(st[c], a, b, i);
+    stat_combine<GREEDY>(a, b, i);
     A = a;
     B = b;
     arg = i;
 }
+
+constexpr int kResolveRows = (65 + kWaves - 1) / kWaves;  // rows per wave (K <= 64)
 
 template <bool BF16, bool GREEDY>
 __global__ __launch_bounds__(kBlk) void acc_resolve(
@@ -365,42 +376,75 @@ __global__ __launch_bounds__(kBlk) void acc_resolve(
         return;
     }
     const size_t esz = BF16 ? 2 : 4;
-    for (int t = wave; t <= l; t += kWaves) {
-        const int64_t row = row0 + t;
-        // the tested draft's target logit, draft probability and uniform are
-        // loaded together with the chunk statistics
+    // row t's results: statistics and accept test, kept by lane `ln`
+    auto finish = [&](int t, int ln, float A, float B, int arg, bool test, float y, float pd,
+                      float uu) {
+        if (lane != ln) return;
+        int rej = 0;
+        if (GREEDY) {
+            if (t < l) rej = s_tok[t] != arg;
+            s_arg[t] = arg;
+        } else {
+            rows[row0 + t] = RowInfo{A, B, r, t};
+            s_M[t] = A;
+            s_S[t] = B;
+            if (t < l) {
+                if (!test) {
+                    rej = 1;  // draft token outside the vocabulary
+                } else {
+                    const float pt = exp2f(y - A) / B;
+                    const float ratio = pd > 0.0f ? pt / pd : __builtin_huge_valf();
+                    rej = !(uu < ratio);
+                }
+            }
+        }
+        s_rej[t] = rej;
+    };
+    // the tested draft's target logit, draft probability and uniform of row t
+    auto gather = [&](int t, bool& test, float& y, float& pd, float& uu) {
         const int x = t < l ? s_tok[t] : -1;
-        const bool test = !GREEDY && lane == 0 && t < l && x >= 0 && x < V;
-        float y = 0.0f, pd = 0.0f, uu = 0.0f;
+        test = !GREEDY && t < l && x >= 0 && x < V;
+        y = pd = uu = 0.0f;
         if (test) {
-            const void* rp = (const char*)logits + (size_t)row * (size_t)ld * esz;
+            const void* rp = (const char*)logits + (size_t)(row0 + t) * (size_t)ld * esz;
             y = load_logit<BF16>(rp, x) * scale2;
             pd = draft_p[((int64_t)r * K + t) * V + x];
             uu = u[(int64_t)r * (K + 1) + t];
         }
-        float A, B;
-        int arg;
-        row_stats<GREEDY>(stats + row * nch, nch, A, B, arg);
-        if (lane == 0) {
-            int rej = 0;
-            if (GREEDY) {
-                if (t < l) rej = x != arg;
-                s_arg[t] = arg;
-            } else {
-                rows[row] = RowInfo{A, B, r, t};
-                s_M[t] = A;
-                s_S[t] = B;
-                if (t < l) {
-                    if (!test) {
-                        rej = 1;  // draft token outside the vocabulary
-                    } else {
-                        const float pt = exp2f(y - A) / B;
-                        const float ratio = pd > 0.0f ? pt / pd : __builtin_huge_valf();
-                        rej = !(uu < ratio);
-                    }
-                }
-            }
-            s_rej[t] = rej;
+    };
+    if (nch <= kLanes) {
+        // one chunk per lane: the chunk statistics of every row of this wave
+        // (t = wave + 4 j) and, on lane j, row t's test inputs are all in
+        // flight at once
+        ChunkStat xs[kResolveRows];
+#pragma unroll
+        for (int j = 0; j < kResolveRows; ++j) {
+            const int t = wave + kWaves * j;
+            if (t <= l && lane < nch) xs[j] = stats[(int64_t)(row0 + t) * nch + lane];
+        }
+        const int tj = wave + kWaves * lane;
+        bool test = false;
+        float y = 0.0f, pd = 0.0f, uu = 0.0f;
+        if (lane < kResolveRows && tj <= l) gather(tj, test, y, pd, uu);
+#pragma unroll
+        for (int j = 0; j < kResolveRows; ++j) {
+            const int t = wave + kWaves * j;
+            if (t > l) break;
+            float a = -__builtin_huge_valf(), b = 0.0f;
+            int i = 0x7fffffff;
+            if (lane < nch) stat_absorb<GREEDY>(xs[j], a, b, i);
+            stat_combine<GREEDY>(a, b, i);
+            finish(t, j, a, b, i, test, y, pd, uu);
+        }
+    } else {
+        for (int t = wave; t <= l; t += kWaves) {
+            bool test = false;
+            float y = 0.0f, pd = 0.0f, uu = 0.0f;
+            if (lane == 0) gather(t, test, y, pd, uu);
+            float A, B;
+            int arg;
+            row_stats<GREEDY>(stats + (int64_t)(row0 + t) * nch, nch, A, B, arg);
+            finish(t, 0, A, B, arg, test, y, pd, uu);
         }
     }
     __syncthreads();

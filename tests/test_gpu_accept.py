@@ -37,7 +37,7 @@ def test_workloads_full_size(name):
 
 @pytest.mark.parametrize("name", ["tiny", "mid", "highconc"])
 def test_reduced_sizes(name):
-    # vocabularies that are not a multiple of the 8192-token chunk, several chunks
+    # vocabularies that are not a multiple of the 4096-token chunk, several chunks
     w = synth.scaled(synth.WORKLOADS[name], R=24, V=20000 + 37)
     for seed in (2, 3):
         case = guard.build_case(w, seed, with_kv=False)
@@ -69,6 +69,46 @@ def test_identical_distributions_accept_all():
     w = synth.scaled(synth.WORKLOADS["mid"], R=R, K=K, V=V)
     acc, nxt, _ = gpu_accept(w, synth.Drafts(tok, dp, u), z, cu)
     assert (acc == K).all()
+
+
+def test_longest_block_accept_all_with_rate():
+    """K = 64: 65 verified rows per request, the bonus draw from row 64, and
+    every row's statistics written for the analytic rate (1 here)."""
+    rng = np.random.default_rng(12)
+    R, K, V = 6, 64, 2500
+    z = (rng.normal(size=(R * (K + 1), V)) * 3).astype(np.float32)
+    cu = np.arange(R + 1, dtype=np.int32) * (K + 1)
+    p = softmax(z.astype(np.float64), axis=1).astype(np.float32)
+    dp = np.stack([p[cu[r]: cu[r] + K] for r in range(R)])
+    tok = rng.integers(0, V, size=(R, K)).astype(np.int32)
+    u = (rng.random((R, K + 1)) * 0.999).astype(np.float32)
+    w = synth.scaled(synth.WORKLOADS["mid"], R=R, K=K, V=V)
+    acc, nxt, rate = gpu_accept(w, synth.Drafts(tok, dp, u), z, cu, want_rate=True)
+    acc_o, nxt_o, mg, rate_o = oracle.accept(tok, dp, z, "f32", cu, K, V, u=u, want_rate=True)
+    assert (acc == K).all() and (acc_o == K).all()
+    ok = mg >= guard.ACCEPT_GUARD
+    log(f"[accept] K=64 accept-all: {ok.sum()} of {R} requests guarded")
+    assert ok.sum() >= R // 2
+    assert np.array_equal(nxt[ok], nxt_o[ok])
+    tested = rate_o >= 0
+    assert np.array_equal(rate < 0, ~tested)
+    np.testing.assert_allclose(rate[tested], rate_o[tested], atol=2e-5)
+
+
+def test_wide_vocabulary_rows_one_at_a_time():
+    # V = 300007: 74 chunks per row, more than one per lane, so the accept
+    # tests fold each row's statistics on their own
+    w = synth.scaled(synth.WORKLOADS["mid"], R=4, K=5, V=300007)
+    case = guard.build_case(w, 9, with_kv=False)
+    _compare(case, f"wide/V{w.V}")
+    _, _, _, rate_o = oracle.accept(case.drafts.draft_tok, case.drafts.draft_p, case.logits,
+                                    w.logit_dtype, case.cu_q, w.K, w.V, u=case.drafts.u,
+                                    want_rate=True)
+    _, _, rate = gpu_accept(w, case.drafts, case.logits, case.cu_q, want_rate=True)
+    total = case.total_q
+    tested = rate_o[:total] >= 0
+    assert np.array_equal(rate[:total] < 0, ~tested)
+    np.testing.assert_allclose(rate[:total][tested], rate_o[:total][tested], atol=2e-5)
 
 
 def test_greedy_ties_and_rejections():
