@@ -233,6 +233,28 @@ def copy_probe():
     log(f"copy probe: 10 copies of {n} bytes")
 
 
+def copy_ceiling():
+    """Bandwidth of a plain device-to-device copy (1 GiB, read + write bytes,
+    best of ten), measured after the timed steps: the ceiling that a simple
+    streaming kernel reaches on this part, beside the 8 TB/s data-sheet peak."""
+    import torch
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda:0")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    b.copy_(a)
+    best = 0.0
+    for _ in range(10):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        b.copy_(a)
+        e1.record()
+        e1.synchronize()
+        best = max(best, 2 * n / (e0.elapsed_time(e1) / 1e3) / 1e9)
+    del a, b
+    return best
+
+
 def main():
     args = parse()
     if args.traffic_from:
@@ -405,6 +427,12 @@ def main():
         # split-merge launches, bracketed together by the events)
         "roofline": roofline_entry(w.name, path, ab, af, attn_s),
     }
+    ceil = copy_ceiling()
+    result["copy_ceiling"] = {"what": "device-to-device copy of 1 GiB, read + write bytes, best of 10",
+                              "gbps": ceil, "attn_frac": attn_gbps / ceil,
+                              "attn_accept_frac": both_gbps / ceil}
+    log(f"copy ceiling {ceil:.0f} GB/s: attention at {attn_gbps / ceil:.1%} of it, "
+        f"attention+accept at {both_gbps / ceil:.1%}")
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, seed, conf, sps, ln, kv, q, logits, dr,
