@@ -584,10 +584,20 @@ def draft_bench(args):
         while tn * reps < 0.66 * args.cpu_seconds:  # the whole block is quick: repeat it
             tn += run(n)
             reps += 1
+        # one thread, one request
+        oracle.set_threads(1)
+        try:
+            t_one = run(1)
+        finally:
+            oracle.set_threads(th)
         result["cpu_baseline"] = {"value": reps * n * w.K / tn, "unit": "draft tokens/s", "cores": th,
                                   "kind": "oracle", "sample": f"requests 0..{n - 1} of the same block "
-                                  f"({n * w.K} draft tokens), {reps} times", "seconds": tn}
-        log(f"oracle baseline: {n} requests x {reps} in {tn:.1f}s on {th} threads")
+                                  f"({n * w.K} draft tokens), {reps} times", "seconds": tn,
+                                  "cpu_model": cpu_model(),
+                                  "one_thread": {"value": w.K / t_one, "sample": f"request 0 ({w.K} draft tokens)",
+                                                 "seconds": t_one}}
+        log(f"oracle baseline: {n} requests x {reps} in {tn:.1f}s on {th} threads; "
+            f"one request on 1 thread in {t_one:.1f}s")
     print(json.dumps(result), flush=True)
 
 
@@ -644,14 +654,40 @@ def cpu_baseline(w, seed, conf, sps, ln, kv, q, logits, dr, target_s):
         e2, _ = run(n)
         el += e2
         reps += 1
+    nthreads = oracle.threads()
     log(f"oracle baseline: {n} requests, {rows} verify tokens x {reps} in {el:.1f}s "
-        f"on {oracle.threads()} threads")
-    return {"value": rows * reps / el, "unit": "verified tokens/s", "cores": oracle.threads(),
+        f"on {nthreads} threads")
+    # the same oracle on one thread, over a smaller sample (a few seconds)
+    oracle.set_threads(1)
+    try:
+        n1 = 1
+        el1, rows1 = run(n1)
+        while el1 < target_s / 8 and n1 < n:
+            n1 = min(n, max(n1 + 1, int(n1 * min(4.0, target_s / 6 / max(el1, 1e-3)))))
+            el1, rows1 = run(n1)
+    finally:
+        oracle.set_threads(nthreads)
+    log(f"oracle on 1 thread: {n1} requests, {rows1} verify tokens in {el1:.1f}s")
+    return {"value": rows * reps / el, "unit": "verified tokens/s", "cores": nthreads,
             "kind": "oracle",
             "sample": f"schedule over all {w.R} requests; attention + acceptance for requests "
                       f"0..{n - 1} ({rows} verify tokens, {int(kvk.kv_len[:n].sum())} context tokens)"
                       + (f", repeated {reps} times" if reps > 1 else ""),
-            "seconds": el}
+            "seconds": el,
+            "cpu_model": cpu_model(),
+            "one_thread": {"value": rows1 / el1, "sample": f"requests 0..{n1 - 1} ({rows1} verify tokens)",
+                           "seconds": el1}}
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 if __name__ == "__main__":

@@ -51,6 +51,8 @@ def _load():
         lib.oracle_rnn_draft.argtypes = [p, p, i32, i64, p, p, p, i32, p, p, i32, p, p, f64, i32,
                                          i32, i32, p, p, p, p]
         lib.oracle_threads.argtypes = []
+        lib.oracle_set_threads.argtypes = [i32]
+        lib.oracle_set_threads.restype = None
         for f in (lib.oracle_survival, lib.oracle_schedule, lib.oracle_verify_attn,
                   lib.oracle_accept, lib.oracle_markov_draft, lib.oracle_rnn_draft,
                   lib.oracle_threads):
@@ -78,6 +80,11 @@ def _check(rc: int, what: str) -> None:
 
 def threads() -> int:
     return int(_load().oracle_threads())
+
+
+def set_threads(n: int) -> None:
+    """OpenMP threads for the oracle's later calls (timing baselines)."""
+    _load().oracle_set_threads(int(n))
 
 
 def survival(conf: np.ndarray) -> np.ndarray:

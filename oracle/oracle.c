@@ -589,6 +589,15 @@ int oracle_rnn_draft(const int32_t* anchor, const void* U, int u_dtype, int64_t 
     return bad ? ORACLE_EINVAL : ORACLE_OK;
 }
 
+/* Sets how many OpenMP threads later parallel regions of the oracle use. */
+void oracle_set_threads(int n) {
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* Reports how many OpenMP threads a parallel region of the oracle uses. */
 int oracle_threads(void) {
     int n = 1;
