@@ -52,6 +52,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="time the steps as replays of one captured HIP graph per input copy "
+                         "instead of direct launches (--stage step; measured slower on this stack)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy 10 times (calibrates the HBM counters)")
     ap.add_argument("--traffic-from", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV",
@@ -363,11 +366,27 @@ def main():
     torch.cuda.synchronize()
     accepted = copies[0]["acc"].cpu().numpy()
 
+    # one captured step per input copy: a replay enqueues the whole step at once
+    graphs = []
+    if args.graph:
+        for c in range(NCOPY):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                step(copies[c])
+            graphs.append(g)
+        torch.cuda.synchronize()
+        for i in range(args.warmup):
+            graphs[i % NCOPY].replay()
+        torch.cuda.synchronize()
+
     # the timed region: exactly K steps and nothing else on the stream
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for i in range(args.steps):
-        step(copies[i % NCOPY])
+        if graphs:
+            graphs[i % NCOPY].replay()
+        else:
+            step(copies[i % NCOPY])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
     # per-stage times from a second, separate pass with events between the
@@ -423,6 +442,7 @@ def main():
         "attn_accept_hbm": {"bytes": ab + cb, "achieved_gbps": both_gbps,
                             "frac_of_peak": both_gbps / HBM_PEAK_GBPS},
         "emitted_tokens_per_s": float((accepted + 1).sum()) / (ms_per_step / 1e3),
+        "launch": "HIP graph replay (one captured step per input copy)" if args.graph else "direct launches",
         # the dominant kernel: one dspark_verify_attn call (plan, attention and
         # split-merge launches, bracketed together by the events)
         "roofline": roofline_entry(w.name, path, ab, af, attn_s),
