@@ -62,8 +62,8 @@ constexpr int kTileChunks = kStep * kRowChunks;     // 2304
 constexpr int kTileB = kTileChunks * 16;            // 36864 bytes
 constexpr int kInstr = kTileChunks / 64;            // 36 wave copy instructions per step
 constexpr int kCopies = kInstr / kWaves;            // 9 per wave: 8 whole rows
-constexpr int kSplit = 8192;                        // keys per split (the last one holds the rest)
-constexpr int kPageRegs = kSplit / 64 / DSPARK_WAVE;  // page-id registers per lane (pages >= 64 keys)
+constexpr int kSplit = 4096;                        // keys per split (the last one holds the rest)
+constexpr int kPageRegs = (kSplit / 64 + DSPARK_WAVE - 1) / DSPARK_WAVE;  // page-id registers per lane (pages >= 64 keys)
 constexpr int kKs = kDk / 32;                       // 18 slices of the score product
 constexpr int kDb = kDv / 16;                       // 32 blocks of output dims
 constexpr int kDbW = kDb / kWaves;                  // 8 blocks (128 dims) per wave
