@@ -183,7 +183,7 @@ dspark_status dspark_verify_attn(const void* q, const void* k_cache, const void*
  *             t < len_r the analytic acceptance probability
  *             sum_v min(p_t(v), p_d(v)) (one minus the total variation
  *             distance, the confidence head's training label); -1 for bonus
- *             rows.
+ *             rows and for rows that no request with len_r in 0..K owns.
  *   Limits: 1 <= V <= 2^20, ld >= V, 0 <= K <= 64, inv_temperature > 0.
  * ---------------------------------------------------------------------- */
 size_t dspark_accept_workspace_size(int R, int K, int V);

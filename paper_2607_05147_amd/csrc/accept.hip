@@ -251,10 +251,13 @@ __device__ __forceinline__ void chunk_stat(const float* x, int v0, int lane, flo
     }
 }
 
+// Stochastic mode also marks every row it covers as owned by no request
+// (RowInfo req = -1); resolve then claims the rows of the well-formed requests,
+// so rows that no well-formed request owns read as such in the rate pass.
 template <bool BF16, bool GREEDY, bool VEC>
 __global__ __launch_bounds__(kBlk) void acc_rowpass(
     const void* __restrict__ logits, int64_t ld, const int32_t* __restrict__ cu_q, int R, int V,
-    int max_rows, float scale2, ChunkStat* __restrict__ stats) {
+    int max_rows, float scale2, ChunkStat* __restrict__ stats, RowInfo* __restrict__ rows) {
     const int nch = n_chunks(V);
     const int items = clamp_rows(cu_q[R], max_rows) * nch;
     const int lane = threadIdx.x & (kLanes - 1);
@@ -276,6 +279,7 @@ __global__ __launch_bounds__(kBlk) void acc_rowpass(
             wc_load_slow<BF16>(row_of(i), v0, v1, lane, -__builtin_huge_valf(), x);
         }
         chunk_stat<BF16, GREEDY>(x, v0, lane, scale2, stats + i);
+        if (!GREEDY && lane == 0 && v0 == 0) rows[i / nch] = RowInfo{0.0f, 0.0f, -1, -1};
     };
     // each wave walks a contiguous range of (row, chunk) items, i.e. whole
     // stretches of logit rows, with the next chunk's loads in flight (two
@@ -817,7 +821,7 @@ static hipError_t launch_typed(const AcceptArgs& a, void* ws, hipStream_t s) {
         1, std::min<int64_t>((wave_items + kWaves - 1) / kWaves, resident_blocks(rowpass, cus)));
 #define DS_ROWPASS(G, VV)                                                                    \
     hipLaunchKernelGGL((acc_rowpass<BF16, G, VV>), dim3(pgrid), blk, 0, s, a.logits, a.ld, \
-                       a.cu_q, a.R, a.V, max_rows, scale2, w.stats)
+                       a.cu_q, a.R, a.V, max_rows, scale2, w.stats, w.rows)
     if (greedy) { if (vec) DS_ROWPASS(true, true); else DS_ROWPASS(true, false); }
     else { if (vec) DS_ROWPASS(false, true); else DS_ROWPASS(false, false); }
 #undef DS_ROWPASS

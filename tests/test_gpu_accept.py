@@ -111,6 +111,43 @@ def test_wide_vocabulary_rows_one_at_a_time():
     np.testing.assert_allclose(rate[:total][tested], rate_o[:total][tested], atol=2e-5)
 
 
+def test_malformed_request_with_rate():
+    """A request whose q_len exceeds K + 1 gets accepted_len = next_tok = -1
+    and rate -1 on its rows; the others are unaffected (requests are
+    independent), checked against the oracle on the unmodified batch."""
+    w = synth.scaled(synth.WORKLOADS["mid"], R=6, V=9000)
+    case = guard.build_case(w, 13, with_kv=False)
+    acc_o, nxt_o, _, rate_o = oracle.accept(case.drafts.draft_tok, case.drafts.draft_p, case.logits,
+                                            w.logit_dtype, case.cu_q, w.K, w.V, u=case.drafts.u,
+                                            want_rate=True)
+    bad = 2
+    ql = np.diff(case.cu_q).astype(np.int64)
+    ql_m = ql.copy()
+    ql_m[bad] = w.K + 2
+    cu_m = np.concatenate([[0], np.cumsum(ql_m)]).astype(np.int32)
+    rng = np.random.default_rng(5)
+    rows = []
+    for r in range(w.R):
+        if r == bad:
+            rows.append((rng.normal(size=(w.K + 2, w.V)) * 4).astype(case.logits.dtype))
+        else:
+            rows.append(case.logits[case.cu_q[r]:case.cu_q[r + 1]])
+    logits_m = np.concatenate(rows)
+    acc, nxt, rate = gpu_accept(w, case.drafts, logits_m, cu_m, want_rate=True)
+    assert acc[bad] == -1 and nxt[bad] == -1
+    assert (rate[cu_m[bad]:cu_m[bad + 1]] == -1).all()
+    ok = [r for r in range(w.R) if r != bad and r not in case.unguarded]
+    assert np.array_equal(acc[ok], acc_o[ok]) and np.array_equal(nxt[ok], nxt_o[ok])
+    for r in range(w.R):
+        if r == bad:
+            continue
+        got = rate[cu_m[r]:cu_m[r + 1]]
+        ref = rate_o[case.cu_q[r]:case.cu_q[r + 1]]
+        assert np.array_equal(got < 0, ref < 0)
+        np.testing.assert_allclose(got[ref >= 0], ref[ref >= 0], atol=2e-5)
+    log(f"[accept] malformed request {bad}: -1 everywhere; {len(ok)} others exact")
+
+
 def test_greedy_ties_and_rejections():
     rng = np.random.default_rng(8)
     R, K, V = 40, 4, 9000
