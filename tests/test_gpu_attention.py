@@ -211,3 +211,49 @@ def test_repeatable_bitwise():
     import torch
     assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
     assert torch.equal(l1.view(torch.int32), l2.view(torch.int32))
+
+
+@pytest.mark.parametrize("name", ["tiny", "mid", "mla"])
+def test_invalid_requests_left_unwritten(name):
+    """A request whose kv_len is shorter than its q_len, or longer than its
+    block table covers, is skipped: its output and LSE rows keep what was
+    there, and every other request is unaffected (generic, GQA and latent
+    paths)."""
+    import torch
+    from paper_2607_05147_amd import dspark
+    from gpu_helpers import to_dev
+    over = dict(R=4)
+    if name == "mla":
+        over = dict(R=3, kv_dist=("uniform", 5000, 12000))
+    w = synth.scaled(synth.WORKLOADS[name], **over)
+    q_len = [3, 2, 4, 1][: w.R]
+    cu = oracle.cu_from_len(np.asarray(q_len) - 1)
+    kv = synth.paged_kv(w, 21)
+    q = synth.query_rows(w, 21, synth.flat_keys(np.diff(cu)))
+    ref, ref_lse = oracle.verify_attn(q, kv.k, kv.v, kv.k_strides, kv.v_strides, kv.block_table,
+                                      kv.kv_len, cu, w.Hq, w.Hkv, w.Dqk, w.Dv, w.page, w.scale,
+                                      w.dtype)
+    bf16 = w.dtype == "bf16"
+    dkv = DevKV(kv, bf16)
+    kv_bad = kv.kv_len.copy()
+    kv_bad[0] = q_len[0] - 1                                 # fewer keys than verify tokens
+    kv_bad[2] = kv.block_table.shape[1] * w.page + 1         # beyond the block table
+    dkv.kv_len = to_dev(kv_bad)
+    qd = to_dev(q, bf16)
+    sentinel = 7.0
+    out = torch.full((q.shape[0], w.Hq, w.Dv), sentinel, dtype=qd.dtype, device=qd.device)
+    lse = torch.full((q.shape[0], w.Hq), sentinel, dtype=torch.float32, device=qd.device)
+    dspark.dspark_verify_attn(qd, dkv.k, dkv.v, dkv.ks, dkv.vs, dkv.bt, dkv.kv_len, to_dev(cu),
+                              w.max_q, w.Hkv, w.Dv, w.page, w.scale, out=out, lse=lse)
+    torch.cuda.synchronize()
+    o, l = to_f64(out), to_f64(lse)
+    for r in range(w.R):
+        rows = slice(cu[r], cu[r + 1])
+        if r in (0, 2):
+            assert (o[rows] == sentinel).all() and (l[rows] == sentinel).all(), r
+        else:
+            err = row_rel_err(o[rows], ref[rows])
+            assert err.max() <= TOL[w.dtype], (r, err.max())
+            np.testing.assert_allclose(l[rows], ref_lse[rows], rtol=0,
+                                       atol=1e-4 if bf16 else 1e-5)
+    log(f"[attn] invalid requests skipped: {name} R={w.R}, requests 0 and 2 untouched")
