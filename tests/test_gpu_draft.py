@@ -119,3 +119,15 @@ def test_draft_full_size_sampled():
     assert ((tok >= 0) & (tok < w.V)).all().item()
     c = conf.cpu().numpy()
     assert ((c > 0) & (c < 1)).all()
+
+
+@pytest.mark.parametrize("R,K,V", [(1, 1, 700), (3, 1, 129), (2, 5, 5), (2, 3, 1), (2, 64, 300)])
+def test_draft_degenerate_shapes(R, K, V):
+    # one request; one position (no next embedding to gather); a vocabulary
+    # smaller than one tile, down to a single token; the longest block
+    w = synth.scaled(synth.WORKLOADS["serving"], R=R, K=K, V=V)
+    case = guard.draft_case(w, 8, rank=64, d=16)
+    tok, p, conf = _run_gpu(w, case, 64, 16)
+    _compare(w, case, tok, p, conf, f"R={R} K={K} V={V}")
+    if V == 1:
+        assert (tok == 0).all().item() and torch.equal(p, torch.ones_like(p))

@@ -139,3 +139,15 @@ def test_rnn_draft_full_size_sampled():
     tok, p, conf = _run_gpu(w, case, 4096)
     _compare(w, case, tok, p, conf, "full size")
     assert ((tok >= 0) & (tok < w.V)).all().item()
+
+
+@pytest.mark.parametrize("R,K,V", [(1, 1, 700), (2, 5, 5), (2, 3, 1), (2, 64, 300)])
+def test_rnn_draft_degenerate_shapes(R, K, V):
+    # one request; one position; a vocabulary smaller than one tile, down to
+    # a single token; the longest block (64 state updates)
+    w = synth.scaled(synth.WORKLOADS["serving"], R=R, K=K, V=V)
+    case = guard.draft_case(w, 9, rank=64, d=16, head="rnn")
+    tok, p, conf = _run_gpu(w, case, 16)
+    _compare(w, case, tok, p, conf, f"R={R} K={K} V={V}")
+    if V == 1:
+        assert (tok == 0).all().item() and torch.equal(p, torch.ones_like(p))
