@@ -158,7 +158,8 @@ dspark_status dspark_verify_attn(const void* q, const void* k_cache, const void*
  *   draft_tok [R, K] int32: draft token for verify slot t+1 (the paper's
  *             x_{t+1}); values outside [0, V) are read as rejected.
  *   draft_p   [R, K, V] fp32 (nullable): draft distribution p_d for slot t+1,
- *             used as given (not renormalised).
+ *             used as given (not renormalised); with K = 0 it may be NULL in
+ *             stochastic mode too (u alone selects it).
  *   logits    target logits, row cu_q[r] + t (row stride `ld` elements) is the
  *             target distribution for the token after verify slot t:
  *             rows t < len_r test draft_tok[r, t]; row len_r gives the bonus.

@@ -218,8 +218,9 @@ dspark_status dspark_accept(const int32_t* draft_tok, const float* draft_p, cons
         return fail(DSPARK_EINVAL, "inv_temperature must be positive and finite");
     if (!logits || !cu_q || !accepted_len || !next_tok || (K > 0 && !draft_tok))
         return fail(DSPARK_EINVAL, "null argument");
+    // (with K = 0 there is no draft distribution to give: draft_p may be null)
     const bool greedy = draft_p == nullptr && u == nullptr;
-    if (!greedy && (draft_p == nullptr || u == nullptr))
+    if (!greedy && (u == nullptr || (K > 0 && draft_p == nullptr)))
         return fail(DSPARK_EINVAL, "draft_p and u must both be given (stochastic) or both null");
     if (greedy && accept_rate)
         return fail(DSPARK_EINVAL, "accept_rate needs draft distributions (stochastic mode)");

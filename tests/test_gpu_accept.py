@@ -211,3 +211,31 @@ def test_repeatable():
     a1 = gpu_accept(case.w, case.drafts, case.logits, case.cu_q)
     a2 = gpu_accept(case.w, case.drafts, case.logits, case.cu_q)
     assert all(np.array_equal(x, y) for x, y in zip(a1[:2], a2[:2]))
+
+
+@pytest.mark.parametrize("K,V,greedy", [(0, 1000, False), (0, 1000, True), (4, 1, False),
+                                        (4, 1, True)])
+def test_degenerate_shapes(K, V, greedy):
+    """K = 0 (no drafts: the bonus draw only) and a single-token vocabulary
+    (every draft is accepted and the emitted token is 0)."""
+    rng = np.random.default_rng(17 + K + V)
+    R = 5
+    ln = rng.integers(0, K + 1, size=R)
+    cu = oracle.cu_from_len(ln)
+    z = (rng.normal(size=(int(cu[-1]), V)) * 3).astype(np.float32)
+    tok = rng.integers(0, V, size=(R, K)).astype(np.int32)
+    if greedy:
+        dr = synth.Drafts(tok, None, None)
+    else:
+        dp = rng.dirichlet(np.ones(V), size=(R, K)).astype(np.float32).reshape(R, K, V)
+        u = (rng.random((R, K + 1)) * 0.999).astype(np.float32)
+        dr = synth.Drafts(tok, dp, u)
+    w = synth.scaled(synth.WORKLOADS["mid"], R=R, K=K, V=V, greedy=greedy)
+    acc, nxt, _ = gpu_accept(w, dr, z, cu)
+    acc_o, nxt_o, mg, _ = oracle.accept(tok, dr.draft_p, z, "f32", cu, K, V, u=dr.u)
+    ok = np.ones(R, bool) if greedy else mg >= guard.ACCEPT_GUARD
+    log(f"[accept] K={K} V={V} greedy={greedy}: {ok.sum()} of {R} guarded")
+    assert np.array_equal(acc, acc_o)
+    assert np.array_equal(nxt[ok], nxt_o[ok])
+    if V == 1:
+        assert (acc == ln).all() and (nxt == 0).all()
