@@ -257,3 +257,30 @@ def test_invalid_requests_left_unwritten(name):
             np.testing.assert_allclose(l[rows], ref_lse[rows], rtol=0,
                                        atol=1e-4 if bf16 else 1e-5)
     log(f"[attn] invalid requests skipped: {name} R={w.R}, requests 0 and 2 untouched")
+
+
+@pytest.mark.parametrize("name,Hq,Hkv,q_len,kv_len", [
+    # one query head per KV head; every context exactly its verify block (the
+    # first query sees a single key)
+    ("mid", 8, 8, [1, 2, 5], [1, 2, 5]),
+    # contexts one key past a page, and one key past a 4096-key split
+    ("mid", 32, 8, [1, 3, 17], [64, 65, 4097]),
+    # latent: a single key; one key past a split
+    ("mla", 128, 1, [1, 2], [1, 4097]),
+])
+def test_edge_context_lengths(name, Hq, Hkv, q_len, kv_len):
+    w = synth.scaled(synth.WORKLOADS[name], R=len(q_len), Hq=Hq, Hkv=Hkv)
+    cu = oracle.cu_from_len(np.asarray(q_len) - 1)
+    kv = synth.paged_kv(w, 31, kv_len=np.asarray(kv_len, np.int32))
+    q = synth.query_rows(w, 31, synth.flat_keys(np.diff(cu)))
+    ref, ref_lse = oracle.verify_attn(q, kv.k, kv.v, kv.k_strides, kv.v_strides, kv.block_table,
+                                      kv.kv_len, cu, w.Hq, w.Hkv, w.Dqk, w.Dv, w.page, w.scale,
+                                      w.dtype)
+    out, lse = gpu_attention(w, DevKV(kv, w.dtype == "bf16"), q, cu)
+    o = to_f64(out)
+    assert np.isfinite(o).all()
+    err = row_rel_err(o, ref)
+    log(f"[attn] edge lengths {name} Hq={Hq}/{Hkv} q_len={q_len} kv={kv_len}: "
+        f"max row rel err {err.max():.3g}")
+    assert err.max() <= TOL[w.dtype]
+    np.testing.assert_allclose(to_f64(lse), ref_lse, rtol=0, atol=1e-4)
