@@ -36,9 +36,15 @@ def build(force: bool = True) -> str:
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-            build(force=True)
-        lib = C.CDLL(_LIB)
+        # ORACLE_LIB: a prebuilt copy to load instead (the planted-mistake
+        # tests compile mutated copies of oracle.c and run the pins on them)
+        override = os.environ.get("ORACLE_LIB")
+        if override:
+            lib = C.CDLL(override)
+        else:
+            if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+                build(force=True)
+            lib = C.CDLL(_LIB)
         p = C.c_void_p
         i32, i64, f64 = C.c_int, C.c_int64, C.c_double
         lib.oracle_survival.argtypes = [p, i32, i32, p]

@@ -263,3 +263,37 @@ def test_bf16_logits_widen_exactly():
     r1 = oracle.accept(tok, dp, zb, "bf16", cu, L, V, u=u)
     r2 = oracle.accept(tok, dp, zw, "f32", cu, L, V, u=u)
     assert all(np.array_equal(a, b) for a, b in zip(r1[:3], r2[:3]))
+
+
+def test_draw_exactly_at_a_bucket_edge_takes_the_next_bucket():
+    # a draw is the smallest token whose running mass EXCEEDS u * total: on a
+    # uniform distribution of four tokens u = 0.25 lands exactly on the edge of
+    # token 0 and gives token 1; a token without mass is never drawn, even at u = 0
+    V = 4
+    u = np.array([[0.0], [0.25], [0.5], [0.75]], np.float32)
+    N = u.shape[0]
+    cu = np.arange(N + 1, dtype=np.int32)
+    dp = np.zeros((N, 0, V), np.float32)
+    tok = np.zeros((N, 0), np.int32)
+    z = np.zeros((N, V), np.float32)
+    _, nxt, _, _ = oracle.accept(tok, dp, z, "f32", cu, 0, V, u=u)
+    assert nxt.tolist() == [0, 1, 2, 3]
+    z[:, 0] = -np.inf  # p = (0, 1/3, 1/3, 1/3)
+    _, nxt, _, _ = oracle.accept(tok, dp, z, "f32", cu, 0, V, u=u)
+    assert nxt[0] == 1
+
+
+def test_bonus_after_all_accepted_comes_from_row_l():
+    # rows concentrated on different tokens, drafts equal to the target: every
+    # draft is accepted and the emitted token is drawn from row l, not l - 1
+    V, L = 8, 3
+    z = np.zeros((L + 1, V), np.float32)
+    for t in range(L + 1):
+        z[t, (t + 4) % V] = 30.0
+    p = softmax(z.astype(np.float64), axis=1).astype(np.float32)
+    tok = np.array([[(t + 4) % V for t in range(L)]], np.int32)
+    u = np.full((1, L + 1), 0.5, np.float32)
+    cu = np.array([0, L + 1], np.int32)
+    acc, nxt, _, _ = oracle.accept(tok, p[None, :L], z, "f32", cu, L, V, u=u)
+    assert acc[0] == L
+    assert nxt[0] == (L + 4) % V

@@ -188,3 +188,28 @@ def test_requests_are_independent():
     np.testing.assert_array_equal(p2, p[perm])
     np.testing.assert_array_equal(c2, c[perm])
     np.testing.assert_allclose(p.sum(axis=-1), 1.0, rtol=1e-13)
+
+
+def test_inverse_temperature_scales_base_logits_and_bias():
+    # the temperature divides the whole logit U_k + B_k: halving both U and
+    # the projection (exact, powers of two in fp32 and bf16) at temperature 1
+    # must give bit for bit what inverse temperature 0.5 gives on the originals
+    rng = np.random.default_rng(11)
+    R, K, V, rank = 3, 4, 60, 8
+    W1, W2t = _weights(rng, V, rank)
+    U = (4 * rng.normal(size=(R * K, V))).astype(np.float32)
+    u = rng.random((R, K)).astype(np.float32)
+    anchor = rng.integers(0, V, R)
+    wc = (rng.normal(size=rank) * 0.1).astype(np.float32)
+    tok_a, p_a, c_a, _ = oracle.markov_draft(anchor, U, "f32", W1, W2t, wc, u, K, V,
+                                             inv_temperature=0.5)
+    W2h = bf16((synth.bf16_bits_to_f32(W2t) * np.float32(0.5)).astype(np.float32))
+    assert np.array_equal(synth.bf16_bits_to_f32(W2h) * 2, synth.bf16_bits_to_f32(W2t))
+    tok_b, p_b, c_b, _ = oracle.markov_draft(anchor, U * np.float32(0.5), "f32", W1, W2h, wc, u,
+                                             K, V, inv_temperature=1.0)
+    np.testing.assert_array_equal(tok_a, tok_b)
+    np.testing.assert_array_equal(p_a, p_b)
+    np.testing.assert_array_equal(c_a, c_b)
+    # and the temperature matters: at 1.0 on the originals the distributions differ
+    _, p_c, _, _ = oracle.markov_draft(anchor, U, "f32", W1, W2t, wc, u, K, V)
+    assert np.abs(p_c - p_a).max() > 1e-3
