@@ -36,6 +36,11 @@ MUTANTS = {
     "schedule: exclusive survival product": (SCHED,
         "            p = p * c;\n            a[(int64_t)r * K + j] = p;",
         "            a[(int64_t)r * K + j] = p;\n            p = p * c;"),
+    "schedule: mode 1 stops at the first loss as well": (SCHED,
+        "        } else if (mode == 0) {\n            break;", "        } else {\n            break;"),
+    "schedule: snapshot of the admitted request only": (SCHED,
+        "            for (int r = 0; r < R; ++r) len[r] = l[r]; /* snapshot l* <- l */",
+        "            len[E[i].r] = E[i].j;"),
     # ---- verify attention
     "attention: causal limit one key short": (ATTN,
         "        int64_t visible = (int64_t)kv_len[r] - ql + t + 1;",
@@ -67,6 +72,13 @@ MUTANTS = {
         "ar += p[v] > (double)pd[v] ? p[v] : (double)pd[v];"),
     "accept: inverse CDF takes the bucket edge": (ACC,
         "        if (cum > thr) {", "        if (cum >= thr) {"),
+    "accept: test reads the next uniform": (ACC,
+        "                double uu = (double)u[(int64_t)r * (K + 1) + t];",
+        "                double uu = (double)u[(int64_t)r * (K + 1) + t + 1];"),
+    "accept: greedy rejection emits the bonus row's argmax": (ACC,
+        "                if (draft_tok[(int64_t)r * K + t] != am) { acc = t; tok = am; break; }",
+        "                if (draft_tok[(int64_t)r * K + t] != am) { acc = t; tok = argmax_row("
+        "base + (size_t)(cu_q[r] + l) * (size_t)ld * esz, logit_dtype, V); break; }"),
     # ---- Markov-head draft block
     "draft: embedding does not follow the draws": (DRAFT,
         "            prev = x;\n        }\n        free(z);\n        free(e);",

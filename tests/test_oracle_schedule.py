@@ -203,3 +203,18 @@ def test_workload_schedules_are_sane(name):
     assert np.all((ln0 >= 0) & (ln0 <= w.K))
     assert th1 >= th0  # the global search never does worse along the same path
     assert th0 > w.R * sps[w.R] or ln0.sum() == 0
+
+
+def test_mode1_keeps_every_candidate_before_its_best_point():
+    # two requests, one candidate each: admitting the first lowers Theta
+    # (2.9 * 0.6 = 1.74 < 2.0), admitting the second raises it past the start
+    # (3.7 * 0.6 = 2.22).  Mode 1 takes the best prefix of the path, so both
+    # requests get their candidate; mode 0 stops at the first loss.
+    conf = np.array([[0.9], [0.8]], np.float32)
+    sps = np.array([0.0, 0.0, 1.0, 0.6, 0.6])
+    ln1, th1, n1, _ = oracle.schedule(conf, sps, 1)
+    a = conf.astype(np.float64)[:, 0]
+    assert ln1.tolist() == [1, 1] and n1 == 2
+    assert th1 == pytest.approx((2 + a[0] + a[1]) * 0.6, rel=1e-15)
+    ln0, th0, n0, _ = oracle.schedule(conf, sps, 0)
+    assert ln0.tolist() == [0, 0] and n0 == 0 and th0 == 2.0
