@@ -82,3 +82,13 @@ def test_sizes(R, K):
         if not case.sched_guarded:
             pytest.skip("no guarded draw")
         _check(case.conf, case.sps, mode, f"R{R}K{K}")
+
+
+def test_mode1_keeps_the_prefix_before_its_best_point():
+    # the first admission loses throughput, the second gains past the start:
+    # mode 1 admits both requests, mode 0 neither (the oracle's pin, on the GPU)
+    conf = np.array([[0.9], [0.8]], np.float32)
+    sps = np.array([0.0, 0.0, 1.0, 0.6, 0.6])
+    assert gpu_schedule(conf, sps, 1)[0].tolist() == [1, 1]
+    assert gpu_schedule(conf, sps, 0)[0].tolist() == [0, 0]
+    _check(conf, sps, 1, "dip then gain")
