@@ -462,11 +462,16 @@ __global__ __launch_bounds__(kThreads) void md_stats(MarkovArgs a, const float2*
     const float2* st = stats + (int64_t)r * ntiles;
     const int per = ceil_div(ntiles, kThreads);  // a contiguous run of tiles per thread
     const int t0 = tid * per;
+    // the uniform and every tile of the run are loaded up front (clamped
+    // indices, then masked: no load waits behind a branch)
+    const float uu = a.u[(int64_t)r * a.K + (k - 1)];
     float2 x[kStatsPer];
+#pragma unroll
+    for (int i = 0; i < kStatsPer; ++i) x[i] = st[min(t0 + i, ntiles - 1)];
     float m = -__builtin_huge_valf();
 #pragma unroll
     for (int i = 0; i < kStatsPer; ++i) {
-        x[i] = i < per && t0 + i < ntiles ? st[t0 + i] : float2{-__builtin_huge_valf(), 0.0f};
+        if (!(i < per && t0 + i < ntiles)) x[i] = float2{-__builtin_huge_valf(), 0.0f};
         m = fmaxf(m, x[i].x);
     }
     const float M = block_max(m, s_f);
@@ -480,7 +485,7 @@ __global__ __launch_bounds__(kThreads) void md_stats(MarkovArgs a, const float2*
     }
     double total;
     const double incl = block_scan(loc, s_d, &total);
-    const double thr = (double)a.u[(int64_t)r * a.K + (k - 1)] * total;
+    const double thr = (double)uu * total;
     if (tid == 0) {
         s_pick = kThreads;
         s_last = -1;
