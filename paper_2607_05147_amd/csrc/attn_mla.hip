@@ -774,9 +774,16 @@ __global__ __launch_bounds__(256) void mla_merge(Params p) {
     const AttnArgs& a = p.a;
     const int count = p.head[3 * kQueues];
     const int tid = threadIdx.x;
+    // the first item's entries are loaded together with the count: the list
+    // has room for at least gridDim.x items (the launch caps the grid at its
+    // capacity), and entries past the count are never used
+    int4 e0 = p.mlist[2 * blockIdx.x];
+    int4 e1 = p.mlist[2 * blockIdx.x + 1];
     for (int m = blockIdx.x; m < count; m += gridDim.x) {
-        const int4 e0 = p.mlist[2 * m];
-        const int4 e1 = p.mlist[2 * m + 1];
+        if (m != (int)blockIdx.x) {
+            e0 = p.mlist[2 * m];
+            e1 = p.mlist[2 * m + 1];
+        }
         const int r = e0.x, g = e0.y, rb = e0.z;
         const int q0 = e1.x, ql = e1.y, ns = e1.w;
         const int rows = ql * p.group;
