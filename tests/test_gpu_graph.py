@@ -21,17 +21,18 @@ pytestmark = pytest.mark.gpu
 CASES = {
     # GQA with several splits per context and stochastic acceptance
     "serving": dict(R=8, kv_dist=("uniform", 5000, 13000)),
-    # latent attention (V aliases K) with several 8192-key splits
+    # latent attention (V aliases K) with several 4096-key splits
     "mla": dict(R=2, kv_dist=("uniform", 9000, 20000)),
     # greedy acceptance
     "highconc": dict(R=24, kv_dist=("uniform", 600, 3000)),
 }
 
 
-@pytest.mark.parametrize("name", sorted(CASES))
-def test_verify_step_graph_replays(name):
+def _step_setup(name, seed=3):
+    """Device inputs, outputs and workspaces of one verify step, and a closure
+    that enqueues it on the current stream."""
     w = synth.scaled(synth.WORKLOADS[name], **CASES[name])
-    case = guard.build_case(w, 3)
+    case = guard.build_case(w, seed)
     bf16 = w.dtype == "bf16"
     dkv = DevKV(case.kv, bf16)
     dev = torch.device("cuda:0")
@@ -60,9 +61,15 @@ def test_verify_step_graph_replays(name):
         dspark.dspark_accept(tok, logits, cu, draft_p=dp, u=u, accepted_len=acc, next_tok=nxt,
                              ws=ws_c)
 
+    return w, case, q, step, (ln, cu, out, acc, nxt)
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_verify_step_graph_replays(name):
+    w, case, q, step, outs = _step_setup(name)
+    dev = q.device
     step()
     torch.cuda.synchronize()
-    outs = (ln, cu, out, acc, nxt)
     ref = [t.clone() for t in outs]
     assert np.array_equal(ref[1].cpu().numpy(), case.cu_q)
 
@@ -78,5 +85,32 @@ def test_verify_step_graph_replays(name):
         g.replay()
         torch.cuda.synchronize()
         same = [torch.equal(t, r) for t, r in zip(outs, ref)]
-        log(f"[graph] {name} R={R} rows={q.shape[0]} replay {rep}: identical {same} ({y:.1f})")
+        log(f"[graph] {name} R={w.R} rows={q.shape[0]} replay {rep}: identical {same} ({y:.1f})")
         assert all(same)
+
+
+def test_two_steps_on_two_streams_at_once():
+    # the library keeps no state between calls: two steps with their own
+    # buffers, enqueued on two streams at the same time (default priority),
+    # give what each gives alone
+    a = _step_setup("serving", 3)
+    b = _step_setup("mla", 4)
+    refs = []
+    for _, _, _, step, outs in (a, b):
+        step()
+        torch.cuda.synchronize()
+        refs.append([t.clone() for t in outs])
+    for rep in range(3):
+        for _, _, _, _, outs in (a, b):
+            for t in outs:
+                t.zero_()
+        torch.cuda.synchronize()
+        s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+        with torch.cuda.stream(s1):
+            a[3]()
+        with torch.cuda.stream(s2):
+            b[3]()
+        torch.cuda.synchronize()
+        same = [[torch.equal(t, r) for t, r in zip(x[4], ref)] for x, ref in zip((a, b), refs)]
+        log(f"[streams] rep {rep}: identical {same}")
+        assert all(all(v) for v in same)
