@@ -137,6 +137,9 @@ def test_accept_validation(L):
     assert _acc(L, it=0.0) == EINVAL
     assert _acc(L, it=float("inf")) == EINVAL
     assert _acc(L, dp=None) == EINVAL  # u without draft_p
+    # with K = 0 there is no draft distribution: u alone selects stochastic
+    # mode (the call gets as far as the workspace check)
+    assert _acc(L, K=0, tok=None, dp=None, ws_bytes=8) == EWORKSPACE
     assert _acc(L, u=None) == EINVAL
     assert _acc(L, dp=None, u=None, rate=FAKE) == EINVAL  # rate needs stochastic mode
     assert _acc(L, logits=None) == EINVAL
