@@ -675,6 +675,21 @@ __global__ __launch_bounds__(kThreads) void rnn_state(MarkovArgs a, const float*
             bfr[slot][p] = *(const bf16x8*)(a.Wrnn + (int64_t)(p * rank + j0 + lr) * nz + col);
     };
     const int nmine = st0 < nst ? (nst - st0 + kWaves - 1) / kWaves : 0;
+    // wave 0's epilogue inputs (the projection of the hidden states and the
+    // previous state of its requests m0 + 4 lq + e, dim j0 + lr) do not depend
+    // on the products: they are loaded first (rows clamped, then masked)
+    const int j = j0 + lr;
+    float hpv[4][3], spv[4];
+    if (wave == 0) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int rc = min(m0 + 4 * lq + e, a.R - 1);
+            const float* hp = Hp ? Hp + ((int64_t)rc * a.K + (k - 1)) * (3 * rank) : nullptr;
+#pragma unroll
+            for (int p = 0; p < 3; ++p) hpv[e][p] = hp ? hp[p * rank + j] : 0.0f;
+            spv[e] = k > 1 ? s_prev[(int64_t)rc * rank + j] : 0.0f;
+        }
+    }
     f32x4 acc[3];
 #pragma unroll
     for (int p = 0; p < 3; ++p) acc[p] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -702,20 +717,18 @@ __global__ __launch_bounds__(kThreads) void rnn_state(MarkovArgs a, const float*
 #pragma unroll
         for (int p = 0; p < 3; ++p) acc[p] += part[w][p][lane];
     // lane holds requests m0 + 4 lq + e, state dim j0 + lr
-    const int j = j0 + lr;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
         const int r = m0 + 4 * lq + e;
         if (r >= a.R) continue;
         float ag = acc[0][e], ac = acc[1][e], ao = acc[2][e];
         if (Hp) {
-            const float* hp = Hp + ((int64_t)r * a.K + (k - 1)) * (3 * rank);
-            ag += hp[j];
-            ac += hp[rank + j];
-            ao += hp[2 * rank + j];
+            ag += hpv[e][0];
+            ac += hpv[e][1];
+            ao += hpv[e][2];
         }
         const float g = 1.0f / (1.0f + expf(-ag));
-        const float sp = k > 1 ? s_prev[(int64_t)r * rank + j] : 0.0f;
+        const float sp = spv[e];
         const float sn = g * sp + (1.0f - g) * tanhf(ac);
         s_next[(int64_t)r * rank + j] = sn;
         split3(sn, S3_next + (int64_t)r * 3 * rank + j, rank);
