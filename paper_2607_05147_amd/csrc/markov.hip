@@ -288,6 +288,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 
                 }
             }
         }
+        // (drawing pass) the chunk's row statistics, needed only after the
+        // products, are in flight with the other loads
+        RowInfo ri_c[PASS == 1 ? kRT : 1];
+        if (PASS == 1) {
+#pragma unroll
+            for (int rt = 0; rt < kRT; ++rt) ri_c[rt] = info[min(c0 + 16 * rt + lr, a.R - 1)];
+        }
         lds_barrier();  // the previous chunk's LDS reads are done (global loads stay in flight)
         // (no guard when the copy divides evenly: a branch here would make the
         // stores wait for the base logits as well)
@@ -355,7 +362,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 
                 s = quad_sum(s);
                 if (lq == 0) sst[wave][16 * rt + lr] = float2{m, s};
             } else {
-                const RowInfo ri = info[rok ? r : 0];
+                const RowInfo ri = ri_c[PASS == 1 ? rt : 0];
                 const float inv = 1.0f / ri.S;
                 float q[kVT][4];
 #pragma unroll
