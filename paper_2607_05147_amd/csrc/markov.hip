@@ -12,7 +12,7 @@
 //   md_tile<0>  one workgroup per 128 vocabulary entries: W2^T e for every
 //               request on v_mfma_f32_16x16x32_bf16 (the tile's W2t rows stay
 //               in registers as A operands, the embeddings stream through LDS
-//               in chunks of 64 requests as B operands), plus the base logits;
+//               in chunks of 32 requests as B operands), plus the base logits;
 //               then the tile's softmax statistics (max, sum of exp) per request;
 //   md_stats    one wave per request: the row's max and total and the tile in
 //               which the running mass passes u * total (fp64 prefix over the
@@ -55,52 +55,6 @@ __host__ __device__ constexpr int ceil_div(int a, int b) { return (a + b - 1) / 
 __device__ __forceinline__ int eslot(int t, int c, int nch) {
     const int f = (t & 1) | (((t >> 2) & 1) << 1) | (((t >> 1) & 1) << 2) | (((t >> 3) & 1) << 3);
     return c ^ (f & (nch - 1));
-}
-
-__device__ __forceinline__ float block_sum(float v, float* s) {
-    v = wave_sum(v);
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    __syncthreads();
-    if (lane == 0) s[wave] = v;
-    __syncthreads();
-    float t = 0.0f;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) t += s[w];
-    return t;
-}
-
-__device__ __forceinline__ float block_max(float v, float* s) {
-    v = wave_max(v);
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    __syncthreads();
-    if (lane == 0) s[wave] = v;
-    __syncthreads();
-    float t = -__builtin_huge_valf();
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) t = fmaxf(t, s[w]);
-    return t;
-}
-
-// Inclusive prefix sum over the block in thread order (fp64); *total gets the sum.
-__device__ __forceinline__ double block_scan(double v, double* s, double* total) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    double incl = v;
-#pragma unroll
-    for (int o = 1; o < DSPARK_WAVE; o <<= 1) {
-        const double t = __shfl_up(incl, o, DSPARK_WAVE);
-        if (lane >= o) incl += t;
-    }
-    __syncthreads();
-    if (lane == DSPARK_WAVE - 1) s[wave] = incl;
-    __syncthreads();
-    double before = 0.0, all = 0.0;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-        if (w < wave) before += s[w];
-        all += s[w];
-    }
-    *total = all;
-    return before + incl;
 }
 
 // token of position k - 1 (the anchor for k = 1); -1 when it is not a valid token
@@ -455,82 +409,94 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 
 
 // ---------------------------------------------------------------- md_stats
 
-// Per request (one workgroup): the row maximum and total from the tile
-// statistics (tile masses in fp64), and the tile in which the running mass
-// passes u * total, scanning the tiles in vocabulary order.
-constexpr int kStatsPer = 8;  // tiles per thread (up to 2048 tiles: V <= 262144)
-__global__ __launch_bounds__(kThreads) void md_stats(MarkovArgs a, const float2* stats, RowInfo* info,
-                                                     int ntiles, int k) {
-    __shared__ float s_f[kWaves];
-    __shared__ double s_d[kWaves];
-    __shared__ int s_pick, s_last;
+// Per request (one wave): the row maximum and total from the tile statistics
+// (tile masses in fp64), and the tile in which the running mass passes
+// u * total, scanning the tiles in vocabulary order.  Lane l takes the
+// contiguous run of tiles l * per .. l * per + per - 1, so the lane order is
+// the vocabulary order; the reductions are lane shuffles, with no barrier.
+constexpr int kStatsMaxPer = 32;  // tiles per lane (up to 2048 tiles: V <= 262144)
+template <int P>
+__global__ __launch_bounds__(DSPARK_WAVE) void md_stats(MarkovArgs a, const float2* stats, RowInfo* info,
+                                                        int ntiles, int k) {
     const int r = blockIdx.x;
-    const int tid = threadIdx.x;
+    const int lane = threadIdx.x;
     const float2* st = stats + (int64_t)r * ntiles;
-    const int per = ceil_div(ntiles, kThreads);  // a contiguous run of tiles per thread
-    const int t0 = tid * per;
+    const int per = ceil_div(ntiles, DSPARK_WAVE);
+    const int t0 = lane * per;
     // the uniform and every tile of the run are loaded up front (clamped
     // indices, then masked: no load waits behind a branch)
     const float uu = a.u[(int64_t)r * a.K + (k - 1)];
-    float2 x[kStatsPer];
+    float2 x[P];
 #pragma unroll
-    for (int i = 0; i < kStatsPer; ++i) x[i] = st[min(t0 + i, ntiles - 1)];
+    for (int i = 0; i < P; ++i) x[i] = st[min(t0 + i, ntiles - 1)];
     float m = -__builtin_huge_valf();
 #pragma unroll
-    for (int i = 0; i < kStatsPer; ++i) {
+    for (int i = 0; i < P; ++i) {
         if (!(i < per && t0 + i < ntiles)) x[i] = float2{-__builtin_huge_valf(), 0.0f};
         m = fmaxf(m, x[i].x);
     }
-    const float M = block_max(m, s_f);
-    double w[kStatsPer], loc = 0.0;
+    const float M = wave_max(m);
+    double w[P], loc = 0.0;
     int lastpos = -1;
 #pragma unroll
-    for (int i = 0; i < kStatsPer; ++i) {
+    for (int i = 0; i < P; ++i) {
         w[i] = x[i].x > -__builtin_huge_valf() ? (double)x[i].y * (double)exp2f(x[i].x - M) : 0.0;
         loc += w[i];
         if (w[i] > 0.0) lastpos = t0 + i;
     }
-    double total;
-    const double incl = block_scan(loc, s_d, &total);
-    const double thr = (double)uu * total;
-    if (tid == 0) {
-        s_pick = kThreads;
-        s_last = -1;
+    double incl = loc;  // inclusive prefix over the lanes
+#pragma unroll
+    for (int o = 1; o < DSPARK_WAVE; o <<= 1) {
+        const double t = __shfl_up(incl, o, DSPARK_WAVE);
+        if (lane >= o) incl += t;
     }
-    __syncthreads();
-    if (incl > thr && loc > 0.0) atomicMin(&s_pick, tid);
-    if (lastpos >= 0) atomicMax(&s_last, lastpos);
-    __syncthreads();
+    const double total = __shfl(incl, DSPARK_WAVE - 1, DSPARK_WAVE);
+    const double thr = (double)uu * total;
+    int last = lastpos;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) last = max(last, __shfl_xor(last, o, DSPARK_WAVE));
+    // the first lane whose run holds the crossing
+    const uint64_t hit = __builtin_amdgcn_ballot_w64(incl > thr && loc > 0.0);
     RowInfo ri;
     ri.M = M;
     ri.S = (float)total;
     ri.pad = 0;
-    if (tid == s_pick) {
-        double cum = incl - loc;
-        int pick = -1;
-        double before = 0.0;
+    if (hit != 0) {
+        if (lane == __builtin_ctzll(hit)) {
+            double cum = incl - loc;
+            int pick = -1;
+            double before = 0.0;
 #pragma unroll
-        for (int i = 0; i < kStatsPer; ++i) {
-            if (pick < 0 && w[i] > 0.0 && cum + w[i] > thr) {
-                pick = t0 + i;
-                before = cum;
+            for (int i = 0; i < P; ++i) {
+                if (pick < 0 && w[i] > 0.0 && cum + w[i] > thr) {
+                    pick = t0 + i;
+                    before = cum;
+                }
+                cum += w[i];
             }
-            cum += w[i];
+            if (pick >= 0) {
+                ri.tile = pick;
+                ri.thr = thr - before;
+            } else {  // rounding inside the run: its last tile with mass
+                ri.tile = lastpos;
+                ri.thr = __builtin_huge_val();
+            }
+            info[r] = ri;
         }
-        if (pick >= 0) {
-            ri.tile = pick;
-            ri.thr = thr - before;
-        } else {  // rounding inside the run: its last tile with mass
-            ri.tile = lastpos;
-            ri.thr = __builtin_huge_val();
-        }
-        info[r] = ri;
-    } else if (s_pick == kThreads && tid == 0) {
+    } else if (lane == 0) {
         // rounding pushed u * total past the end: the row's last tile with mass
-        ri.tile = max(s_last, 0);
+        ri.tile = max(last, 0);
         ri.thr = __builtin_huge_val();
         info[r] = ri;
     }
+}
+
+inline void stats_pass(const MarkovArgs& a, const float2* stats, RowInfo* info, int ntiles, int k,
+                       hipStream_t s) {
+    if (ntiles <= DSPARK_WAVE * 16)
+        hipLaunchKernelGGL(md_stats<16>, dim3(a.R), dim3(DSPARK_WAVE), 0, s, a, stats, info, ntiles, k);
+    else
+        hipLaunchKernelGGL(md_stats<kStatsMaxPer>, dim3(a.R), dim3(DSPARK_WAVE), 0, s, a, stats, info, ntiles, k);
 }
 
 // One launch of md_tile over every vocabulary tile, instantiated for the
@@ -765,7 +731,7 @@ hipError_t launch_rnn_ks(const MarkovArgs& a, uint16_t* Ee, uint16_t* E3, float*
         hipLaunchKernelGGL(rnn_state, dim3(a.rank / kStJ, ceil_div(a.R, kStR)), dim3(kThreads), 0, s, a, hpp,
                            sp, tp, sn, tn, (const uint16_t*)Ee, E3, k);
         tile_pass<KS, 3, 0>(a, E3, stats, info, Ee, shp, ntiles, k, vec, s);
-        hipLaunchKernelGGL(md_stats, dim3(a.R), dim3(kThreads), 0, s, a, stats, info, ntiles, k);
+        stats_pass(a, stats, info, ntiles, k, s);
         // the draw gathers W1[x_k] into Ee: the embedding input of position k + 1
         tile_pass<KS, 3, 1>(a, E3, stats, info, Ee, shp, ntiles, k, vec, s);
     }
@@ -783,7 +749,7 @@ hipError_t launch_ks(const MarkovArgs& a, uint16_t* E0, uint16_t* E1, float2* st
         uint16_t* Ek = (k & 1) ? E0 : E1;
         uint16_t* En = (k & 1) ? E1 : E0;
         tile_pass<KS, 1, 0>(a, Ek, stats, info, En, shp, ntiles, k, vec, s);
-        hipLaunchKernelGGL(md_stats, dim3(a.R), dim3(kThreads), 0, s, a, stats, info, ntiles, k);
+        stats_pass(a, stats, info, ntiles, k, s);
         tile_pass<KS, 1, 1>(a, Ek, stats, info, En, shp, ntiles, k, vec, s);
     }
     return hipGetLastError();
@@ -862,7 +828,7 @@ hipError_t launch_rnn(const MarkovArgs& a, void* ws, hipStream_t s) {
 
 bool markov_rank_supported(int rank) { return rank == 32 || rank == 64 || rank == 128 || rank == 256; }
 
-int markov_max_vocab() { return mkd::kThreads * mkd::kStatsPer * mkd::kTileV; }
+int markov_max_vocab() { return DSPARK_WAVE * mkd::kStatsMaxPer * mkd::kTileV; }
 
 hipError_t launch_markov(const MarkovArgs& a, void* ws, hipStream_t s) {
     const int ntiles = mkd::ceil_div(a.V, mkd::kTileV);

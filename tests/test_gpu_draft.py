@@ -85,11 +85,20 @@ def test_draft_other_ranks(rank):
 
 
 def test_draft_several_request_chunks():
-    # 150 requests: the embeddings stream through LDS in three chunks of 64
+    # 150 requests: the embeddings stream through LDS in five chunks of 32
     w = synth.scaled(synth.WORKLOADS["serving"], R=150, K=2, V=1024)
     case = guard.draft_case(w, 4, rank=64, d=8)
     tok, p, conf = _run_gpu(w, case, 64, 8)
     _compare(w, case, tok, p, conf, "150 requests")
+
+
+def test_draft_wide_vocabulary():
+    # 1563 vocabulary tiles: the per-request statistics take 32 tiles per lane
+    # (the serving vocabulary has 1010 tiles, 16 per lane)
+    w = synth.scaled(synth.WORKLOADS["serving"], R=3, K=2, V=200003)
+    case = guard.draft_case(w, 9, rank=64, d=16)
+    tok, p, conf = _run_gpu(w, case, 64, 16)
+    _compare(w, case, tok, p, conf, "wide vocabulary")
 
 
 def test_draft_invalid_anchor():
