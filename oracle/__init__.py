@@ -49,6 +49,8 @@ def _load():
         i32, i64, f64 = C.c_int, C.c_int64, C.c_double
         lib.oracle_survival.argtypes = [p, i32, i32, p]
         lib.oracle_schedule.argtypes = [p, i32, i32, p, i64, i32, p, p, p, p, p, p]
+        lib.oracle_schedule_capacity.argtypes = [p, i32, i32, p, i64, p, p]
+        lib.oracle_schedule_topk.argtypes = [p, i32, i32, i64, p, p]
         lib.oracle_verify_attn.argtypes = [p, p, p, p, p, p, i32, p, p, i32, i32, i32, i32, i32,
                                            i32, f64, i32, p, i64, p, p]
         lib.oracle_accept.argtypes = [p, p, p, i32, i64, p, p, i32, i32, i32, f64, p, p, p, p]
@@ -59,7 +61,8 @@ def _load():
         lib.oracle_threads.argtypes = []
         lib.oracle_set_threads.argtypes = [i32]
         lib.oracle_set_threads.restype = None
-        for f in (lib.oracle_survival, lib.oracle_schedule, lib.oracle_verify_attn,
+        for f in (lib.oracle_survival, lib.oracle_schedule, lib.oracle_schedule_capacity,
+                  lib.oracle_schedule_topk, lib.oracle_verify_attn,
                   lib.oracle_accept, lib.oracle_markov_draft, lib.oracle_rnn_draft,
                   lib.oracle_threads):
             f.restype = C.c_int
@@ -119,6 +122,33 @@ def schedule(conf: np.ndarray, sps: np.ndarray, mode: int = 0, trace: bool = Fal
     if trace:
         return ln, tb.value, na.value, mm.value, tr[: nt.value]
     return ln, tb.value, na.value, mm.value
+
+
+def schedule_capacity(conf_prev: np.ndarray, sps: np.ndarray):
+    """Capacity of the asynchronous scheduler: the number of draft tokens the
+    no-break search admits on earlier confidences.  Returns (capacity,
+    min_margin of its throughput comparisons)."""
+    conf_prev = _c(conf_prev, np.float32)
+    sps = _c(sps, np.float64)
+    R, K = conf_prev.shape
+    cap = C.c_int32()
+    mm = C.c_double()
+    rc = _load().oracle_schedule_capacity(_ptr(conf_prev), R, K, _ptr(sps), sps.size,
+                                          C.byref(cap), C.byref(mm))
+    _check(rc, "schedule_capacity")
+    return cap.value, mm.value
+
+
+def schedule_topk(conf: np.ndarray, capacity: int):
+    """Dynamic top-K admission of the current candidates.  Returns
+    (len[R] int32, n_admitted)."""
+    conf = _c(conf, np.float32)
+    R, K = conf.shape
+    ln = np.zeros(R, dtype=np.int32)
+    na = C.c_int32()
+    rc = _load().oracle_schedule_topk(_ptr(conf), R, K, int(capacity), _ptr(ln), C.byref(na))
+    _check(rc, "schedule_topk")
+    return ln, na.value
 
 
 def cu_from_len(ln: np.ndarray) -> np.ndarray:

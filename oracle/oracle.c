@@ -8,7 +8,10 @@
  *
  * It is deliberately slow and literal:
  *   - scheduling follows the hardware-aware prefix scheduler (Algorithm 1 of
- *     the section on confidence-scheduled verification) step by step;
+ *     the section on confidence-scheduled verification) step by step, and its
+ *     asynchronous form (the section on the scheduler in practice): a
+ *     capacity from the no-break search on earlier confidences, then top-K
+ *     admission of the current candidates;
  *   - attention is the textbook masked softmax attention, written out;
  *   - acceptance is the left-to-right speculative acceptance rule of the
  *     background section on speculative decoding, with the conventions listed
@@ -164,6 +167,60 @@ int oracle_schedule(const float* conf, int R, int K, const double* sps, int64_t 
     if (min_margin_out) *min_margin_out = min_margin;
     if (n_trace) *n_trace = nt;
     free(a); free(E); free(l);
+    return ORACLE_OK;
+}
+
+/*
+ * Capacity of the asynchronous scheduler (section "Hardware-Aware Prefix
+ * Scheduler in Practice").  The search without the early stop (mode 1 above)
+ * runs on the confidences of an earlier step; the number of draft tokens it
+ * admits is the truncation length of a later step's top-K admission.
+ *   conf_prev [R, K] fp32, sps as for oracle_schedule.
+ * Outputs *capacity; *min_margin (nullable) as for oracle_schedule.
+ */
+int oracle_schedule_capacity(const float* conf_prev, int R, int K, const double* sps,
+                             int64_t sps_len, int32_t* capacity, double* min_margin_out) {
+    if (!capacity) return ORACLE_EINVAL;
+    int32_t* len = (int32_t*)malloc(sizeof(int32_t) * (size_t)(R > 0 ? R : 1));
+    if (!len) return ORACLE_EINVAL;
+    int32_t n_adm = 0;
+    int rc = oracle_schedule(conf_prev, R, K, sps, sps_len, 1, len, NULL, &n_adm,
+                             min_margin_out, NULL, NULL);
+    free(len);
+    if (rc != ORACLE_OK) return rc;
+    *capacity = n_adm;
+    return ORACLE_OK;
+}
+
+/*
+ * Dynamic top-K admission of the same section.  The current candidates
+ * {(r, j) : a_{r,j} > 0}, with a the survival products of the CURRENT
+ * confidences, are ranked exactly as in Algorithm 1 (descending a, ties by
+ * request then position) and admitted in that order, each admission setting
+ * l_r = j, until `capacity` of them are in (all of them if there are fewer;
+ * a negative capacity admits none).  No throughput is evaluated here: the
+ * capacity carries the whole trade-off, decided on earlier information.
+ * Outputs len[R] and *n_admitted (nullable).
+ */
+int oracle_schedule_topk(const float* conf, int R, int K, int64_t capacity, int32_t* len,
+                         int32_t* n_admitted_out) {
+    if (!conf || !len || R <= 0 || K < 0) return ORACLE_EINVAL;
+    double* a = (double*)malloc(sizeof(double) * ((size_t)R * K + 1));
+    cand_t* E = (cand_t*)malloc(sizeof(cand_t) * ((size_t)R * K + 1));
+    if (!a || !E) { free(a); free(E); return ORACLE_EINVAL; }
+    oracle_survival(conf, R, K, a);
+    int64_t n = 0;
+    for (int r = 0; r < R; ++r)
+        for (int j = 1; j <= K; ++j) {
+            double v = a[(int64_t)r * K + (j - 1)];
+            if (v > 0.0) { E[n].a = v; E[n].r = r; E[n].j = j; ++n; }
+        }
+    qsort(E, (size_t)n, sizeof(cand_t), cand_order);
+    int64_t take = capacity < 0 ? 0 : (capacity < n ? capacity : n);
+    for (int r = 0; r < R; ++r) len[r] = 0;
+    for (int64_t i = 0; i < take; ++i) len[E[i].r] = E[i].j;
+    if (n_admitted_out) *n_admitted_out = (int32_t)take;
+    free(a); free(E);
     return ORACLE_OK;
 }
 

@@ -105,6 +105,39 @@ def test_appendix_selection_bias(appendix):
         np.testing.assert_allclose(law, expect, atol=5e-4)
 
 
+def test_capacity_fixed_in_advance_keeps_the_target_law(appendix):
+    """The asynchronous scheduler of the scheduler-in-practice section: the
+    capacity comes from confidences of an earlier step, so it cannot depend on
+    the current draft x_1; the current step admits its top-capacity
+    candidates.  Whatever capacity the earlier search hands over (the two
+    appendix realisations give 2 and 0; 1 is the remaining case), the first
+    output token keeps the target law (0.7, 0.3), where the same search run
+    on the current confidences gives (0.85, 0.15)."""
+    sps = np.array([0.0, appendix["sps_1"], appendix["sps_2"], appendix["sps_3"]])
+    p_d = np.array(appendix["p_draft"], dtype=np.float32)
+    z = np.log(np.array(appendix["p_target"])).astype(np.float32)
+    c2_of = {0: appendix["case1_c2"], 1: appendix["case2_c2"]}  # x_1 = A -> high c_2
+    caps = [oracle.schedule_capacity(np.array([[appendix["a_1"], c2]], np.float32), sps)[0]
+            for c2 in (appendix["case1_c2"], appendix["case2_c2"])]
+    assert caps == [2, 0]
+    n = 20000
+    grid = _midpoints(n)
+    for cap in caps + [1]:
+        law = np.zeros(2)
+        for x in (0, 1):
+            conf = np.array([[appendix["a_1"], c2_of[x]]], dtype=np.float32)
+            ln, _ = oracle.schedule_topk(conf, cap)
+            L = int(ln[0])
+            assert (L >= 1) == (cap >= 1)  # x_1's admission does not depend on x_1
+            rows = np.stack([z] * (L + 1))
+            u = np.stack([grid, grid, grid[::-1]], axis=1)
+            logits, dp, tk, cu = _tile_case(rows, np.stack([p_d, p_d]), np.array([x, 0]), u)
+            acc, nxt, _, _ = oracle.accept(tk, dp, logits, "f32", cu, 2, 2, u=u)
+            first = np.where(acc >= 1, x, nxt)
+            law += p_d[x] * np.bincount(first, minlength=2) / n
+        np.testing.assert_allclose(law, appendix["lossless_output"], atol=5e-4)
+
+
 @pytest.mark.parametrize("seed", range(6))
 def test_lossless_by_enumeration(seed):
     rng = np.random.default_rng(seed)

@@ -41,6 +41,19 @@ MUTANTS = {
     "schedule: snapshot of the admitted request only": (SCHED,
         "            for (int r = 0; r < R; ++r) len[r] = l[r]; /* snapshot l* <- l */",
         "            len[E[i].r] = E[i].j;"),
+    "schedule capacity: taken from the search with the early stop": (SCHED,
+        "    int rc = oracle_schedule(conf_prev, R, K, sps, sps_len, 1, len, NULL, &n_adm,",
+        "    int rc = oracle_schedule(conf_prev, R, K, sps, sps_len, 0, len, NULL, &n_adm,"),
+    "schedule top-K: one candidate past the capacity": (SCHED,
+        "    int64_t take = capacity < 0 ? 0 : (capacity < n ? capacity : n);",
+        "    int64_t take = capacity < 0 ? 0 : (capacity + 1 < n ? capacity + 1 : n);"),
+    "schedule top-K: ranked by the position's own confidence": (SCHED,
+        "    oracle_survival(conf, R, K, a);\n    int64_t n = 0;",
+        "    for (int64_t i = 0; i < (int64_t)R * K; ++i) a[i] = conf_value(conf[i]);\n"
+        "    int64_t n = 0;"),
+    "schedule top-K: the capacity is ignored": (SCHED,
+        "    for (int64_t i = 0; i < take; ++i) len[E[i].r] = E[i].j;",
+        "    for (int64_t i = 0; i < n; ++i) len[E[i].r] = E[i].j;"),
     # ---- verify attention
     "attention: causal limit one key short": (ATTN,
         "        int64_t visible = (int64_t)kv_len[r] - ql + t + 1;",

@@ -218,3 +218,115 @@ def test_mode1_keeps_every_candidate_before_its_best_point():
     assert th1 == pytest.approx((2 + a[0] + a[1]) * 0.6, rel=1e-15)
     ln0, th0, n0, _ = oracle.schedule(conf, sps, 0)
     assert ln0.tolist() == [0, 0] and n0 == 0 and th0 == 2.0
+
+
+# --------------------------------------------------------------------------
+# the asynchronous scheduler: capacity from earlier confidences, then top-K
+# admission of the current candidates (section on the scheduler in practice)
+# --------------------------------------------------------------------------
+
+def _leading_positive(conf):
+    """Closed form of admitting every candidate: the run of confidences > 0
+    at the start of each row (NaN, zero and negative end it)."""
+    ok = np.nan_to_num(conf.astype(np.float64), nan=-1.0) > 0
+    return np.where(ok.all(axis=1), conf.shape[1], np.argmin(ok, axis=1)).astype(np.int32)
+
+
+def test_appendix_capacities(appendix):
+    """The no-break search on the appendix's two realisations admits 2 and 0
+    draft tokens: those are the capacities it hands to a later step."""
+    sps = _sps([appendix["sps_1"], appendix["sps_2"], appendix["sps_3"]])
+    for c2, expect in ((appendix["case1_c2"], appendix["case1_len_no_break"]),
+                       (appendix["case2_c2"], appendix["case2_len_no_break"])):
+        conf = np.array([[appendix["a_1"], c2]], dtype=np.float32)
+        cap, _ = oracle.schedule_capacity(conf, sps)
+        assert cap == int(expect)
+
+
+def test_topk_capacity_extremes():
+    rng = np.random.default_rng(11)
+    R, K = 9, 6
+    conf = rng.uniform(0.0, 1.0, size=(R, K)).astype(np.float32)
+    conf[2, 0] = 0.0
+    conf[4, 3] = np.nan
+    conf[5, 1] = -0.5
+    conf[6, 2] = 1.5
+    n_pos = int(_leading_positive(conf).sum())
+    for cap in (0, -1, -1000):
+        ln, n = oracle.schedule_topk(conf, cap)
+        assert ln.tolist() == [0] * R and n == 0
+    for cap in (n_pos, n_pos + 1, R * K, 10 ** 9):
+        ln, n = oracle.schedule_topk(conf, cap)
+        assert ln.tolist() == _leading_positive(conf).tolist()
+        assert n == n_pos
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_topk_is_the_first_capacity_candidates_brute_force(seed):
+    """For every capacity, the admitted set is the first min(capacity, |E|)
+    candidates of numpy's (-a, r, j) ranking; so it is a threshold set of the
+    current a, and within a request a prefix."""
+    rng = np.random.default_rng(100 + seed)
+    R = int(rng.integers(1, 5))
+    K = int(rng.integers(1, 6))
+    conf = rng.uniform(0.0, 1.0, size=(R, K)).astype(np.float32)
+    if seed % 3 == 0:
+        conf[rng.integers(0, R), rng.integers(0, K)] = 1.0  # equal survival values
+    if seed % 4 == 0:
+        conf[:] = np.float32(0.5)  # ties everywhere
+    if seed % 5 == 0:
+        conf[0, rng.integers(0, K)] = 0.0
+    a = np.cumprod(np.clip(conf.astype(np.float64), 0, 1), axis=1)
+    rs, js = _greedy_path(a)
+    for cap in range(0, R * K + 2):
+        ln, n = oracle.schedule_topk(conf, cap)
+        take = min(cap, len(rs))
+        assert n == take
+        expect = np.zeros(R, dtype=int)
+        for r, j in zip(rs[:take], js[:take]):
+            expect[r] = max(expect[r], j)
+        assert ln.tolist() == expect.tolist()
+        adm = np.arange(K)[None, :] < ln[:, None]
+        assert adm.sum() == take
+        rest = ~adm & (a > 0)
+        if adm.any() and rest.any():
+            assert a[adm].min() >= a[rest].max()
+
+
+@pytest.mark.parametrize("name", synth.WORKLOAD_ORDER)
+def test_topk_with_its_own_capacity_is_mode1(name):
+    """With no change of confidences between the two steps, the capacity
+    decided by the no-break search and the top-K admission together are the
+    no-break search itself."""
+    w = synth.WORKLOADS[name]
+    sps = synth.sps_table(w)
+    for seed in range(2):
+        conf = synth.confidences(w, seed)
+        cap, _ = oracle.schedule_capacity(conf, sps)
+        ln1, _, n1, _ = oracle.schedule(conf, sps, 1)
+        assert cap == n1 == int(ln1.sum())
+        ln, n = oracle.schedule_topk(conf, cap)
+        assert n == cap
+        assert ln.tolist() == ln1.tolist()
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_capacity_is_the_brute_force_optimum_size(seed):
+    """The capacity equals the number of draft tokens of the best length
+    vector over [0, K]^R (exhaustive search) whenever that best is unique."""
+    rng = np.random.default_rng(300 + seed)
+    R = int(rng.integers(1, 4))
+    K = int(rng.integers(1, 5))
+    conf = rng.uniform(0.0, 1.0, size=(R, K)).astype(np.float32)
+    T = np.arange(R * (K + 1) + 1)
+    knee = int(rng.integers(0, R * (K + 1)))
+    sps = 1.0 / (1.0 + rng.uniform(0.02, 0.6) * np.maximum(0, T - knee))
+    a = np.cumprod(conf.astype(np.float64), axis=1)
+    scored = []
+    for ln in itertools.product(range(K + 1), repeat=R):
+        scored.append((_theta(a, ln, sps), sum(ln)))
+    scored.sort(reverse=True)
+    if len(scored) > 1 and scored[0][0] - scored[1][0] <= 1e-12 * scored[0][0]:
+        pytest.skip("tied optimum")
+    cap, _ = oracle.schedule_capacity(conf, sps)
+    assert cap == scored[0][1]
