@@ -40,7 +40,7 @@
 extern "C" {
 #endif
 
-#define DSPARK_ABI_VERSION 1
+#define DSPARK_ABI_VERSION 2
 
 typedef enum {
     DSPARK_OK = 0,
@@ -65,8 +65,7 @@ const char* dspark_last_error(void);
 
 /* ------------------------------------------------------------------------
  * Stage 1: hardware-aware prefix scheduler (Algorithm 1 of the section on
- * confidence-scheduled verification; the "scheduler in practice" section for
- * mode 1).
+ * confidence-scheduled verification).
  *
  *   conf     [R, K] fp32   conditional confidence c_{r,j} of draft position
  *                          j+1 (confidence-head section).  The survival
@@ -80,6 +79,12 @@ const char* dspark_last_error(void);
  *   mode     0 = the causal greedy with early stop (stop at the first
  *                admission that does not strictly raise Theta = tau * SPS(B));
  *            1 = no early stop: the best prefix of the same greedy path.
+ *                On the CURRENT confidences this search is not lossless: the
+ *                appendix counterexample shows it biasing the first output
+ *                token, because later confidences depend on the realised
+ *                drafts.  The lossless use of the no-break search is the
+ *                asynchronous scheduler below (dspark_schedule_capacity on
+ *                an earlier step's confidences, then dspark_schedule_topk).
  *   len      [R] int32 out  selected verification length l*_r in 0..K.
  *   cu_q     [R+1] int32 out (nullable) exclusive prefix sum of 1 + len_r:
  *                          request r's verify tokens are rows
@@ -104,6 +109,38 @@ dspark_status dspark_schedule(const float* conf, int R, int K, const double* sps
                               dspark_stream stream);
 
 /* ------------------------------------------------------------------------
+ * Stage 1, asynchronous form (the section on the hardware-aware prefix
+ * scheduler in practice).  The candidates of the current step are ranked by
+ * their current survival products exactly as in dspark_schedule; only the
+ * truncation length -- the capacity, a count of draft tokens -- comes from the
+ * no-break search over the confidences of an earlier step (two steps before,
+ * in the paper's pipeline).  Since the capacity cannot depend on the current
+ * drafts, the admission of a draft does not depend on its own realisation.
+ *
+ * dspark_schedule_capacity: runs the no-break search (mode 1 above) on
+ *   conf_prev [R, K] fp32 with the table sps [sps_len] fp64 (sps_len > R*(K+1))
+ *   and writes the number of draft tokens it admits to *capacity (device
+ *   int32).  It writes nothing else outside the workspace.
+ * dspark_schedule_topk: admits the first min(*capacity, |E|) candidates of the
+ *   current order (descending a of conf [R, K], ties by r then j; E = the
+ *   candidates with a > 0; a negative capacity admits none) and writes len,
+ *   cu_q and tok_req as dspark_schedule does.  *capacity is read on the device
+ *   (typically written by an earlier dspark_schedule_capacity on the same
+ *   stream), so the step needs no host round trip.  No throughput table is
+ *   read.  With an unchanged request set the verify batch is R + *capacity
+ *   tokens whenever |E| >= *capacity.
+ * Both take the workspace of dspark_schedule_workspace_size(R, K) (256-aligned)
+ * and the limits of dspark_schedule; null or misaligned pointers -> EINVAL.
+ * ---------------------------------------------------------------------- */
+dspark_status dspark_schedule_capacity(const float* conf_prev, int R, int K, const double* sps,
+                                       int64_t sps_len, int32_t* capacity, void* ws,
+                                       size_t ws_bytes, dspark_stream stream);
+
+dspark_status dspark_schedule_topk(const float* conf, int R, int K, const int32_t* capacity,
+                                   int32_t* len, int32_t* cu_q, int32_t* tok_req, void* ws,
+                                   size_t ws_bytes, dspark_stream stream);
+
+/* ------------------------------------------------------------------------
  * Stage 2: ragged causal verify attention over a paged KV cache (the target
  * model's verification forward pass over the flattened verify tokens).
  *
@@ -120,9 +157,12 @@ dspark_status dspark_schedule(const float* conf, int R, int K, const double* sps
  *             request r (0-based) attends keys 0 .. kv_len_r - q_len_r + t.
  *   cu_q      [R+1] int32: as produced by dspark_schedule.
  *   max_q     host bound on every q_len_r = cu_q[r+1] - cu_q[r] (K+1 after
- *             scheduling).  Rows with q_len_r > max_q or kv_len_r outside
- *             [q_len_r, max_pages*page_size] are skipped (left unwritten).
+ *             scheduling).  A request is skipped (its rows left unwritten)
+ *             when q_len_r > max_q, when kv_len_r lies outside
+ *             [q_len_r, max_pages*page_size], or when its rows cu_q[r] ..
+ *             cu_q[r+1]-1 do not lie inside [0, min(cu_q[R], R*max_q)).
  *   Head h reads KV head h / (Hq / Hkv).
+ *   scale     softmax scale, finite and > 0 (else DSPARK_EINVAL).
  *   out       [total_q, Hq, Dv] softmax(scale * q k^T) v in dtype `dt`
  *             (fp32 accumulation, rounded to nearest-even on store).
  *   lse       [total_q, Hq] fp32 (nullable): natural-log sum of exp of the
@@ -167,8 +207,9 @@ dspark_status dspark_verify_attn(const void* q, const void* k_cache, const void*
  *   u         [R, K+1] fp32 uniforms in [0,1) (nullable): u[r,t] (t < K) tests
  *             draft t+1, u[r,K] draws the emitted token.
  *   cu_q      [R+1] int32 as produced by dspark_schedule; len_r = q_len_r - 1
- *             must lie in 0..K (requests outside it get accepted_len = -1,
- *             next_tok = -1).
+ *             must lie in 0..K and the rows cu_q[r] .. cu_q[r+1]-1 inside
+ *             [0, min(cu_q[R], R*(K+1))) (other requests get
+ *             accepted_len = -1, next_tok = -1).
  *   draft_p == NULL and u == NULL: greedy -- draft t+1 is accepted iff it is
  *             the argmax of the raw logits of row t (lowest index on ties);
  *             the emitted token is the argmax of row accepted_len.

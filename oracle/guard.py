@@ -77,6 +77,40 @@ def schedule_case(w: synth.Workload, seed: int, mode: int = 0, max_tries: int = 
                     sched_margin=mm, sched_guarded=mm >= guard)
 
 
+@dataclass
+class CapacityCase:
+    conf_prev: np.ndarray  # earlier step's confidences (capacity decided on them)
+    conf: np.ndarray  # current confidences (ranked)
+    sps: np.ndarray
+    capacity: int  # oracle capacity
+    len: np.ndarray  # oracle top-K lengths
+    cu_q: np.ndarray
+    margin: float  # min margin of the capacity search's throughput comparisons
+    guarded: bool
+
+
+def capacity_case(w: synth.Workload, seed: int, max_tries: int = 64,
+                  guard: float = SCHED_GUARD) -> CapacityCase:
+    """Asynchronous scheduler inputs: the earlier confidences are redrawn until
+    the no-break search's comparisons are all outside the guard band; the
+    top-K admission itself takes no floating-point decision that can tie
+    (equal survival values are ordered by index)."""
+    sps = synth.sps_table(w)
+    best = None
+    for attempt in range(max_tries):
+        prev = synth.previous_confidences(w, seed, attempt)
+        cap, mm = oracle.schedule_capacity(prev, sps)
+        if best is None or mm > best[2]:
+            best = (prev, cap, mm)
+        if mm >= guard:
+            break
+    prev, cap, mm = best
+    conf = synth.confidences(w, seed)
+    ln, _ = oracle.schedule_topk(conf, cap)
+    return CapacityCase(conf_prev=prev, conf=conf, sps=sps, capacity=cap, len=ln,
+                        cu_q=oracle.cu_from_len(ln), margin=mm, guarded=mm >= guard)
+
+
 def _accept_subset(case: StepCase, reqs: List[int], u: np.ndarray):
     """Oracle acceptance for a subset of requests (rows gathered)."""
     w = case.w

@@ -371,7 +371,10 @@ __global__ __launch_bounds__(kBlk) void acc_resolve(
     const int row0 = cu_q[r];
     const int l = cu_q[r + 1] - row0 - 1;
     __syncthreads();
-    if (l < 0 || l > K || row0 < 0 || (int64_t)row0 + l + 1 > (int64_t)R * (K + 1)) {
+    // the request's rows must lie inside the rows the row pass covered (and the
+    // caller sized): [0, min(cu_q[R], R * (K + 1)))
+    if (l < 0 || l > K || row0 < 0 ||
+        (int64_t)row0 + l + 1 > (int64_t)clamp_rows(cu_q[R], R * (K + 1))) {
         if (tid == 0) {
             accepted_len[r] = -1;
             next_tok[r] = -1;

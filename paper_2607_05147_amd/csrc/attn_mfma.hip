@@ -149,11 +149,15 @@ __global__ __launch_bounds__(kPlanThreads) void mf_plan(MfParams p) {
     for (int i = tid; i < kBins; i += kPlanThreads) s_bin[i] = 0;
     if (tid == 0) s_merge = 0;
     __syncthreads();
+    const int total_rows = min(max(a.cu_q[a.R], 0), a.R * a.max_q);
     auto shape = [&](int r, int& q0, int& ql, int& kv, int& ns, int& nr) {
         q0 = a.cu_q[r];
         ql = a.cu_q[r + 1] - q0;
         kv = a.kv_len[r];
         if (ql < 1 || ql > a.max_q || kv < ql || kv > a.max_pages * a.page) return false;
+        // the request's rows must lie inside the flattened batch the caller
+        // sized: [0, min(cu_q[R], R * max_q))
+        if (q0 < 0 || (int64_t)q0 + ql > total_rows) return false;
         ns = (kv + kSplit - 1) / kSplit;
         nr = (ql * p.group + p.chunk_rows - 1) / p.chunk_rows;
         return true;

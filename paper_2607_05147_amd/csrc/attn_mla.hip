@@ -204,11 +204,15 @@ __global__ __launch_bounds__(kPlanThreads) void mla_plan(Params p) {
     const int lane = tid & (DSPARK_WAVE - 1);
     const int wave = tid / DSPARK_WAVE;
     for (int i = tid; i < kQueues * kBins; i += kPlanThreads) (&s_bin[0][0])[i] = 0;
+    const int total_rows = min(max(a.cu_q[a.R], 0), a.R * a.max_q);
     auto shape = [&](int r, int& q0, int& ql, int& kv, int& ns, int& nrb) {
         q0 = a.cu_q[r];
         ql = a.cu_q[r + 1] - q0;
         kv = a.kv_len[r];
         if (ql < 1 || ql > a.max_q || kv < ql || kv > a.max_pages * a.page) return false;
+        // the request's rows must lie inside the flattened batch the caller
+        // sized: [0, min(cu_q[R], R * max_q))
+        if (q0 < 0 || (int64_t)q0 + ql > total_rows) return false;
         ns = (kv + kSplit - 1) / kSplit;
         nrb = (ql * p.group + kRows - 1) / kRows;
         return true;

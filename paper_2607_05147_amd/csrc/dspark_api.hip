@@ -131,9 +131,62 @@ dspark_status dspark_schedule(const float* conf, int R, int K, const double* sps
     if (ws_bytes < need || !ws || !aligned(ws, 256))
         return fail(DSPARK_EWORKSPACE, "workspace of %zu bytes (256-aligned) needed, got %zu",
                     need, ws_bytes);
-    return hip_status(dspark::launch_schedule(conf, R, K, sps, mode, len, cu_q, tok_req, ws,
-                                              (hipStream_t)stream),
+    return hip_status(dspark::launch_schedule(conf, R, K, sps, mode, nullptr, nullptr, len, cu_q,
+                                              tok_req, ws, (hipStream_t)stream),
                       "dspark_schedule");
+}
+
+namespace {
+
+dspark_status check_sched_sizes(int R, int K) {
+    if (R < 1 || R > kMaxR) return fail(DSPARK_EINVAL, "R=%d outside [1, %d]", R, kMaxR);
+    if (K < 0 || K > kMaxK) return fail(DSPARK_EINVAL, "K=%d outside [0, %d]", K, kMaxK);
+    if ((int64_t)R * K > kMaxSchedCand)
+        return fail(DSPARK_EUNSUPPORTED, "R*K=%lld exceeds %d candidates", (long long)R * K,
+                    kMaxSchedCand);
+    return DSPARK_OK;
+}
+
+dspark_status check_sched_ws(int R, int K, const void* ws, size_t ws_bytes) {
+    const size_t need = dspark::schedule_workspace(R, K);
+    if (ws_bytes < need || !ws || !aligned(ws, 256))
+        return fail(DSPARK_EWORKSPACE, "workspace of %zu bytes (256-aligned) needed, got %zu",
+                    need, ws_bytes);
+    return DSPARK_OK;
+}
+
+}  // namespace
+
+dspark_status dspark_schedule_capacity(const float* conf_prev, int R, int K, const double* sps,
+                                       int64_t sps_len, int32_t* capacity, void* ws,
+                                       size_t ws_bytes, dspark_stream stream) {
+    if (dspark_status st = check_sched_sizes(R, K)) return st;
+    if (!capacity || !sps || (K > 0 && !conf_prev))
+        return fail(DSPARK_EINVAL, "null conf_prev/sps/capacity");
+    if (sps_len <= (int64_t)R * (K + 1))
+        return fail(DSPARK_ESHAPE, "sps_len=%lld must exceed R*(K+1)=%lld", (long long)sps_len,
+                    (long long)R * (K + 1));
+    if (!aligned(conf_prev, 4) || !aligned(sps, 8) || !aligned(capacity, 4))
+        return fail(DSPARK_EINVAL, "misaligned pointer");
+    if (dspark_status st = check_sched_ws(R, K, ws, ws_bytes)) return st;
+    return hip_status(dspark::launch_schedule(conf_prev, R, K, sps, 1, nullptr, capacity, nullptr,
+                                              nullptr, nullptr, ws, (hipStream_t)stream),
+                      "dspark_schedule_capacity");
+}
+
+dspark_status dspark_schedule_topk(const float* conf, int R, int K, const int32_t* capacity,
+                                   int32_t* len, int32_t* cu_q, int32_t* tok_req, void* ws,
+                                   size_t ws_bytes, dspark_stream stream) {
+    if (dspark_status st = check_sched_sizes(R, K)) return st;
+    if (!capacity || !len || (K > 0 && !conf))
+        return fail(DSPARK_EINVAL, "null conf/capacity/len");
+    if (!aligned(conf, 4) || !aligned(capacity, 4) || !aligned(len, 4) || !aligned(cu_q, 4) ||
+        !aligned(tok_req, 4))
+        return fail(DSPARK_EINVAL, "misaligned pointer");
+    if (dspark_status st = check_sched_ws(R, K, ws, ws_bytes)) return st;
+    return hip_status(dspark::launch_schedule(conf, R, K, nullptr, 2, capacity, nullptr, len,
+                                              cu_q, tok_req, ws, (hipStream_t)stream),
+                      "dspark_schedule_topk");
 }
 
 // ------------------------------------------------------------------ verify attention
@@ -172,7 +225,10 @@ dspark_status dspark_verify_attn(const void* q, const void* k_cache, const void*
             return fail(DSPARK_EINVAL, "negative stride");
     if (k_strides[2] < Dqk || v_strides[2] < Dv)
         return fail(DSPARK_ESHAPE, "token stride smaller than the head dim");
-    if (!isfinite(scale)) return fail(DSPARK_EINVAL, "scale is not finite");
+    // the kernels take each row's running maximum over raw scores and scale it
+    // afterwards, which is the maximum of the scaled scores only for scale > 0
+    if (!isfinite(scale) || !(scale > 0.0f))
+        return fail(DSPARK_EINVAL, "scale=%g (must be finite and > 0)", (double)scale);
     const size_t esz = dt == DSPARK_BF16 ? 2 : 4;
     if (!aligned(q, esz) || !aligned(k_cache, esz) || !aligned(v_cache, esz) ||
         !aligned(out, esz) || !aligned(lse, 4) || !aligned(block_table, 4) ||

@@ -9,9 +9,12 @@ namespace dspark {
 
 // ---- scheduler --------------------------------------------------------------
 size_t schedule_workspace(int R, int K);
+// mode 0: early stop; 1: no break; 2: top-K with the capacity *cap_in (device).
+// cap_out (device, nullable) receives the admitted count; len == null skips
+// the lengths, cu_q and tok_req.
 hipError_t launch_schedule(const float* conf, int R, int K, const double* sps, int mode,
-                           int32_t* len, int32_t* cu_q, int32_t* tok_req, void* ws,
-                           hipStream_t s);
+                           const int32_t* cap_in, int32_t* cap_out, int32_t* len, int32_t* cu_q,
+                           int32_t* tok_req, void* ws, hipStream_t s);
 
 // ---- verify attention ---------------------------------------------------------
 struct AttnArgs {

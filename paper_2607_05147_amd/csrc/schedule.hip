@@ -18,7 +18,10 @@
 // sched_select (one workgroup):
 //   4. Theta_n = tau_n * SPS(R + n + 1); mode 0 stops at the first n whose
 //      Theta does not exceed its predecessor's (Theta_{-1} = R * SPS(R)),
-//      mode 1 takes the first maximum;
+//      mode 1 takes the first maximum; mode 2 (the asynchronous scheduler's
+//      top-K admission) admits a capacity read from device memory, decided on
+//      an earlier step's confidences, and evaluates no throughput at all;
+//      the capacity call is mode 1 writing its admitted count;
 //   5. len[r] = the largest admitted position of r (admission follows each
 //      request's prefix order, since a is non-increasing in j), then cu_q and
 //      the token -> request marker.
@@ -134,6 +137,7 @@ __global__ __launch_bounds__(kRankThreads) void sched_rank(const float* __restri
 template <int E>
 __global__ __launch_bounds__(kSelThreads) void sched_select(
     const unsigned char* __restrict__ ws, int R, int K, const double* __restrict__ sps, int mode,
+    const int32_t* __restrict__ cap_in, int32_t* __restrict__ cap_out,
     int32_t* __restrict__ len_out, int32_t* __restrict__ cu_q, int32_t* __restrict__ tok_req) {
     extern __shared__ int32_t lenl[];  // [R]
     __shared__ int s_first;
@@ -153,21 +157,25 @@ __global__ __launch_bounds__(kSelThreads) void sched_select(
     // and SPS(R + n + 1) at each position n, SPS(R + i0) before them
     // (indices are clamped, not guarded, so that no load waits behind a
     // branch; the workspace holds at least 256 bytes and sps at least R + N + 1
-    // entries, so every clamped index is in bounds, N = 0 included)
+    // entries, so every clamped index is in bounds, N = 0 included).  Mode 2
+    // has no table (sps may be null) and reads only the flat indices.
     const int i0 = tid * E;
     const int nmax = N > 0 ? N - 1 : 0;
     double tv[E], sv[E];
     int iv[E];
+    double tprev = 0.0, sprev = 0.0, theta0 = 0.0;
+    if (mode != 2) {
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-        const int n = min(i0 + e, nmax);
-        tv[e] = tau_s[n];
-        sv[e] = sps[min(R + i0 + e + 1, R + N)];
-        iv[e] = idx_s[n];
+        for (int e = 0; e < E; ++e) {
+            tv[e] = tau_s[min(i0 + e, nmax)];
+            sv[e] = sps[min(R + i0 + e + 1, R + N)];
+        }
+        tprev = tau_s[min(max(i0 - 1, 0), nmax)];
+        sprev = sps[min(R + i0, R + N)];
+        theta0 = (double)R * sps[R];
     }
-    const double tprev = tau_s[min(max(i0 - 1, 0), nmax)];
-    const double sprev = sps[min(R + i0, R + N)];
-    const double theta0 = (double)R * sps[R];
+#pragma unroll
+    for (int e = 0; e < E; ++e) iv[e] = idx_s[min(i0 + e, nmax)];
     const int ncand = *reinterpret_cast<const int32_t*>(ws);  // written by sched_rank, N = 0 too
 
     for (int r = tid; r < R; r += kSelThreads) lenl[r] = 0;
@@ -176,7 +184,11 @@ __global__ __launch_bounds__(kSelThreads) void sched_select(
 
     // 4. throughput along the greedy path and the stop rule
     int n_adm;
-    if (mode == 0) {
+    if (mode == 2) {
+        // top-K admission: the first min(capacity, candidates) positions; a
+        // negative capacity admits none
+        n_adm = min(max(*cap_in, 0), ncand);
+    } else if (mode == 0) {
         int first = ncand;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
@@ -234,6 +246,9 @@ __global__ __launch_bounds__(kSelThreads) void sched_select(
         n_adm = s_first;
     }
 
+    if (cap_out && tid == 0) *cap_out = n_adm;
+    if (!len_out) return;  // the capacity call: no lengths
+
     // 5. lengths: the largest admitted position of each request
 #pragma unroll
     for (int e = 0; e < E; ++e) {
@@ -280,16 +295,16 @@ __global__ __launch_bounds__(kSelThreads) void sched_select(
 
 template <int E>
 static hipError_t launch_select(const unsigned char* ws, int R, int K, const double* sps,
-                                int mode, int32_t* len, int32_t* cu_q, int32_t* tok_req,
-                                hipStream_t s) {
+                                int mode, const int32_t* cap_in, int32_t* cap_out, int32_t* len,
+                                int32_t* cu_q, int32_t* tok_req, hipStream_t s) {
     hipLaunchKernelGGL(sched_select<E>, dim3(1), dim3(kSelThreads), (size_t)R * 4, s, ws, R, K,
-                       sps, mode, len, cu_q, tok_req);
+                       sps, mode, cap_in, cap_out, len, cu_q, tok_req);
     return hipGetLastError();
 }
 
 hipError_t launch_schedule(const float* conf, int R, int K, const double* sps, int mode,
-                           int32_t* len, int32_t* cu_q, int32_t* tok_req, void* ws,
-                           hipStream_t s) {
+                           const int32_t* cap_in, int32_t* cap_out, int32_t* len, int32_t* cu_q,
+                           int32_t* tok_req, void* ws, hipStream_t s) {
     const int N = R * K;
     unsigned char* w = static_cast<unsigned char*>(ws);
     const size_t lds = (size_t)(N > 0 ? N : 1) * 12;
@@ -304,10 +319,10 @@ hipError_t launch_schedule(const float* conf, int R, int K, const double* sps, i
     if (e != hipSuccess) return e;
     // positions per thread of the selection (N <= 8192)
     const int per = (N + kSelThreads - 1) / kSelThreads;
-    if (per <= 1) return launch_select<1>(w, R, K, sps, mode, len, cu_q, tok_req, s);
-    if (per <= 2) return launch_select<2>(w, R, K, sps, mode, len, cu_q, tok_req, s);
-    if (per <= 4) return launch_select<4>(w, R, K, sps, mode, len, cu_q, tok_req, s);
-    return launch_select<8>(w, R, K, sps, mode, len, cu_q, tok_req, s);
+    if (per <= 1) return launch_select<1>(w, R, K, sps, mode, cap_in, cap_out, len, cu_q, tok_req, s);
+    if (per <= 2) return launch_select<2>(w, R, K, sps, mode, cap_in, cap_out, len, cu_q, tok_req, s);
+    if (per <= 4) return launch_select<4>(w, R, K, sps, mode, cap_in, cap_out, len, cu_q, tok_req, s);
+    return launch_select<8>(w, R, K, sps, mode, cap_in, cap_out, len, cu_q, tok_req, s);
 }
 
 }  // namespace dspark

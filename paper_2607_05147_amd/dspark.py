@@ -51,6 +51,10 @@ def lib():
         L.dspark_schedule_workspace_size.argtypes = [i32, i32]
         L.dspark_schedule.restype = i32
         L.dspark_schedule.argtypes = [p, i32, i32, p, i64, i32, p, p, p, p, sz, p]
+        L.dspark_schedule_capacity.restype = i32
+        L.dspark_schedule_capacity.argtypes = [p, i32, i32, p, i64, p, p, sz, p]
+        L.dspark_schedule_topk.restype = i32
+        L.dspark_schedule_topk.argtypes = [p, i32, i32, p, p, p, p, p, sz, p]
         L.dspark_verify_attn_workspace_size.restype = sz
         L.dspark_verify_attn_workspace_size.argtypes = [i32] * 8 + [i32]
         L.dspark_verify_attn.restype = i32
@@ -154,6 +158,54 @@ def dspark_schedule(conf: torch.Tensor, sps: torch.Tensor, mode: int = 0,
     st = lib().dspark_schedule(_p(conf), R, K, _p(sps), sps.numel(), mode, _p(len_out), _p(cu_q),
                                _p(tok_req), _p(ws), ws_bytes, _stream(stream))
     _raise(st, "dspark_schedule")
+    return len_out, cu_q, tok_req
+
+
+def dspark_schedule_capacity(conf_prev: torch.Tensor, sps: torch.Tensor,
+                             capacity: Optional[torch.Tensor] = None,
+                             ws: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """conf_prev fp32 [R, K], sps fp64 [> R*(K+1)] -> capacity int32 [1] (device)."""
+    _dev(conf_prev, "conf_prev", torch.float32)
+    if conf_prev.dim() != 2:
+        raise DSparkError("conf_prev must be [R, K]")
+    R, K = conf_prev.shape
+    _dev(sps, "sps", torch.float64)
+    dev = conf_prev.device
+    if capacity is None:
+        capacity = torch.empty(1, dtype=torch.int32, device=dev)
+    _dev(capacity, "capacity", torch.int32, (1,))
+    ws, ws_bytes = _workspace(dspark_schedule_workspace_size(R, K), dev, ws)
+    st = lib().dspark_schedule_capacity(_p(conf_prev), R, K, _p(sps), sps.numel(), _p(capacity),
+                                        _p(ws), ws_bytes, _stream(stream))
+    _raise(st, "dspark_schedule_capacity")
+    return capacity
+
+
+def dspark_schedule_topk(conf: torch.Tensor, capacity: torch.Tensor,
+                         len_out: Optional[torch.Tensor] = None,
+                         cu_q: Optional[torch.Tensor] = None,
+                         tok_req: Optional[torch.Tensor] = None, want_tok_req: bool = False,
+                         ws: Optional[torch.Tensor] = None, stream=None):
+    """conf fp32 [R, K], capacity int32 [1] (device) -> (len, cu_q, tok_req|None)."""
+    _dev(conf, "conf", torch.float32)
+    if conf.dim() != 2:
+        raise DSparkError("conf must be [R, K]")
+    R, K = conf.shape
+    _dev(capacity, "capacity", torch.int32, (1,))
+    dev = conf.device
+    if len_out is None:
+        len_out = torch.empty(R, dtype=torch.int32, device=dev)
+    if cu_q is None:
+        cu_q = torch.empty(R + 1, dtype=torch.int32, device=dev)
+    if tok_req is None and want_tok_req:
+        tok_req = torch.empty(R * (K + 1), dtype=torch.int32, device=dev)
+    _dev(len_out, "len", torch.int32, (R,))
+    _dev(cu_q, "cu_q", torch.int32, (R + 1,))
+    _dev(tok_req, "tok_req", torch.int32, (R * (K + 1),), optional=True)
+    ws, ws_bytes = _workspace(dspark_schedule_workspace_size(R, K), dev, ws)
+    st = lib().dspark_schedule_topk(_p(conf), R, K, _p(capacity), _p(len_out), _p(cu_q),
+                                    _p(tok_req), _p(ws), ws_bytes, _stream(stream))
+    _raise(st, "dspark_schedule_topk")
     return len_out, cu_q, tok_req
 
 

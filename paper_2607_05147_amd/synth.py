@@ -48,6 +48,7 @@ _STREAM = {
     "mk_wconf": 16,
     "mk_uniform": 17,
     "rnn_w": 18,
+    "conf_prev": 19,
 }
 
 _KV_CHUNK_PAGES = 64  # pages per generator chunk of the KV pool
@@ -188,6 +189,17 @@ def scaled(w: Workload, **over) -> Workload:
 def confidences(w: Workload, seed: int, attempt: int = 0) -> np.ndarray:
     """Per-position draft confidences c[r, j], fp32 [R, K]."""
     g = _rng(seed, "conf", attempt)
+    c = g.beta(w.conf_beta[0], w.conf_beta[1], size=(w.R, w.K))
+    if w.conf_decay != 1.0:
+        c = c * (w.conf_decay ** np.arange(w.K, dtype=np.float64))[None, :]
+    return np.ascontiguousarray(c.astype(np.float32))
+
+
+def previous_confidences(w: Workload, seed: int, attempt: int = 0) -> np.ndarray:
+    """Confidences of an earlier step for the same requests (same law as
+    ``confidences``, an independent sub-stream): the input from which the
+    asynchronous scheduler decides its capacity."""
+    g = _rng(seed, "conf_prev", attempt)
     c = g.beta(w.conf_beta[0], w.conf_beta[1], size=(w.R, w.K))
     if w.conf_decay != 1.0:
         c = c * (w.conf_decay ** np.arange(w.K, dtype=np.float64))[None, :]

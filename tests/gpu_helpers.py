@@ -34,6 +34,20 @@ def gpu_schedule(conf: np.ndarray, sps: np.ndarray, mode: int = 0):
     return ln.cpu().numpy(), cu.cpu().numpy(), tok.cpu().numpy()
 
 
+def gpu_capacity(conf_prev: np.ndarray, sps: np.ndarray) -> torch.Tensor:
+    """Device capacity from the earlier confidences (stays on the device)."""
+    return dspark.dspark_schedule_capacity(to_dev(conf_prev), to_dev(sps))
+
+
+def gpu_topk(conf: np.ndarray, capacity):
+    """Top-K admission; ``capacity`` is a device tensor or a host int."""
+    if not isinstance(capacity, torch.Tensor):
+        capacity = torch.tensor([int(capacity)], dtype=torch.int32, device=dev())
+    ln, cu, tok = dspark.dspark_schedule_topk(to_dev(conf), capacity, want_tok_req=True)
+    torch.cuda.synchronize()
+    return ln.cpu().numpy(), cu.cpu().numpy(), tok.cpu().numpy()
+
+
 class DevKV:
     """Device copy of a synth.PagedKV."""
 

@@ -71,6 +71,41 @@ def test_schedule_validation(L):
     assert _sched(L, conf=C.c_void_p((1 << 20) + 2)) == EINVAL  # misaligned
 
 
+def test_schedule_capacity_validation(L):
+    need = L.dspark_schedule_workspace_size(4, 8)
+
+    def cap(conf=FAKE, R=4, K=8, sps=FAKE, sps_len=100, out=FAKE, ws=FAKE, ws_bytes=need):
+        return L.dspark_schedule_capacity(conf, R, K, sps, sps_len, out, ws, ws_bytes, None)
+
+    assert cap(conf=None) == EINVAL
+    assert cap(sps=None) == EINVAL
+    assert cap(out=None) == EINVAL
+    assert cap(R=0) == EINVAL
+    assert cap(K=65) == EINVAL
+    assert cap(sps_len=36) == ESHAPE
+    assert cap(R=8192, K=2, sps_len=10**6) == EUNSUPPORTED
+    assert cap(out=C.c_void_p((1 << 20) + 2)) == EINVAL
+    assert cap(ws=None) == EWORKSPACE
+    assert cap(ws_bytes=need - 1) == EWORKSPACE
+
+
+def test_schedule_topk_validation(L):
+    need = L.dspark_schedule_workspace_size(4, 8)
+
+    def topk(conf=FAKE, R=4, K=8, capacity=FAKE, ln=FAKE, ws=FAKE, ws_bytes=need):
+        return L.dspark_schedule_topk(conf, R, K, capacity, ln, None, None, ws, ws_bytes, None)
+
+    assert topk(conf=None) == EINVAL
+    assert topk(capacity=None) == EINVAL
+    assert topk(ln=None) == EINVAL
+    assert topk(R=0) == EINVAL
+    assert topk(K=-1) == EINVAL
+    assert topk(R=8192, K=2) == EUNSUPPORTED
+    assert topk(capacity=C.c_void_p((1 << 20) + 1)) == EINVAL
+    assert topk(ws=C.c_void_p((1 << 20) + 64)) == EWORKSPACE
+    assert topk(ws_bytes=need - 1) == EWORKSPACE
+
+
 def test_schedule_workspace(L):
     need = L.dspark_schedule_workspace_size(4, 8)
     assert need >= 16 + 12 * 32 and need % 256 == 0
@@ -110,6 +145,9 @@ def test_verify_attn_validation(L):
     assert _attn(L, R=0) == EINVAL
     assert _attn(L, ks=(C.c_int64 * 3)(1, 1, 64)) == ESHAPE  # token stride < Dqk
     assert _attn(L, scale=float("nan")) == EINVAL
+    assert _attn(L, scale=0.0) == EINVAL
+    assert _attn(L, scale=-0.1) == EINVAL
+    assert _attn(L, scale=float("inf")) == EINVAL
     assert _attn(L, q=C.c_void_p((1 << 20) + 1)) == EINVAL
     assert _attn(L, ws_bytes=16) == EWORKSPACE  # far too small
 

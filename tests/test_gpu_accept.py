@@ -239,3 +239,22 @@ def test_degenerate_shapes(K, V, greedy):
     assert np.array_equal(nxt[ok], nxt_o[ok])
     if V == 1:
         assert (acc == ln).all() and (nxt == 0).all()
+
+
+def test_rows_past_the_batch_end():
+    """Requests whose rows leave [0, cu_q[R]) get accepted_len = next_tok = -1
+    (their rows were not covered by the row pass); the well-formed request is
+    exact against the oracle."""
+    w = synth.scaled(synth.WORKLOADS["mid"], R=4, V=9000)
+    case = guard.build_case(w, 13, with_kv=False)
+    ql = np.diff(case.cu_q)
+    assert ql[1] >= 2 and not case.unguarded
+    # request 0 as scheduled; requests 1 and 2 end past cu_q[R] = ql0 + 1;
+    # request 3 runs backwards
+    cu_m = np.array([0, ql[0], ql[0] + ql[1], ql[0] + ql[1] + ql[2], ql[0] + 1], np.int32)
+    acc, nxt, rate = gpu_accept(w, case.drafts, case.logits, cu_m, want_rate=True)
+    assert acc[0] == case.accepted_len[0] and nxt[0] == case.next_tok[0]
+    assert acc[1:].tolist() == [-1, -1, -1] and nxt[1:].tolist() == [-1, -1, -1]
+    # the one row past request 0 is owned by no well-formed request
+    assert rate[ql[0]] == -1
+    log("[accept] rows past cu_q[R]: requests 1-3 rejected, request 0 exact")

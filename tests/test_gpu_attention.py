@@ -259,6 +259,51 @@ def test_invalid_requests_left_unwritten(name):
     log(f"[attn] invalid requests skipped: {name} R={w.R}, requests 0 and 2 untouched")
 
 
+@pytest.mark.parametrize("name", ["tiny", "mid", "mla"])
+def test_rows_outside_the_batch_left_unwritten(name):
+    """Requests whose row range leaves [0, cu_q[R]) -- a negative start, or an
+    end past cu_q[R] -- are skipped on every path: their rows, and every row
+    past cu_q[R] of buffers sized for R * max_q rows, keep what was there;
+    the well-formed requests match the oracle."""
+    import torch
+    from paper_2607_05147_amd import dspark
+    from gpu_helpers import to_dev
+    over = dict(R=5)
+    if name == "mla":
+        over = dict(R=5, kv_dist=("uniform", 5000, 9000))
+    w = synth.scaled(synth.WORKLOADS[name], **over)
+    kv = synth.paged_kv(w, 23)
+    bf16 = w.dtype == "bf16"
+    # request 0: rows 0..2; request 1: rows 3..10, past cu_q[R] = 6;
+    # request 2: 11 -> 4 (negative length); request 3: rows 4..5; request 4:
+    # rows 6..5 (empty, q_len 0)
+    cu = np.array([0, 3, 11, 4, 6, 6], np.int32)
+    good = {0: (0, 3), 3: (4, 2)}
+    rows_total = w.R * w.max_q
+    q = synth.query_rows(w, 23, [(0, t) for t in range(rows_total)])
+    dkv = DevKV(kv, bf16)
+    qd = to_dev(q, bf16)
+    sentinel = 7.0
+    out = torch.full((rows_total, w.Hq, w.Dv), sentinel, dtype=qd.dtype, device=qd.device)
+    lse = torch.full((rows_total, w.Hq), sentinel, dtype=torch.float32, device=qd.device)
+    dspark.dspark_verify_attn(qd, dkv.k, dkv.v, dkv.ks, dkv.vs, dkv.bt, dkv.kv_len, to_dev(cu),
+                              w.max_q, w.Hkv, w.Dv, w.page, w.scale, out=out, lse=lse)
+    torch.cuda.synchronize()
+    o, l = to_f64(out), to_f64(lse)
+    written = np.zeros(rows_total, bool)
+    for r, (q0, ql) in good.items():
+        written[q0:q0 + ql] = True
+        ref, ref_lse = oracle.verify_attn(q[q0:q0 + ql], kv.k, kv.v, kv.k_strides, kv.v_strides,
+                                          kv.block_table[r:r + 1], kv.kv_len[r:r + 1],
+                                          np.array([0, ql], np.int32), w.Hq, w.Hkv, w.Dqk, w.Dv,
+                                          w.page, w.scale, w.dtype)
+        err = row_rel_err(o[q0:q0 + ql], ref)
+        assert err.max() <= TOL[w.dtype], (r, err.max())
+        np.testing.assert_allclose(l[q0:q0 + ql], ref_lse, rtol=0, atol=1e-4 if bf16 else 1e-5)
+    assert (o[~written] == sentinel).all() and (l[~written] == sentinel).all()
+    log(f"[attn] rows outside the batch skipped: {name}, only requests 0 and 3 written")
+
+
 @pytest.mark.parametrize("name,Hq,Hkv,q_len,kv_len", [
     # one query head per KV head; every context exactly its verify block (the
     # first query sees a single key)

@@ -92,3 +92,91 @@ def test_mode1_keeps_the_prefix_before_its_best_point():
     assert gpu_schedule(conf, sps, 1)[0].tolist() == [1, 1]
     assert gpu_schedule(conf, sps, 0)[0].tolist() == [0, 0]
     _check(conf, sps, 1, "dip then gain")
+
+
+# --------------------------------------------------------------------------
+# asynchronous scheduler: capacity from earlier confidences, top-K admission
+# --------------------------------------------------------------------------
+
+def _check_topk(conf, capacity, label):
+    from gpu_helpers import gpu_topk
+    ln_o, n_o = oracle.schedule_topk(conf, int(capacity))
+    R, K = conf.shape
+    log(f"[schedule-topk] {label} R={R} K={K} capacity={int(capacity)} admitted={n_o}")
+    ln_g, cu_g, tok_g = gpu_topk(conf, capacity)
+    assert np.array_equal(ln_g, ln_o), (label, np.nonzero(ln_g != ln_o))
+    cu_o = oracle.cu_from_len(ln_o)
+    assert np.array_equal(cu_g, cu_o)
+    tok_o = np.full(R * (K + 1), -1, np.int32)
+    for r in range(R):
+        tok_o[cu_o[r]:cu_o[r + 1]] = r
+    assert np.array_equal(tok_g, tok_o)
+
+
+@pytest.mark.parametrize("name", synth.WORKLOAD_ORDER)
+def test_capacity_then_topk_workloads(name):
+    """The device capacity (no-break search on earlier confidences) is exact,
+    and the top-K admission that reads it on the device gives exact lengths,
+    cu_q and token markers, on every workload and 3 seeds."""
+    from gpu_helpers import gpu_capacity, gpu_topk
+    w = synth.WORKLOADS[name]
+    for seed in range(3):
+        case = guard.capacity_case(w, seed)
+        assert case.guarded
+        log(f"[schedule-capacity] {name}/seed{seed} capacity={case.capacity} "
+            f"margin={case.margin:.3g}")
+        cap_d = gpu_capacity(case.conf_prev, case.sps)
+        ln_g, cu_g, tok_g = gpu_topk(case.conf, cap_d)  # reads the capacity on the device
+        assert int(cap_d.item()) == case.capacity
+        assert np.array_equal(ln_g, case.len)
+        assert np.array_equal(cu_g, case.cu_q)
+        R, K = case.conf.shape
+        tok_o = np.full(R * (K + 1), -1, np.int32)
+        for r in range(R):
+            tok_o[case.cu_q[r]:case.cu_q[r + 1]] = r
+        assert np.array_equal(tok_g, tok_o)
+
+
+@pytest.mark.parametrize("name", synth.WORKLOAD_ORDER)
+def test_capacity_on_the_current_confidences_is_mode1(name):
+    from gpu_helpers import gpu_capacity, gpu_topk
+    w = synth.WORKLOADS[name]
+    case = guard.schedule_case(w, 0, mode=1)
+    assert case.sched_guarded
+    ln_g, cu_g, _ = gpu_topk(case.conf, gpu_capacity(case.conf, case.sps))
+    assert np.array_equal(ln_g, case.len)
+    assert np.array_equal(cu_g, case.cu_q)
+
+
+def test_capacity_appendix(appendix):
+    from gpu_helpers import gpu_capacity
+    sps = np.array([0.0, appendix["sps_1"], appendix["sps_2"], appendix["sps_3"]])
+    for c2, expect in ((appendix["case1_c2"], 2), (appendix["case2_c2"], 0)):
+        conf = np.array([[appendix["a_1"], c2]], np.float32)
+        assert int(gpu_capacity(conf, sps).item()) == expect
+
+
+def test_topk_edge_cases():
+    rng = np.random.default_rng(3)
+    conf = rng.uniform(0.0, 1.0, (37, 9)).astype(np.float32)
+    conf[1] = 0.0
+    conf[2, 4] = np.nan
+    conf[3, 0] = -1.0
+    conf[4, 5] = 1.5
+    n_pos = oracle.schedule_topk(conf, 10 ** 6)[1]
+    for cap in (0, -5, 1, 17, n_pos - 1, n_pos, n_pos + 1, 37 * 9, 2 ** 31 - 1):
+        _check_topk(conf, cap, f"capacity {cap}")
+    # ties everywhere: admission by request, then position
+    _check_topk(np.full((64, 8), 0.75, np.float32), 100, "ties")
+    # K = 0
+    _check_topk(np.zeros((5, 0), np.float32), 3, "K=0")
+
+
+@pytest.mark.parametrize("R,K", [(512, 16), (8192, 1), (1024, 8), (33, 7)])
+def test_topk_sizes(R, K):
+    """Largest candidate counts (R*K = 8192) and ragged sizes, at capacities
+    spread over the candidate count."""
+    w = synth.scaled(synth.WORKLOADS["highconc"], R=R, K=K, knee=R + R // 2)
+    conf = synth.confidences(w, 5)
+    for frac in (0.0, 0.1, 0.5, 0.97, 1.2):
+        _check_topk(conf, int(frac * R * K), f"R{R}K{K}")
