@@ -47,14 +47,17 @@ __device__ __forceinline__ int cu_q_total(const AttnArgs& a) {
     return t < 0 ? 0 : (t > mx ? mx : t);
 }
 
-// request owning flattened token `tok` (cu_q is non-decreasing)
-__device__ __forceinline__ int find_request(const int32_t* cu_q, int R, int tok) {
-    int lo = 0, hi = R - 1;
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (cu_q[mid] <= tok) lo = mid; else hi = mid - 1;
-    }
-    return lo;
+// Request r's first row q0, row count ql and context kv; false when the
+// request is malformed: ql outside [1, max_q], kv outside [ql, max_pages *
+// page], or rows outside [0, min(cu_q[R], R * max_q)).  The grid is indexed by
+// slot = r * max_q + t, so no token -> request search depends on cu_q being
+// ordered.
+__device__ __forceinline__ bool gen_request(const AttnArgs& a, int r, int& q0, int& ql, int& kv) {
+    q0 = a.cu_q[r];
+    ql = a.cu_q[r + 1] - q0;
+    kv = a.kv_len[r];
+    if (ql < 1 || ql > a.max_q || kv < ql || kv > a.max_pages * a.page) return false;
+    return q0 >= 0 && (int64_t)q0 + ql <= cu_q_total(a);
 }
 
 template <typename T>
@@ -66,14 +69,12 @@ __global__ __launch_bounds__(DSPARK_WAVE) void attn_generic_kernel(GenParams p) 
     const int s = (int)(b % p.splits); b /= p.splits;
     const int hb = (int)(b % p.nhb);   b /= p.nhb;
     const int g = (int)(b % a.Hkv);    b /= a.Hkv;
-    const int tok = (int)b;
-    const int total = cu_q_total(a);
-    if (tok >= total) return;
-    const int r = find_request(a.cu_q, a.R, tok);
-    const int ql = a.cu_q[r + 1] - a.cu_q[r];
-    const int kv = a.kv_len[r];
-    if (ql < 1 || ql > a.max_q || kv < ql || kv > a.max_pages * a.page) return;
-    const int t = tok - a.cu_q[r];
+    const int slot = (int)b;  // r * max_q + t
+    const int r = slot / a.max_q;
+    const int t = slot - r * a.max_q;
+    int q0, ql, kv;
+    if (!gen_request(a, r, q0, ql, kv) || t >= ql) return;
+    const int tok = q0 + t;
     const int visible = kv - ql + t + 1;
     const int h0 = g * p.group + hb * kGenHB;
     const int nh = min(kGenHB, p.group - hb * kGenHB);
@@ -149,9 +150,9 @@ __global__ __launch_bounds__(DSPARK_WAVE) void attn_generic_kernel(GenParams p) 
             }
         }
     }
-    // partial for (tok, h, s): [m, l, o[0..Dv)]
+    // partial for (slot, h, s): [m, l, o[0..Dv)]
     for (int hh = 0; hh < nh; ++hh) {
-        float* dst = p.part + (((int64_t)tok * a.Hq + h0 + hh) * p.splits + s) * (a.Dv + 2);
+        float* dst = p.part + (((int64_t)slot * a.Hq + h0 + hh) * p.splits + s) * (a.Dv + 2);
         if (lane == 0) { dst[0] = m[hh]; dst[1] = l[hh]; }
 #pragma unroll
         for (int e = 0; e < kGenDPL; ++e) {
@@ -164,15 +165,15 @@ __global__ __launch_bounds__(DSPARK_WAVE) void attn_generic_kernel(GenParams p) 
 template <typename T>
 __global__ __launch_bounds__(256) void attn_generic_merge(GenParams p) {
     const AttnArgs& a = p.a;
-    const int total = cu_q_total(a);
-    const int64_t row = (int64_t)blockIdx.x;  // (tok, h)
-    const int tok = (int)(row / a.Hq);
-    if (tok >= total) return;
-    const int r = find_request(a.cu_q, a.R, tok);
-    const int ql = a.cu_q[r + 1] - a.cu_q[r];
-    const int kv = a.kv_len[r];
-    if (ql < 1 || ql > a.max_q || kv < ql || kv > a.max_pages * a.page) return;
-    const float* src = p.part + row * p.splits * (a.Dv + 2);
+    const int64_t prow = (int64_t)blockIdx.x;  // (slot, h)
+    const int slot = (int)(prow / a.Hq);
+    const int h = (int)(prow - (int64_t)slot * a.Hq);
+    const int r = slot / a.max_q;
+    const int t = slot - r * a.max_q;
+    int q0, ql, kv;
+    if (!gen_request(a, r, q0, ql, kv) || t >= ql) return;
+    const int64_t row = (int64_t)(q0 + t) * a.Hq + h;  // output row (token, head)
+    const float* src = p.part + prow * p.splits * (a.Dv + 2);
     float M = -__builtin_huge_valf();
     for (int s = 0; s < p.splits; ++s) M = fmaxf(M, src[s * (a.Dv + 2)]);
     float L = 0.0f;
