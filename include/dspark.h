@@ -109,6 +109,24 @@ dspark_status dspark_schedule(const float* conf, int R, int K, const double* sps
                               dspark_stream stream);
 
 /* ------------------------------------------------------------------------
+ * Stage 1 without a workspace argument, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  Arguments, outputs, limits and errors are those of
+ * dspark_schedule.  The workspace is a fixed 98560-byte array in device memory
+ * (the workspace of the largest schedule the limits allow, R*K = 8192), one
+ * copy per GPU, held until the process ends; sizes needing more return
+ * DSPARK_EWORKSPACE.  The call allocates nothing (no hipMalloc, hipFree or
+ * allocating library routine); on its first call for a device it looks up the
+ * array's address on that device (the device of `stream`).  Every call on one
+ * GPU shares that GPU's array, so calls that may overlap on one GPU (two
+ * streams, or two host threads) race and must not be issued; calls ordered on
+ * one stream are safe.
+ * ---------------------------------------------------------------------- */
+dspark_status dspark_schedule_noalloc(const float* conf, int R, int K, const double* sps,
+                                      int64_t sps_len, int mode, int32_t* len, int32_t* cu_q,
+                                      int32_t* tok_req, dspark_stream stream);
+
+/* ------------------------------------------------------------------------
  * Stage 1, asynchronous form (the section on the hardware-aware prefix
  * scheduler in practice).  The candidates of the current step are ranked by
  * their current survival products exactly as in dspark_schedule; only the

@@ -5,6 +5,7 @@
 #include <stdio.h>
 
 #include <algorithm>
+#include <atomic>
 #include <string>
 
 #include "dspark.h"
@@ -156,6 +157,86 @@ dspark_status check_sched_ws(int R, int K, const void* ws, size_t ws_bytes) {
 }
 
 }  // namespace
+
+}  // extern "C"
+
+// ------------------------------------------------------------------ no-allocation scheduler
+
+namespace {
+
+// Scratch memory of dspark_schedule_noalloc: the scheduler workspace for the
+// largest schedule the ABI accepts (R*K = 8192 candidates), one copy on each
+// GPU the library runs on, held until the process ends.
+constexpr size_t kNoAllocScratchBytes = ((16 + 12 * (size_t)kMaxSchedCand) + 255) & ~(size_t)255;
+constexpr int kMaxDevices = 64;
+// Device address of `scratch` on each GPU, looked up once per device.
+std::atomic<void*> g_scratch_addr[kMaxDevices];
+
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+
+// Device address of `scratch` on `dev`, looked up with that device current.
+// The host-side name `scratch` is not a device address; only this value is
+// handed to kernels.
+dspark_status scratch_on(int dev, void** out) {
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(DSPARK_EUNSUPPORTED, "device %d outside [0, %d)", dev, kMaxDevices);
+    void* ptr = g_scratch_addr[dev].load(std::memory_order_acquire);
+    if (!ptr) {
+        int cur = 0;
+        hipError_t e = hipGetDevice(&cur);
+        if (e != hipSuccess) return hip_status(e, "hipGetDevice");
+        if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return hip_status(e, "hipSetDevice");
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (cur != dev) {
+            hipError_t e2 = hipSetDevice(cur);
+            if (e == hipSuccess) e = e2;
+        }
+        if (e != hipSuccess) return hip_status(e, "hipGetSymbolAddress(scratch)");
+        if (!ptr) return fail(DSPARK_EHIP, "hipGetSymbolAddress(scratch) returned null");
+        g_scratch_addr[dev].store(ptr, std::memory_order_release);
+    }
+    *out = ptr;
+    return DSPARK_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+dspark_status dspark_schedule_noalloc(const float* conf, int R, int K, const double* sps,
+                                      int64_t sps_len, int mode, int32_t* len, int32_t* cu_q,
+                                      int32_t* tok_req, dspark_stream stream) {
+    if (R < 1 || R > kMaxR) return fail(DSPARK_EINVAL, "R=%d outside [1, %d]", R, kMaxR);
+    if (K < 0 || K > kMaxK) return fail(DSPARK_EINVAL, "K=%d outside [0, %d]", K, kMaxK);
+    if ((int64_t)R * K > kMaxSchedCand)
+        return fail(DSPARK_EUNSUPPORTED, "R*K=%lld exceeds %d candidates", (long long)R * K,
+                    kMaxSchedCand);
+    if (mode != 0 && mode != 1) return fail(DSPARK_EINVAL, "mode=%d (0 or 1)", mode);
+    if (!len || !sps || (K > 0 && !conf)) return fail(DSPARK_EINVAL, "null conf/sps/len");
+    if (sps_len <= (int64_t)R * (K + 1))
+        return fail(DSPARK_ESHAPE, "sps_len=%lld must exceed R*(K+1)=%lld", (long long)sps_len,
+                    (long long)R * (K + 1));
+    if (!aligned(conf, 4) || !aligned(sps, 8) || !aligned(len, 4) || !aligned(cu_q, 4) ||
+        !aligned(tok_req, 4))
+        return fail(DSPARK_EINVAL, "misaligned pointer");
+    const size_t need = dspark::schedule_workspace(R, K);
+    if (need > kNoAllocScratchBytes)
+        return fail(DSPARK_EWORKSPACE, "needs %zu bytes of scratch; the fixed maximum is %zu",
+                    need, kNoAllocScratchBytes);
+    hipDevice_t dev = 0;
+    hipError_t e = hipStreamGetDevice((hipStream_t)stream, &dev);
+    if (e != hipSuccess) return hip_status(e, "hipStreamGetDevice");
+    void* ws = nullptr;
+    if (dspark_status st = scratch_on((int)dev, &ws)) return st;
+    // the scheduler writes every workspace value it reads, so nothing is cleared
+    return hip_status(dspark::launch_schedule(conf, R, K, sps, mode, nullptr, nullptr, len, cu_q,
+                                              tok_req, ws, (hipStream_t)stream),
+                      "dspark_schedule_noalloc");
+}
 
 dspark_status dspark_schedule_capacity(const float* conf_prev, int R, int K, const double* sps,
                                        int64_t sps_len, int32_t* capacity, void* ws,

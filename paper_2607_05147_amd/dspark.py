@@ -51,6 +51,8 @@ def lib():
         L.dspark_schedule_workspace_size.argtypes = [i32, i32]
         L.dspark_schedule.restype = i32
         L.dspark_schedule.argtypes = [p, i32, i32, p, i64, i32, p, p, p, p, sz, p]
+        L.dspark_schedule_noalloc.restype = i32
+        L.dspark_schedule_noalloc.argtypes = [p, i32, i32, p, i64, i32, p, p, p, p]
         L.dspark_schedule_capacity.restype = i32
         L.dspark_schedule_capacity.argtypes = [p, i32, i32, p, i64, p, p, sz, p]
         L.dspark_schedule_topk.restype = i32
@@ -158,6 +160,25 @@ def dspark_schedule(conf: torch.Tensor, sps: torch.Tensor, mode: int = 0,
     st = lib().dspark_schedule(_p(conf), R, K, _p(sps), sps.numel(), mode, _p(len_out), _p(cu_q),
                                _p(tok_req), _p(ws), ws_bytes, _stream(stream))
     _raise(st, "dspark_schedule")
+    return len_out, cu_q, tok_req
+
+
+def dspark_schedule_noalloc(conf: torch.Tensor, sps: torch.Tensor, mode: int,
+                            len_out: torch.Tensor, cu_q: torch.Tensor,
+                            tok_req: Optional[torch.Tensor] = None, stream=None):
+    """As dspark_schedule, with the library's fixed scratch array as workspace;
+    every output is the caller's (nothing is allocated)."""
+    _dev(conf, "conf", torch.float32)
+    if conf.dim() != 2:
+        raise DSparkError("conf must be [R, K]")
+    R, K = conf.shape
+    _dev(sps, "sps", torch.float64)
+    _dev(len_out, "len", torch.int32, (R,))
+    _dev(cu_q, "cu_q", torch.int32, (R + 1,))
+    _dev(tok_req, "tok_req", torch.int32, (R * (K + 1),), optional=True)
+    st = lib().dspark_schedule_noalloc(_p(conf), R, K, _p(sps), sps.numel(), mode, _p(len_out),
+                                       _p(cu_q), _p(tok_req), _stream(stream))
+    _raise(st, "dspark_schedule_noalloc")
     return len_out, cu_q, tok_req
 
 

@@ -71,6 +71,21 @@ def test_schedule_validation(L):
     assert _sched(L, conf=C.c_void_p((1 << 20) + 2)) == EINVAL  # misaligned
 
 
+def test_schedule_noalloc_validation(L):
+    def na(conf=FAKE, R=4, K=8, sps=FAKE, sps_len=100, mode=0, ln=FAKE):
+        return L.dspark_schedule_noalloc(conf, R, K, sps, sps_len, mode, ln, None, None, None)
+
+    assert na(conf=None) == EINVAL
+    assert na(sps=None) == EINVAL
+    assert na(ln=None) == EINVAL
+    assert na(R=0) == EINVAL
+    assert na(K=65) == EINVAL
+    assert na(mode=2) == EINVAL
+    assert na(sps_len=36) == ESHAPE
+    assert na(R=8192, K=2, sps_len=10**6) == EUNSUPPORTED
+    assert na(ln=C.c_void_p((1 << 20) + 2)) == EINVAL
+
+
 def test_schedule_capacity_validation(L):
     need = L.dspark_schedule_workspace_size(4, 8)
 
