@@ -55,12 +55,21 @@ def parse():
     ap.add_argument("--graph", action="store_true",
                     help="time the steps as replays of one captured HIP graph per input copy "
                          "instead of direct launches (--stage step; measured slower on this stack)")
+    ap.add_argument("--rate", action="store_true",
+                    help="also time dspark_accept with the analytic acceptance-rate output "
+                         "(stochastic workloads) and report its extra time and bytes")
+    ap.add_argument("--identity-pages", action="store_true",
+                    help="also time attention on a copy of the KV pool laid out in request and "
+                         "page order (identity block table) beside the shuffled pages")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy 10 times (calibrates the HBM counters)")
     ap.add_argument("--traffic-from", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV",
                                                         "COPY_WRITE_CSV"),
                     help="turn four rocprofv3 --pmc counter files (FETCH_SIZE and WRITE_SIZE of a bench "
                          "run, then of a --copy-probe run) into the committed traffic summary")
+    ap.add_argument("--traffic-group", default="attention", choices=["attention", "accept"],
+                    help="which launches --traffic-from summarises: one dspark_verify_attn call "
+                         "(or draft block with --stage draft), or one dspark_accept call")
     return ap.parse_args()
 
 
@@ -110,6 +119,10 @@ ATTN_PATHS = {
     "rnn_draft": {"src": "markov.hip", "kernels": ("md_hidden", "rnn_hproj", "md_first", "rnn_state",
                                                    "md_tile", "md_stats"),
                   "bound": "hbm"},
+    # not attention: the acceptance launches of one dspark_accept call (the
+    # resolve kernel runs once per call)
+    "accept": {"src": "accept.hip", "kernels": ("acc_resolve", "acc_rowpass", "acc_resid", "acc_draw"),
+               "bound": "hbm"},
 }
 
 
@@ -132,7 +145,9 @@ def path_of_workload(name: str) -> str:
     return attn_path(w, w.kv_elem_bytes == 2)
 
 
-def traffic_file(workload: str) -> str:
+def traffic_file(workload: str, group: str = "attention") -> str:
+    if group == "accept":
+        return os.path.join(HERE, "profiles", f"accept_{workload}_traffic.json")
     if workload == "draft":
         return os.path.join(HERE, "profiles", "markov_draft_serving_traffic.json")
     if workload == "rnn_draft":
@@ -157,12 +172,15 @@ def _counter_rows(path: str):
     return [(k[1], v) for k, v in per.items()]
 
 
-def traffic_from(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, workload="serving"):
-    """Per-call HBM traffic of dspark_verify_attn from FETCH_SIZE / WRITE_SIZE
-    (KiB per dispatch), each scaled by what the same counter reads for a plain
-    1 GiB device copy; written next to the other profile summaries."""
-    path = ATTN_PATHS[path_of_workload(workload)]
+def traffic_from(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, workload="serving",
+                 group="attention"):
+    """Per-call HBM traffic of dspark_verify_attn (or a draft block, or with
+    group "accept" of dspark_accept) from FETCH_SIZE / WRITE_SIZE (KiB per
+    dispatch), each scaled by what the same counter reads for a plain 1 GiB
+    device copy; written next to the other profile summaries."""
+    path = ATTN_PATHS["accept" if group == "accept" else path_of_workload(workload)]
     kernels = path["kernels"]
+    first = kernels[0] if group == "accept" else kernels[1]  # launched once per call
     def copy_scale(path):
         vals = [v for name, v in _counter_rows(path) if "copyBuffer" in name or "copy" in name.lower()]
         vals = [v for v in vals if v > 1e5]  # the 1 GiB copies
@@ -170,7 +188,7 @@ def traffic_from(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, workload=
 
     def per_call(path):
         rows = _counter_rows(path)
-        calls = sum(1 for name, _ in rows if kernels[1] in name)
+        calls = sum(1 for name, _ in rows if first in name)
         if workload in ("draft", "rnn_draft"):  # one md_first launch per call
             calls = sum(1 for name, _ in rows if "md_first" in name)
         tot = {k: sum(v for name, v in rows if k in name) for k in kernels}
@@ -183,6 +201,7 @@ def traffic_from(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, workload=
     write, _ = per_call(write_csv)
     out = {
         "workload": workload,
+        "group": group,
         "kernels": list(kernels),
         "calls": calls,
         "copy_scale": {"FETCH_SIZE": sf, "WRITE_SIZE": sw},
@@ -197,14 +216,16 @@ def traffic_from(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, workload=
             f"{sel} --steps 2 --warmup 1 --no-cpu-baseline",
             "rocprofv3 --pmc FETCH_SIZE --output-format csv -d <dir> -o pmc -- python bench.py --copy-probe",
             "rocprofv3 --pmc WRITE_SIZE --output-format csv -d <dir> -o pmc -- python bench.py --copy-probe",
-            f"python bench.py {sel} --traffic-from <the four pmc_counter_collection.csv files>",
+            f"python bench.py {sel} --traffic-group {group} --traffic-from <the four "
+            "pmc_counter_collection.csv files>",
         ],
     }
-    os.makedirs(os.path.dirname(traffic_file(workload)), exist_ok=True)
-    with open(traffic_file(workload), "w") as f:
+    dest = traffic_file(workload, group)
+    os.makedirs(os.path.dirname(dest), exist_ok=True)
+    with open(dest, "w") as f:
         json.dump(out, f, indent=1)
     log(f"traffic: {out['bytes_per_call'] / 1e9:.3f} GB per call (copy scale fetch {sf:.3f}, "
-        f"write {sw:.3f}) -> {traffic_file(workload)}")
+        f"write {sw:.3f}) -> {dest}")
 
 
 def measured_traffic(workload: str):
@@ -236,10 +257,11 @@ def copy_probe():
     log(f"copy probe: 10 copies of {n} bytes")
 
 
-def copy_ceiling():
+def device_copy_gbps():
     """Bandwidth of a plain device-to-device copy (1 GiB, read + write bytes,
-    best of ten), measured after the timed steps: the ceiling that a simple
-    streaming kernel reaches on this part, beside the 8 TB/s data-sheet peak."""
+    best of ten), measured after the timed steps.  A reference point for a
+    streaming kernel that reads and writes equal amounts, not a ceiling: a
+    read-mostly kernel such as attention can exceed it."""
     import torch
     n = 1 << 30
     a = torch.empty(n, dtype=torch.uint8, device="cuda:0")
@@ -261,7 +283,9 @@ def copy_ceiling():
 def main():
     args = parse()
     if args.traffic_from:
-        traffic_from(*args.traffic_from, workload=draft_key(args) if args.stage == "draft" else args.workload)
+        traffic_from(*args.traffic_from,
+                     workload=draft_key(args) if args.stage == "draft" else args.workload,
+                     group=args.traffic_group)
         return
     if args.copy_probe:
         copy_probe()
@@ -400,6 +424,15 @@ def main():
     attn_ms = np.array([e[1].elapsed_time(e[2]) for e in evs])
     acc_ms = np.array([e[2].elapsed_time(e[3]) for e in evs])
     ms_per_step = wall * 1e3 / args.steps
+    # per-step times from a third pass with one event at each step boundary
+    # (one event record per step, so each includes one record's idle gap)
+    bnd = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    bnd[0].record(stream)
+    for i in range(args.steps):
+        step(copies[i % NCOPY])
+        bnd[i + 1].record(stream)
+    torch.cuda.synchronize()
+    step_ms = np.array([bnd[i].elapsed_time(bnd[i + 1]) for i in range(args.steps)])
 
     ab = attention_bytes(w, kv.kv_len, q_len)
     path = attn_path(w, bf16)
@@ -410,6 +443,8 @@ def main():
     attn_gbps = ab / attn_s / 1e9
     both_gbps = (ab + cb) / (attn_s + acc_s) / 1e9
     attn_tflops = af / attn_s / 1e12
+    log(f"step: {ms_per_step * 1e3:.1f} us (wall mean), median {np.median(step_ms) * 1e3:.1f} us "
+        f"over {args.steps} event-bounded steps")
     log(f"per step: schedule {sched_ms.mean() * 1e3:.1f} us, attention {attn_ms.mean() * 1e3:.1f} us "
         f"({attn_gbps:.0f} GB/s, {attn_tflops:.1f} TFLOP/s), accept {acc_ms.mean() * 1e3:.1f} us; "
         f"attention+accept {both_gbps:.0f} GB/s = {both_gbps / HBM_PEAK_GBPS:.1%} of peak")
@@ -436,9 +471,17 @@ def main():
             "mean_q_len": float(q_len.mean()),
             "kv_tokens": int(kv.kv_len.sum()),
         },
+        "ms_per_step_median": float(np.median(step_ms)),
+        "timing": f"ms_per_step: wall clock over exactly {args.steps} steps / {args.steps}; "
+                  f"ms_per_step_median: median of {args.steps} steps bounded by HIP events "
+                  "(one event record per step); stages: HIP events between the stages in a "
+                  "separate pass, mean and median",
         "stages_us": {"schedule": float(sched_ms.mean() * 1e3),
                       "verify_attn": float(attn_ms.mean() * 1e3),
                       "accept": float(acc_ms.mean() * 1e3)},
+        "stages_us_median": {"schedule": float(np.median(sched_ms) * 1e3),
+                             "verify_attn": float(np.median(attn_ms) * 1e3),
+                             "accept": float(np.median(acc_ms) * 1e3)},
         "attn_accept_hbm": {"bytes": ab + cb, "achieved_gbps": both_gbps,
                             "frac_of_peak": both_gbps / HBM_PEAK_GBPS},
         "emitted_tokens_per_s": float((accepted + 1).sum()) / (ms_per_step / 1e3),
@@ -447,17 +490,101 @@ def main():
         # split-merge launches, bracketed together by the events)
         "roofline": roofline_entry(w.name, path, ab, af, attn_s),
     }
-    ceil = copy_ceiling()
-    result["copy_ceiling"] = {"what": "device-to-device copy of 1 GiB, read + write bytes, best of 10",
-                              "gbps": ceil, "attn_frac": attn_gbps / ceil,
-                              "attn_accept_frac": both_gbps / ceil}
-    log(f"copy ceiling {ceil:.0f} GB/s: attention at {attn_gbps / ceil:.1%} of it, "
-        f"attention+accept at {both_gbps / ceil:.1%}")
+    if args.rate and not w.greedy:
+        result["accept_rate"] = rate_timing(args, w, copies, ws_acc, stream, q_len, cb, acc_ms)
+    if args.identity_pages:
+        result["page_layout"] = page_layout_timing(args, w, kv, copies, ws_attn, stream, ab)
+    cp = device_copy_gbps()
+    result["device_copy"] = {"what": "device-to-device copy of 1 GiB, read + write bytes, best "
+                                     "of 10 (a reference point, not a ceiling)",
+                             "gbps": cp, "attn_ratio": attn_gbps / cp,
+                             "attn_accept_ratio": both_gbps / cp}
+    log(f"device copy {cp:.0f} GB/s: attention at {attn_gbps / cp:.2f}x of it, "
+        f"attention+accept at {both_gbps / cp:.2f}x")
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, seed, conf, sps, ln, kv, q, logits, dr,
                                               args.cpu_seconds)
     print(json.dumps(result), flush=True)
+
+
+def rate_timing(args, w, copies, ws_acc, stream, q_len, accept_nbytes, acc_ms):
+    """dspark_accept with the analytic acceptance-rate output (sum_v min(p_t,
+    p_d) of every tested row): its time beside the plain call, and the bytes
+    of the rate pass (it reads every tested logit row and its draft row
+    again, after the row statistics are known)."""
+    import torch
+    from paper_2607_05147_amd import dspark
+    rates = [torch.empty(int(q_len.sum()), dtype=torch.float32, device="cuda:0") for _ in copies]
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    for i in range(args.warmup + args.steps):
+        d = copies[i % NCOPY]
+        if i >= args.warmup:
+            evs[i - args.warmup][0].record(stream)
+        dspark.dspark_accept(d["tok"], d["logits"], d["cu"], draft_p=d["dp"], u=d["u"],
+                             accepted_len=d["acc"], next_tok=d["nxt"],
+                             accept_rate=rates[i % NCOPY], ws=ws_acc)
+        if i >= args.warmup:
+            evs[i - args.warmup][1].record(stream)
+    torch.cuda.synchronize()
+    ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    tested = int((q_len - 1).sum())
+    rate_bytes = tested * w.V * (w.logit_elem_bytes + 4)
+    extra_us = (np.median(ms) - np.median(acc_ms)) * 1e3
+    out = {"accept_with_rate_us_median": float(np.median(ms) * 1e3),
+           "accept_us_median": float(np.median(acc_ms) * 1e3),
+           "extra_us": float(extra_us),
+           "rate_pass_bytes": rate_bytes,
+           "rate_pass_gbps": rate_bytes / max(extra_us, 1e-3) / 1e3,
+           "tested_rows": tested}
+    log(f"accept with rate: {out['accept_with_rate_us_median']:.1f} us vs "
+        f"{out['accept_us_median']:.1f} us; rate pass {rate_bytes / 1e6:.0f} MB in "
+        f"{extra_us:.1f} us")
+    return out
+
+
+def page_layout_timing(args, w, kv, copies, ws_attn, stream, nbytes):
+    """Attention on the shuffled page pool against a copy laid out in request
+    and page order with an identity block table: the cost of page scatter."""
+    import torch
+    from paper_2607_05147_amd import dspark
+    bt = kv.block_table
+    npg = (kv.kv_len.astype(np.int64) + w.page - 1) // w.page
+    perm = np.concatenate([bt[r, :npg[r]] for r in range(w.R)]).astype(np.int64)
+    offs = np.concatenate([[0], np.cumsum(npg)])
+    bt_id = np.zeros_like(bt)
+    for r in range(w.R):
+        bt_id[r, :npg[r]] = np.arange(offs[r], offs[r + 1])
+    d0 = copies[0]
+    pages = int(d0["k"].numel() // kv.k_strides[0])
+    idx = torch.from_numpy(perm).to("cuda:0")
+    k_id = d0["k"].view(pages, -1).index_select(0, idx).reshape(-1)
+    v_id = k_id if w.mla else d0["v"].view(pages, -1).index_select(0, idx).reshape(-1)
+    bt_d = torch.from_numpy(bt_id).to("cuda:0")
+
+    def timed(k, v, btab):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+        for i in range(args.warmup + args.steps):
+            if i >= args.warmup:
+                evs[i - args.warmup][0].record(stream)
+            dspark.dspark_verify_attn(d0["q"], k, v, kv.k_strides, kv.v_strides, btab,
+                                      d0["kv_len"], d0["cu"], w.max_q, w.Hkv, w.Dv, w.page,
+                                      w.scale, out=d0["out"], ws=ws_attn)
+            if i >= args.warmup:
+                evs[i - args.warmup][1].record(stream)
+        torch.cuda.synchronize()
+        return float(np.median([e[0].elapsed_time(e[1]) for e in evs]) * 1e3)
+
+    sh = timed(d0["k"], d0["v"], d0["bt"])
+    ident = timed(k_id, v_id, bt_d)
+    del k_id, v_id
+    out = {"note": "one input copy in both runs (the KV is ~9x the 256 MB last-level cache)",
+           "shuffled_us_median": sh, "identity_us_median": ident,
+           "shuffled_gbps": nbytes / sh / 1e3, "identity_gbps": nbytes / ident / 1e3}
+    log(f"page layout: shuffled {sh:.1f} us, identity {ident:.1f} us")
+    return out
 
 
 def draft_bytes(w, rank: int, d: int, base_bytes: int) -> int:
