@@ -52,7 +52,11 @@ typedef enum {
     DSPARK_EHIP = 6          /* a HIP launch failed                           */
 } dspark_status;
 
-typedef enum { DSPARK_F32 = 0, DSPARK_BF16 = 1 } dspark_dtype;
+/* Element type codes.  The type is a plain 32-bit integer rather than an enum
+   so that any value a caller passes is well defined to read (an unknown code
+   is rejected with DSPARK_EDTYPE). */
+typedef int32_t dspark_dtype;
+enum { DSPARK_F32 = 0, DSPARK_BF16 = 1 };
 
 /* A hipStream_t, passed opaquely. */
 typedef void* dspark_stream;

@@ -7,8 +7,11 @@ takes sits at least a stated distance from a tie:
 * scheduler: every throughput comparison made satisfies
   |Theta - Theta_best| >= SCHED_GUARD * Theta_best.  The GPU sums the
   survival probabilities in a different order than the oracle's sequential
-  loop; for at most 4608 fp64 terms in [0, 1] the two sums differ by at most
-  about 1.1e-12 relative, so a 1e-9 band makes equal decisions certain.  (A
+  loop; for at most 8192 positive fp64 terms each order's relative error is
+  below 8192 * 2^-53 (about 9.1e-13), so the two differ by less than 2e-12,
+  and recomputing tau in the GPU's order at 8192 candidates measures 3.5e-15
+  (tests/test_oracle_schedule.py).  A 1e-9 band makes equal decisions
+  certain.  (A
   1e-4 band is unreachable here: the greedy stop happens exactly where the
   marginal throughput gain crosses zero, typically 1e-6..1e-9 from a tie.)
 * acceptance test: |u - min(1, p_t(x) / p_d(x))| >= ACCEPT_GUARD;

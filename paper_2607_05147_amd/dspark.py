@@ -38,10 +38,13 @@ def lib():
     """The loaded C library (raises if it has not been built)."""
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB_PATH):
-            raise DSparkError(f"{LIB_PATH} is missing: build it with "
+        # DSPARK_LIB: another build of the same library to load instead (the
+        # host-sanitizer test builds an instrumented copy)
+        path = os.environ.get("DSPARK_LIB") or LIB_PATH
+        if not os.path.exists(path):
+            raise DSparkError(f"{path} is missing: build it with "
                               "`python -m paper_2607_05147_amd.build` (no fallback path exists)")
-        L = C.CDLL(LIB_PATH)
+        L = C.CDLL(path)
         p, i32, i64, sz, f32 = C.c_void_p, C.c_int, C.c_int64, C.c_size_t, C.c_float
         L.dspark_abi_version.restype = i32
         L.dspark_abi_version.argtypes = []

@@ -330,3 +330,34 @@ def test_bonus_after_all_accepted_comes_from_row_l():
     acc, nxt, _, _ = oracle.accept(tok, p[None, :L], z, "f32", cu, L, V, u=u)
     assert acc[0] == L
     assert nxt[0] == (L + 4) % V
+
+
+def test_margins_are_in_units_of_the_total_mass():
+    """margin = the smallest distance of a decision from its tie: |u - min(1,
+    ratio)| for a test, and for a draw the distance of u * total from the
+    chosen bucket's edges divided by the total mass.  p_t = (0.1, 0.2, 0.3,
+    0.4), p_d uniform."""
+    p_t = np.array([0.1, 0.2, 0.3, 0.4])
+    z = np.log(p_t).astype(np.float32)
+    p_d = np.full((1, 1, 4), 0.25, np.float32)
+    cu = np.array([0, 2], np.int32)
+    rows = np.stack([z, z])
+    # draft 3: ratio 1.6 accepts; test margin |0.3 - 1| = 0.7; bonus draw at
+    # u = 0.25 lands in token 1's bucket [0.1, 0.3): margin 0.05
+    acc, nxt, mg, _ = oracle.accept(np.array([[3]], np.int32), p_d, rows, "f32", cu, 1, 4,
+                                    u=np.array([[0.3, 0.25]], np.float32))
+    assert acc.tolist() == [1] and nxt.tolist() == [1]
+    assert mg[0] == pytest.approx(0.05, abs=1e-6)
+    # draft 0: ratio 0.4, u = 0.5 rejects (test margin 0.1); residual masses
+    # (0, 0, 0.05, 0.15), total 0.2; u = 0.5 -> 0.1 of mass falls in token 3's
+    # bucket [0.05, 0.2): distances 0.05 and 0.1, i.e. 0.25 and 0.5 of the
+    # total; the request's margin is the test's 0.1
+    acc, nxt, mg, _ = oracle.accept(np.array([[0]], np.int32), p_d, rows, "f32", cu, 1, 4,
+                                    u=np.array([[0.5, 0.5]], np.float32))
+    assert acc.tolist() == [0] and nxt.tolist() == [3]
+    assert mg[0] == pytest.approx(0.1, abs=1e-6)
+    # the same draw with the test far from its tie (u = 0.95): the draw's 0.25
+    acc, nxt, mg, _ = oracle.accept(np.array([[0]], np.int32), p_d, rows, "f32", cu, 1, 4,
+                                    u=np.array([[0.95, 0.5]], np.float32))
+    assert acc.tolist() == [0] and nxt.tolist() == [3]
+    assert mg[0] == pytest.approx(0.25, abs=1e-6)

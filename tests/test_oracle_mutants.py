@@ -41,6 +41,12 @@ MUTANTS = {
     "schedule: snapshot of the admitted request only": (SCHED,
         "            for (int r = 0; r < R; ++r) len[r] = l[r]; /* snapshot l* <- l */",
         "            len[E[i].r] = E[i].j;"),
+    "schedule: margin in absolute throughput units": (SCHED,
+        "        double m = fabs(theta - theta_best) / theta_best;",
+        "        double m = fabs(theta - theta_best);"),
+    "accept: draw margin not divided by the total mass": (ACC,
+        "            double m1 = (thr - prev) / total, m2 = (cum - thr) / total;",
+        "            double m1 = thr - prev, m2 = cum - thr;"),
     "schedule capacity: taken from the search with the early stop": (SCHED,
         "    int rc = oracle_schedule(conf_prev, R, K, sps, sps_len, 1, len, NULL, &n_adm,",
         "    int rc = oracle_schedule(conf_prev, R, K, sps, sps_len, 0, len, NULL, &n_adm,"),

@@ -330,3 +330,69 @@ def test_capacity_is_the_brute_force_optimum_size(seed):
         pytest.skip("tied optimum")
     cap, _ = oracle.schedule_capacity(conf, sps)
     assert cap == scored[0][1]
+
+
+# --------------------------------------------------------------------------
+# guard margins and the GPU's summation order
+# --------------------------------------------------------------------------
+
+def test_min_margin_is_relative_to_the_best_throughput(appendix):
+    """The appendix's first comparison is Theta_1 = 0.9 against Theta_0 = 1.0,
+    a relative margin of 0.1; with the table doubled the absolute gap doubles
+    and the margin (relative) stays 0.1.  Mode 1 also compares Theta_2 = 1.134
+    (margin 0.134), so its minimum is still the first comparison's."""
+    base = [appendix["sps_1"], appendix["sps_2"], appendix["sps_3"]]
+    conf = np.array([[appendix["a_1"], appendix["case1_c2"]]], dtype=np.float32)
+    for scale in (1.0, 2.0, 0.25):
+        sps = _sps([scale * v for v in base])
+        for mode in (0, 1):
+            _, _, _, mm = oracle.schedule(conf, sps, mode)
+            assert mm == pytest.approx(0.1, abs=1e-7)
+    _, mm = oracle.schedule_capacity(conf, _sps(base))
+    assert mm == pytest.approx(0.1, abs=1e-7)
+
+
+def _tau_in_gpu_order(a_flat, R):
+    """tau_n as the scheduler kernel forms it: for candidate x, sixteen lanes
+    s = 0..15 each add (in increasing flat index y, y = s mod 16) the a_y that
+    come before x in the admission order, the sixteen partial sums are
+    combined by a butterfly (offsets 8, 4, 2, 1), then tau = R + (sum + a_x).
+    Sums are sequential fp64 additions (cumsum), one per element."""
+    N = a_flat.size
+    pad = (-N) % 16
+    a = np.concatenate([a_flat, np.zeros(pad)])
+    idx = np.arange(a.size)
+    out = np.empty(N)
+    for c0 in range(0, N, 256):
+        xs = np.arange(c0, min(N, c0 + 256))
+        ax = a_flat[xs][:, None]
+        before = np.where(idx[None, :] < xs[:, None], a[None, :] >= ax, a[None, :] > ax)
+        v = np.where(before & (idx[None, :] < N), a[None, :], 0.0)
+        lanes = np.cumsum(v.reshape(len(xs), -1, 16), axis=1)[:, -1, :]  # [x, 16]
+        for o in (8, 4, 2, 1):
+            lanes = lanes + lanes[:, np.arange(16) ^ o]
+        out[xs - c0 + c0] = R + (lanes[:, 0] + a_flat[xs])
+    return out
+
+
+def test_gpu_summation_order_stays_inside_the_guard_band():
+    """The guard band of the scheduler's parity cases (1e-9 relative) rests on
+    the GPU's summation order changing Theta by far less.  Recompute tau in
+    that order at the largest size (R*K = 8192) and compare every Theta_n
+    with the oracle's sequential one."""
+    from oracle import guard
+    w = synth.scaled(synth.WORKLOADS["highconc"], R=1024, K=8, knee=1536)
+    conf = synth.confidences(w, 7)
+    sps = synth.sps_table(w)
+    a = np.cumprod(np.clip(conf.astype(np.float64), 0, 1), axis=1).reshape(-1)
+    tau = _tau_in_gpu_order(a, w.R)
+    # position of each candidate in the admission order
+    order = np.lexsort((np.arange(a.size), -a))
+    order = order[a[order] > 0]
+    *_, trace = oracle.schedule(conf, sps, 1, trace=True)
+    n = np.arange(len(order))
+    theta_gpu = tau[order] * sps[w.R + n + 1]
+    rel = np.abs(theta_gpu - trace[1:]) / trace[1:]
+    assert len(order) == a.size == 8192
+    assert rel.max() <= 1e-11, rel.max()
+    assert rel.max() < guard.SCHED_GUARD / 100
