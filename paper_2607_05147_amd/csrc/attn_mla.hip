@@ -8,23 +8,29 @@
 // unlike the GQA path.
 //
 // Work item = (request r, KV head g, block of 64 rows, KV split s).  A
-// workgroup of four waves owns the block, one 16-row tile per wave (one wave
-// per SIMD); its query fragments stay in registers and its output
-// accumulators in the accumulation registers.  The split is walked in 32-key steps:
-//   * each step's 32 cache rows (36 KB) are copied into LDS with
-//     global_load_lds_dwordx4 (nine instructions per wave), into a ring of
-//     three buffers two steps ahead; LDS rows keep the 1152-byte cache pitch
-//     and the 16-byte chunks are swizzled (bits 0-2 of the chunk index XOR a
-//     function of the row, see pchunk) so that the score operand reads and the
-//     transposing value reads are free of bank conflicts while every read
-//     address stays a per-lane base plus an immediate;
-//   * S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (18 slices of the 576 dims,
-//     two key blocks: 36 products per wave and step);
-//   * softmax in exp2 units against a fixed per-row reference (the first
-//     step's maximum); a block whose scores outgrow it by more than 2^32
-//     runs again with the observed maxima (masks only at the diagonal);
-//   * O^T += V^T P^T with the values read by ds_read_b64_tr_b16 (32 blocks of
-//     16 dims: 32 products per wave and step).
+// workgroup of eight waves owns the block, two per SIMD, in two roles:
+//   * score waves (0-3) hold the query fragments of 32 rows each in
+//     registers and compute S^T = K Q^T for one 16-key block of every step
+//     with v_mfma_f32_16x16x32_bf16 (18 slices of the 576 dims), then the
+//     softmax in exp2 units against a fixed per-row reference (the first
+//     step's maximum; a block whose scores outgrow it by more than 2^32 runs
+//     again with the observed maxima; masks only at the diagonal) and the bf16
+//     probabilities, which go to the value waves through LDS;
+//   * value waves (4-7) own 128 output dims of all 64 rows in the
+//     accumulation registers, issue the step copies and compute
+//     O^T += V^T P^T with the values read by ds_read_b64_tr_b16.
+// Stage t runs the score waves on step t and the value waves on step t - 1,
+// so each SIMD holds one wave of each role: one wave's softmax and operand
+// waits run while the other's products keep the matrix core busy.  One LDS
+// barrier ends a stage.  The split is walked in 32-key steps; each step's 32
+// cache rows (36 KB) are copied into LDS with global_load_lds_dwordx4 (nine
+// instructions per value wave) into a ring of four buffers, two steps ahead
+// (a step is read by the score waves in stage t and by the value waves in
+// stage t + 1).  LDS rows keep the 1152-byte cache pitch and the 16-byte
+// chunks are swizzled (bits 0-2 of the chunk index XOR a function of the row,
+// see pchunk) so that the score operand reads and the transposing value reads
+// are free of bank conflicts while every read address stays a per-lane base
+// plus an immediate.
 // The row blocks of one (request, split) read the same keys: work items go to
 // eight queues, one per XCD (workgroup b runs on XCD b % 8), so those blocks
 // run side by side on one XCD and share its L2.  A workgroup whose queue is
@@ -48,25 +54,26 @@ typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
 
 constexpr int kDk = 576;
 constexpr int kDv = 512;
-constexpr int kThreads = 256;
-constexpr int kWaves = 4;
+constexpr int kThreads = 512;                       // 4 score waves + 4 value waves, two per SIMD
+constexpr int kSW = 4;                              // score waves 0..3, value waves 4..7
+constexpr int kVW = 4;
 constexpr int kRows = 64;                           // rows per work item: four 16-row tiles
 constexpr int kTilesPV = kRows / 16;                // tiles of the value product (all, per wave)
 constexpr int kSTiles = 2;                          // tiles of the score product per wave
 constexpr int kStep = 32;                           // keys per step
-constexpr int kRing = 3;                            // LDS buffers; copies run 2 steps ahead
+constexpr int kRing = 4;                            // step n sits in buffer n % 4; copies run 2 steps ahead
 constexpr int kChunks = kDk / 8;                    // 72 16-byte chunks of a cache row
 constexpr int kRowChunks = kChunks;                 // LDS row pitch in chunks (no pad: the swizzle spreads banks)
 constexpr int kRowB = kRowChunks * 16;              // 1152 bytes
 constexpr int kTileChunks = kStep * kRowChunks;     // 2304
 constexpr int kTileB = kTileChunks * 16;            // 36864 bytes
 constexpr int kInstr = kTileChunks / 64;            // 36 wave copy instructions per step
-constexpr int kCopies = kInstr / kWaves;            // 9 per wave: 8 whole rows
+constexpr int kCopies = kInstr / kVW;               // 9 per value wave: 8 whole rows
 constexpr int kSplit = 4096;                        // keys per split (the last one holds the rest)
 constexpr int kPageRegs = (kSplit / 64 + DSPARK_WAVE - 1) / DSPARK_WAVE;  // page-id registers per lane (pages >= 64 keys)
 constexpr int kKs = kDk / 32;                       // 18 slices of the score product
 constexpr int kDb = kDv / 16;                       // 32 blocks of output dims
-constexpr int kDbW = kDb / kWaves;                  // 8 blocks (128 dims) per wave
+constexpr int kDbW = kDb / kVW;                     // 8 blocks (128 dims) per value wave
 constexpr int kQueues = 8;                          // one per XCD
 constexpr int kBins = kSplit / kStep + 1;           // item lengths in steps: 0 .. kSplit / 32
 constexpr int kMergeRows = 4;                       // rows per merge item (64 threads per row)
@@ -77,7 +84,7 @@ constexpr int kSchedDsRead = 0x100;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kRange = 32.0f;  // scores may exceed a row's reference by this (log2 units)
-static_assert(kInstr == kWaves * kCopies && kCopies * 64 == 8 * kRowChunks, "copy split over the waves");
+static_assert(kInstr == kVW * kCopies && kCopies * 64 == 8 * kRowChunks, "copy split over the value waves");
 static_assert(kChunks % 8 == 0, "the swizzle permutes chunks within aligned groups of 8");
 static_assert(kPageRegs * DSPARK_WAVE * 64 >= kSplit, "page ids of a split fit the lanes");
 
@@ -341,56 +348,42 @@ __global__ __launch_bounds__(kPlanThreads) void mla_plan(Params p) {
 
 // ------------------------------------------------------------------ item
 
-// LDS beside the copy ring: the probability exchange of every step and the
-// per-row statistics the waves of a row pair combine.
+// LDS beside the copy ring: the probability exchange (double-buffered by step
+// parity) and the per-row statistics.
 struct Shared {
-    uint2 p[kTilesPV][2][DSPARK_WAVE];  // [row tile][key block][lane]: 4 bf16 probabilities
-    float mx[kWaves][kSTiles][16];      // row maxima (reference, observed maximum) per wave
-    float ls[kWaves][kSTiles][16];      // row sums per wave
-    int lim[kWaves];                    // per-wave minimum causal limit
+    uint2 p[2][kTilesPV][2][DSPARK_WAVE];  // [step parity][row tile][key block][lane]: 4 bf16
+    float mx[kSW][kSTiles][16];            // row maxima per score wave
+    float ls[kSW][kSTiles][16];            // row sums per score wave
+    int lim[kSW];                          // per-wave minimum causal limit
+    int item;                              // next work item (queue << 24 | index)
+    int flag;                              // some row outgrew its reference
 };
 
-__device__ __forceinline__ void item(const Params& p, const int r, const int g, const int rb,
-                                     const int s, const int q0, const int ql, const int kv,
-                                     const int nsplit, const uint32_t lds0, const int home,
-                                     int& nxt, int& s_flag, Shared& sh) {
+// Score role of one item (waves 0..3; sw = wave).  Barrier sequence per
+// attempt: B0, [X in stage 0 of the first attempt], one per stage for stages
+// 0 .. nsteps, then the two of the rerun check; the value role matches it.
+__device__ __forceinline__ void score_item(const Params& p, const int r, const int g, const int rb,
+                                           const int s, const int q0, const int ql, const int kv,
+                                           const int nsplit, const uint32_t lds0, const int home,
+                                           const int sw, int& nxt, Shared& sh) {
     const AttnArgs& a = p.a;
     constexpr int kSlotFloats = kRows * (kDv + 2);
     const int rows = ql * p.group;
     const int row0 = rb * kRows;
     int start, end;
     split_range(kv, s, start, end);
-
+    const int nsteps = (end - start + kStep - 1) / kStep;  // >= 1
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lr = lane & 15;
     const int lq = lane >> 4;
-    // Roles.  Scores: row tiles 2 hs and 2 hs + 1 (32 rows) against key block
-    // kb of every step (keys 8 i + 4 kb + 0..3), so each K fragment feeds two
-    // products.  Values: output dims [128 wave, 128 wave + 128) of all four row
-    // tiles, so each V fragment feeds four products; the probabilities of the
-    // other waves come through LDS.
-    const int hs = wave >> 1;
-    const int kb = wave & 1;
-    const int partner = wave ^ 1;  // same rows, the other key block
-
+    const int hs = sw >> 1;  // row tiles 2 hs, 2 hs + 1
+    const int kb = sw & 1;   // key block of every step
+    const int partner = sw ^ 1;
     const uint16_t* __restrict__ qg = (const uint16_t*)a.q;
-    const uint16_t* __restrict__ kc = (const uint16_t*)a.k;
 
-    // ---- page ids of the split, kPageRegs per lane
-    const int pg0 = start >> p.page_shift;
-    const int npg = ((end - 1) >> p.page_shift) - pg0 + 1;
-    int my_page[kPageRegs];
-#pragma unroll
-    for (int k = 0; k < kPageRegs; ++k) {
-        const int i = k * DSPARK_WAVE + lane;
-        my_page[k] = i < npg ? a.block_table[(int64_t)r * a.max_pages + pg0 + i] : 0;
-    }
-
-    // ---- query fragments (B operand of S^T = K Q^T) and causal limits of the
-    // two score tiles; rows past the block's end get zero queries (finite
-    // scores, outputs never stored)
+    // query fragments (B operand of S^T = K Q^T) and causal limits; rows past
+    // the block's end get zero queries (finite scores, outputs never stored)
     bf16x8 qf[kSTiles][kKs];
     int lim[kSTiles];
     int lim_min = 0x7fffffff;
@@ -411,121 +404,30 @@ __device__ __forceinline__ void item(const Params& p, const int r, const int g, 
             lim[j] = -1;
         }
     }
-    // The second tile's fragments live in the accumulation registers (the
-    // products read their B operand from there directly), which leaves the
-    // vector registers for the operand pipeline.
+    // the second tile's fragments live in the accumulation registers (free in
+    // this role; the products read their B operand from there directly)
 #pragma unroll
     for (int ks = 0; ks < kKs; ++ks) asm volatile("" : "+a"(qf[1][ks]));
-    // the whole block's minimum: steps below it need no masks
     lim_min = __reduce_min_sync(~0ull, lim_min);  // whole wave: a collective
-    if (lane == 0) sh.lim[wave] = lim_min;
-    __syncthreads();
-    lim_min = min(min(sh.lim[0], sh.lim[1]), min(sh.lim[2], sh.lim[3]));
+    if (lane == 0) sh.lim[sw] = lim_min;          // read after the attempt's first barrier
 
-    // Softmax reference per row: exp2 is taken relative to mref and the
-    // accumulators are never rescaled.  mref is the maximum of the item's first
-    // step over both key blocks (the two waves of a row pair exchange their
-    // halves), so both use the same reference.  fp32 holds the probabilities
-    // comfortably while scores stay below mref + kRange; if one goes above
-    // (mobs tracks the maximum), the item runs again with mref = the row's
-    // observed maximum.  Keeping the accumulators out of every VALU operation
-    // lets them stay in the accumulation registers.
-    f32x4 acc[kTilesPV][kDbW];
     float mref[kSTiles], mobs[kSTiles], lsum[kSTiles];
 #pragma unroll
     for (int j = 0; j < kSTiles; ++j) mref[j] = mobs[j] = -__builtin_huge_valf();
-    bool over = false;  // some row of this wave went above mref + kRange
+    bool over = false;
 
-    // ---- per-lane LDS offsets of the operand fragments (loop invariant)
-    // K (A operand): rows 8 (lr / 4) + 4 kb + lr % 4 (so that the score
-    // accumulator is the B operand of the value product), chunk 4 ks + lq;
-    // the swizzle sees ks only through its parity
-    uint32_t koff[2];  // [ks % 2], + 128 (ks / 2)
+    // K fragment offsets: rows 8 (lr / 4) + 4 kb + lr % 4, chunk 4 ks + lq
+    uint32_t koff[2];
 #pragma unroll
     for (int kp = 0; kp < 2; ++kp) {
         const int t = 8 * (lr >> 2) + 4 * kb + (lr & 3);
         koff[kp] = lds0 + t * kRowB + pchunk(t, 4 * kp + lq) * 16;
     }
-    // V^T (A operand of the value product, transposing reads): rows
-    // 8 lq + 4 h + lr / 4, chunk 2 db + (lr % 4) / 2, half lr % 2, for the
-    // wave's blocks db = 8 wave + d; the swizzle sees db only through db % 4
-    uint32_t voff[4][2];  // [d % 4][h], + 128 (d / 4)
-#pragma unroll
-    for (int dq = 0; dq < 4; ++dq)
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const int t = 8 * lq + 4 * h + (lr >> 2);
-            const int c = 2 * dq + ((lr & 3) >> 1);
-            voff[dq][h] = lds0 + t * kRowB + pchunk(t, c) * 16 + (lr & 1) * 8 + 256 * wave;
-        }
-    // probability fragments: this wave writes [2 hs + j][kb][lane], reads [ti][0 / 1][lane]
-    uint2* const pw0 = &sh.p[kSTiles * hs][kb][lane];
-    const uint2* const pr0 = &sh.p[0][0][lane];
-
-    // ---- copy geometry: this wave's copy instructions cover tile chunks
-    // p = (first + i) * 64 + lane, row p / 72, physical chunk p % 72
-    const int first = kCopies * wave;
-    // row and source chunk of copy i; the swizzle is an involution
-    auto cp_at = [&](int i, int ln, int& t, int& c) {
-        const int pp = (first + i) * 64 + ln;
-        t = pp / kRowChunks;
-        c = pchunk(t, pp - t * kRowChunks);
-    };
-    const int nsteps = (end - start + kStep - 1) / kStep;  // >= 1
-    const uint64_t kc_head = (uint64_t)(uintptr_t)kc + (uint64_t)((uint32_t)g * p.s1b);
-    const uint32_t lds_wave = __builtin_amdgcn_readfirstlane(lds0 + first * 1024);
-
-    auto page_of = [&](int idx) {
-        int pg = 0;
-#pragma unroll
-        for (int k = 0; k < kPageRegs; ++k)
-            if ((idx >> 6) == k) pg = __builtin_amdgcn_readlane(my_page[k], idx & 63);
-        return pg;
-    };
-    // byte offsets of the copies of a whole step from its first key row; they
-    // live in the accumulation registers (one read each per step) so that
-    // neither the geometry arithmetic nor nine vector registers are spent per step
-    uint32_t cpo[kCopies];
-#pragma unroll
-    for (int i = 0; i < kCopies; ++i) {
-        int t, c;
-        cp_at(i, lane, t, c);
-        cpo[i] = t * p.s2b + 16 * c;
-    }
-    auto issue = [&](int n) {
-        const int tok0 = start + n * kStep;
-        const int pidx = min((tok0 >> p.page_shift) - pg0, kPageRegs * DSPARK_WAVE - 1);
-        const int page = page_of(pidx);
-        const int slot0 = tok0 & ((1 << p.page_shift) - 1);
-        const uint32_t dst = lds_wave + ((unsigned)n % kRing) * kTileB;
-        if (tok0 + kStep <= end) {
-            const uint64_t kb = kc_head + (uint64_t)(uint32_t)page * p.s0b + (uint32_t)slot0 * p.s2b;
-#pragma unroll
-            for (int i = 0; i < kCopies; ++i) {
-                asm volatile("" : "+a"(cpo[i]));  // stays in (and is read from) an AGPR
-                lds_copy16_s(kb, cpo[i], dst + i * 1024);
-            }
-        } else {
-            int ln = lane;
-            asm volatile("" : "+v"(ln));
-            // last, partial step or past the end: keys at or past the end read the zero row
-            const uint16_t* kb = kc + (int64_t)page * a.ks[0] + (int64_t)g * a.ks[1];
-#pragma unroll
-            for (int i = 0; i < kCopies; ++i) {
-                int t, c;
-                cp_at(i, ln, t, c);
-                const bool in = tok0 + t < end;
-                const uint16_t* src = in ? kb + (int64_t)(slot0 + t) * a.ks[2] + 8 * c : g_zero_row + 8 * c;
-                lds_copy16(src, dst + i * 1024);
-            }
-        }
-    };
 
     auto compute = [&](int n, bool first_step, auto bufc) {
         constexpr unsigned buf = decltype(bufc)::value;
         constexpr uint32_t boff = buf * kTileB;
         const int tok0 = start + n * kStep;
-        // ---- scores S^T[key, row] of the two tiles: four accumulation chains
         f32x4 sc[kSTiles][2];
 #pragma unroll
         for (int j = 0; j < kSTiles; ++j) sc[j][0] = sc[j][1] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -537,7 +439,6 @@ __device__ __forceinline__ void item(const Params& p, const int r, const int g, 
             for (int j = 0; j < kSTiles; ++j)
                 sc[j][ks & 1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[j][ks], sc[j][ks & 1], 0, 0, 0);
         }
-        // software pipeline: kAheadK fragment reads in flight ahead of the products
         __builtin_amdgcn_sched_group_barrier(kSchedDsRead, kAheadK, 0);
 #pragma unroll
         for (int i = 0; i < kKs - kAheadK; ++i) {
@@ -547,7 +448,7 @@ __device__ __forceinline__ void item(const Params& p, const int r, const int g, 
         __builtin_amdgcn_sched_group_barrier(kSchedMfma, kSTiles * kAheadK, 0);
         __builtin_amdgcn_sched_barrier(0);
 
-        // ---- softmax over this wave's keys: tok0 + 8 lq + 4 kb + e
+        // softmax over this wave's keys tok0 + 8 lq + 4 kb + e
         const bool full = tok0 + kStep <= end && tok0 + kStep - 1 <= lim_min;
         float sv[kSTiles][4], bm[kSTiles];
 #pragma unroll
@@ -568,16 +469,15 @@ __device__ __forceinline__ void item(const Params& p, const int r, const int g, 
             // the reference: the first step's maximum over both key blocks
             if (lq == 0) {
 #pragma unroll
-                for (int j = 0; j < kSTiles; ++j) sh.mx[wave][j][lr] = bm[j];
+                for (int j = 0; j < kSTiles; ++j) sh.mx[sw][j][lr] = bm[j];
             }
-            lds_barrier();
+            lds_barrier();  // X
 #pragma unroll
             for (int j = 0; j < kSTiles; ++j) mref[j] = vmax(bm[j], sh.mx[partner][j][lr]);
         }
+        uint2* const pw = &sh.p[buf & 1][kSTiles * hs][kb][lane];
 #pragma unroll
         for (int j = 0; j < kSTiles; ++j) {
-            // rows with no visible key yet (only rows past the block's end can
-            // see keys later): take the first finite maximum
             if (mref[j] == -__builtin_huge_valf()) mref[j] = bm[j];
             over |= bm[j] > mref[j] + kRange;
             const float mu = mref[j] == -__builtin_huge_valf() ? 0.0f : mref[j];
@@ -585,12 +485,178 @@ __device__ __forceinline__ void item(const Params& p, const int r, const int g, 
 #pragma unroll
             for (int e = 0; e < 4; ++e) pr[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[j][e], p.scale2, -mu));
             lsum[j] += (pr[0] + pr[1]) + (pr[2] + pr[3]);
-            pw0[j * 2 * DSPARK_WAVE] = uint2{cvt_pk_bf16(pr[0], pr[1]), cvt_pk_bf16(pr[2], pr[3])};
+            pw[j * 2 * DSPARK_WAVE] = uint2{cvt_pk_bf16(pr[0], pr[1]), cvt_pk_bf16(pr[2], pr[3])};
         }
-        lds_barrier();  // every wave's probabilities visible
+    };
 
-        // ---- O^T[d, row] += V^T P^T for dims [128 wave, +128) of all four tiles
+    const int claim = max(nsteps - 3, 0);
+    for (int attempt = 0;; ++attempt) {
+#pragma unroll
+        for (int j = 0; j < kSTiles; ++j) lsum[j] = 0.0f;
+        lds_barrier();  // B0: step 0 in LDS; sh.lim written
+        if (attempt == 0) lim_min = min(min(sh.lim[0], sh.lim[1]), min(sh.lim[2], sh.lim[3]));
+        auto one = [&](int n, auto bufc) {
+            if (n == claim && tid == 0 && attempt == 0) nxt = atomicAdd(p.head + home, 1);
+            compute(n, n == 0 && attempt == 0, bufc);
+            lds_barrier();  // end of stage n
+        };
+        for (int n = 0; n < nsteps; n += kRing) {
+            one(n, std::integral_constant<unsigned, 0>{});
+            if (n + 1 < nsteps) one(n + 1, std::integral_constant<unsigned, 1>{});
+            if (n + 2 < nsteps) one(n + 2, std::integral_constant<unsigned, 2>{});
+            if (n + 3 < nsteps) one(n + 3, std::integral_constant<unsigned, 3>{});
+        }
+        lds_barrier();  // end of stage nsteps (the value waves' last product)
+        // rerun check: did any row outgrow its reference?  (ballot on the whole wave)
+        const bool any_over = __builtin_amdgcn_ballot_w64(over) != 0;
+        if (lane == 0 && any_over) atomicOr(&sh.flag, 1);
+        if (lq == 0) {
+#pragma unroll
+            for (int j = 0; j < kSTiles; ++j) sh.mx[sw][j][lr] = mobs[j];
+        }
+        __syncthreads();
+        const int again = sh.flag;
+        float mnext[kSTiles];
+#pragma unroll
+        for (int j = 0; j < kSTiles; ++j) mnext[j] = vmax(mobs[j], sh.mx[partner][j][lr]);
+        __syncthreads();
+        if (!again) break;
+        if (tid == 0) sh.flag = 0;
+#pragma unroll
+        for (int j = 0; j < kSTiles; ++j) mref[j] = mnext[j];
+        over = false;
+    }
+
+    // row sums over the four lanes of a row; the pair's halves are added by the readers
+#pragma unroll
+    for (int j = 0; j < kSTiles; ++j) {
+        lsum[j] += __shfl_xor(lsum[j], 16, 64);
+        lsum[j] += __shfl_xor(lsum[j], 32, 64);
+    }
+    if (lq == 0) {
+#pragma unroll
+        for (int j = 0; j < kSTiles; ++j) sh.ls[sw][j][lr] = lsum[j];
+    }
+    __syncthreads();  // F: the value waves read the sums next
+    if (kb != 0 || lq != 0) return;
+    // waves 0 and 2 write the statistics of their two row tiles
+#pragma unroll
+    for (int j = 0; j < kSTiles; ++j) {
+        const int rr = 16 * (kSTiles * hs + j) + lr;
+        if (row0 + rr >= rows) continue;
+        const float L = sh.ls[sw][j][lr] + sh.ls[partner][j][lr];
+        if (nsplit == 1) {
+            if (a.lse) {
+                const int row = row0 + rr;
+                const int t = row / p.group;
+                const int h = g * p.group + (row - t * p.group);
+                a.lse[(int64_t)(q0 + t) * a.Hq + h] = (mref[j] + log2f(L)) * kLn2;
+            }
+        } else {
+            float* part = p.part + (((int64_t)(r * a.Hkv + g) * p.rb_max + rb) * p.max_splits + s) * kSlotFloats;
+            part[rr] = mref[j];
+            part[kRows + rr] = L;
+        }
+    }
+}
+
+// Value role of one item (waves 4..7; vw = wave - 4): the copies and the
+// value product, on the score role's barrier sequence.
+__device__ __forceinline__ void value_item(const Params& p, const int r, const int g, const int rb,
+                                           const int s, const int q0, const int ql, const int kv,
+                                           const int nsplit, const uint32_t lds0, const int vw,
+                                           Shared& sh) {
+    const AttnArgs& a = p.a;
+    constexpr int kSlotFloats = kRows * (kDv + 2);
+    const int rows = ql * p.group;
+    const int row0 = rb * kRows;
+    int start, end;
+    split_range(kv, s, start, end);
+    const int nsteps = (end - start + kStep - 1) / kStep;  // >= 1
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int lr = lane & 15;
+    const int lq = lane >> 4;
+    const uint16_t* __restrict__ kc = (const uint16_t*)a.k;
+
+    // page ids of the split, kPageRegs per lane
+    const int pg0 = start >> p.page_shift;
+    const int npg = ((end - 1) >> p.page_shift) - pg0 + 1;
+    int my_page[kPageRegs];
+#pragma unroll
+    for (int k = 0; k < kPageRegs; ++k) {
+        const int i = k * DSPARK_WAVE + lane;
+        my_page[k] = i < npg ? a.block_table[(int64_t)r * a.max_pages + pg0 + i] : 0;
+    }
+
+    // V^T fragment offsets (transposing reads): rows 8 lq + 4 h + lr / 4, chunk
+    // 2 db + (lr % 4) / 2, half lr % 2, for this wave's blocks db = 8 vw + d
+    uint32_t voff[4][2];
+#pragma unroll
+    for (int dq = 0; dq < 4; ++dq)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int t = 8 * lq + 4 * h + (lr >> 2);
+            const int c = 2 * dq + ((lr & 3) >> 1);
+            voff[dq][h] = lds0 + t * kRowB + pchunk(t, c) * 16 + (lr & 1) * 8 + 256 * vw;
+        }
+
+    // copy geometry: this wave's copy instructions cover tile chunks
+    // (first + i) * 64 + lane, row / 72, physical chunk % 72
+    const int first = kCopies * vw;
+    auto cp_at = [&](int i, int ln, int& t, int& c) {
+        const int pp_ = (first + i) * 64 + ln;
+        t = pp_ / kRowChunks;
+        c = pchunk(t, pp_ - t * kRowChunks);
+    };
+    const uint64_t kc_head = (uint64_t)(uintptr_t)kc + (uint64_t)((uint32_t)g * p.s1b);
+    const uint32_t lds_wave = __builtin_amdgcn_readfirstlane(lds0 + first * 1024);
+    auto page_of = [&](int idx) {
+        int pg = 0;
+#pragma unroll
+        for (int k = 0; k < kPageRegs; ++k)
+            if ((idx >> 6) == k) pg = __builtin_amdgcn_readlane(my_page[k], idx & 63);
+        return pg;
+    };
+    uint32_t cpo[kCopies];
+#pragma unroll
+    for (int i = 0; i < kCopies; ++i) {
+        int t, c;
+        cp_at(i, lane, t, c);
+        cpo[i] = t * p.s2b + 16 * c;
+    }
+    auto issue = [&](int n) {
+        const int tok0 = start + n * kStep;
+        const int pidx = min(max((tok0 >> p.page_shift) - pg0, 0), kPageRegs * DSPARK_WAVE - 1);
+        const int page = page_of(pidx);
+        const int slot0 = tok0 & ((1 << p.page_shift) - 1);
+        const uint32_t dst = lds_wave + ((unsigned)n % kRing) * kTileB;
+        if (tok0 + kStep <= end) {
+            const uint64_t kbase = kc_head + (uint64_t)(uint32_t)page * p.s0b + (uint32_t)slot0 * p.s2b;
+#pragma unroll
+            for (int i = 0; i < kCopies; ++i) lds_copy16_s(kbase, cpo[i], dst + i * 1024);
+        } else {
+            int ln = lane;
+            asm volatile("" : "+v"(ln));
+            // last, partial step or past the end: keys at or past the end read the zero row
+            const uint16_t* kbase = kc + (int64_t)page * a.ks[0] + (int64_t)g * a.ks[1];
+#pragma unroll
+            for (int i = 0; i < kCopies; ++i) {
+                int t, c;
+                cp_at(i, ln, t, c);
+                const bool in = tok0 + t < end;
+                const uint16_t* src = in ? kbase + (int64_t)(slot0 + t) * a.ks[2] + 8 * c : g_zero_row + 8 * c;
+                lds_copy16(src, dst + i * 1024);
+            }
+        }
+    };
+
+    f32x4 acc[kTilesPV][kDbW];
+    auto product = [&](auto bufc) {
+        constexpr unsigned buf = decltype(bufc)::value;
+        constexpr uint32_t boff = buf * kTileB;
         __builtin_amdgcn_sched_barrier(0);
+        const uint2* const pr0 = &sh.p[buf & 1][0][0][lane];
         bf16x8 pf[kTilesPV];
 #pragma unroll
         for (int ti = 0; ti < kTilesPV; ++ti) {
@@ -610,8 +676,6 @@ __device__ __forceinline__ void item(const Params& p, const int r, const int g, 
             for (int ti = 0; ti < kTilesPV; ++ti)
                 acc[ti][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[ti], acc[ti][d], 0, 0, 0);
         }
-        // software pipeline: the probability reads, then two transposing reads
-        // per four products with kAheadV reads in flight
         __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2 * kTilesPV + kAheadV, 0);
 #pragma unroll
         for (int i = 0; i < kDbW - kAheadV / 2; ++i) {
@@ -622,73 +686,52 @@ __device__ __forceinline__ void item(const Params& p, const int r, const int g, 
         __builtin_amdgcn_sched_barrier(0);
     };
 
-    // ---- main loop: every thread issues kCopies copies per step, in order, also
-    // past the last step (zero-row copies into buffers not read again), so
-    // "step n has landed" is vmcnt <= (kRing - 2) * kCopies.
-    const int claim = max(nsteps - 3, 0);
     for (int attempt = 0;; ++attempt) {
-#pragma unroll
-        for (int j = 0; j < kSTiles; ++j) lsum[j] = 0.0f;
+        // the accumulators live in the accumulation registers (the score role
+        // keeps its second query tile there; this role's vector registers hold
+        // the operand pipeline)
 #pragma unroll
         for (int ti = 0; ti < kTilesPV; ++ti)
 #pragma unroll
-            for (int d = 0; d < kDbW; ++d) acc[ti][d] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int d = 0; d < kDbW; ++d) {
+                acc[ti][d] = f32x4{0.f, 0.f, 0.f, 0.f};
+                asm volatile("" : "+a"(acc[ti][d]));
+            }
+        // every thread issues kCopies copies per step, in order, also past the
+        // last step (zero-row copies into buffers not read again), so "step n
+        // has landed" is vmcnt <= kCopies once step n + 1 is issued
         wait_vmcnt<0>();
-#pragma unroll
-        for (int n = 0; n < kRing - 1; ++n) issue(n);
-        auto one = [&](int n, auto bufc) {
-            wait_vmcnt<(kRing - 2) * kCopies>();
-            lds_barrier();  // step n visible to all; everyone is done with step n - 1
-            if (n == claim && tid == 0 && attempt == 0) nxt = atomicAdd(p.head + home, 1);
-            issue(n + kRing - 1);
-            compute(n, n == 0 && attempt == 0, bufc);
+        issue(0);
+        issue(1);
+        wait_vmcnt<kCopies>();
+        lds_barrier();  // B0
+        // stage t: copies of step t + 2, then the product of step t - 1
+        auto one = [&](int t, auto bufc) {
+            issue(t + 2);
+            if (t == 0 && attempt == 0) lds_barrier();  // X (the score waves' reference exchange)
+            if (t >= 1) product(bufc);
+            wait_vmcnt<kCopies>();  // step t + 1 has landed
+            lds_barrier();          // end of stage t
         };
-        for (int n = 0; n < nsteps; n += kRing) {
-            one(n, std::integral_constant<unsigned, 0>{});
-            if (n + 1 < nsteps) one(n + 1, std::integral_constant<unsigned, 1>{});
-            if (n + 2 < nsteps) one(n + 2, std::integral_constant<unsigned, 2>{});
+        for (int t = 0; t <= nsteps; t += kRing) {
+            // stage t reads step t - 1, in buffer (t - 1) % 4
+            one(t, std::integral_constant<unsigned, 3>{});
+            if (t + 1 <= nsteps) one(t + 1, std::integral_constant<unsigned, 0>{});
+            if (t + 2 <= nsteps) one(t + 2, std::integral_constant<unsigned, 1>{});
+            if (t + 3 <= nsteps) one(t + 3, std::integral_constant<unsigned, 2>{});
         }
         wait_vmcnt<0>();
-        // did any row of the block outgrow its reference?  (all waves agree)
-        // (the ballot runs on the whole wave, outside the lane condition)
-        const bool any_over = __builtin_amdgcn_ballot_w64(over) != 0;
-        if (lane == 0 && any_over) atomicOr(&s_flag, 1);
-        if (lq == 0) {
-#pragma unroll
-            for (int j = 0; j < kSTiles; ++j) sh.mx[wave][j][lr] = mobs[j];
-        }
         __syncthreads();
-        const int again = s_flag;
-        float mnext[kSTiles];
-#pragma unroll
-        for (int j = 0; j < kSTiles; ++j) mnext[j] = vmax(mobs[j], sh.mx[partner][j][lr]);
+        const int again = sh.flag;
         __syncthreads();
         if (!again) break;
-        if (tid == 0) s_flag = 0;
-#pragma unroll
-        for (int j = 0; j < kSTiles; ++j) mref[j] = mnext[j];
-        over = false;
     }
 
-    // ---- finish rows: l over the four lanes of a row and the two key blocks
-#pragma unroll
-    for (int j = 0; j < kSTiles; ++j) {
-        lsum[j] += __shfl_xor(lsum[j], 16, 64);
-        lsum[j] += __shfl_xor(lsum[j], 32, 64);
-    }
-    if (lq == 0) {
-#pragma unroll
-        for (int j = 0; j < kSTiles; ++j) {
-            sh.ls[wave][j][lr] = lsum[j];
-            sh.mx[wave][j][lr] = mref[j];
-        }
-    }
-    __syncthreads();
-    float M[kTilesPV], L[kTilesPV];
+    __syncthreads();  // F: the score waves' row sums are in LDS
+    float L[kTilesPV];
 #pragma unroll
     for (int ti = 0; ti < kTilesPV; ++ti) {
         const int w0 = 2 * (ti / kSTiles);
-        M[ti] = sh.mx[w0][ti % kSTiles][lr];
         L[ti] = sh.ls[w0][ti % kSTiles][lr] + sh.ls[w0 + 1][ti % kSTiles][lr];
     }
     if (nsplit == 1) {
@@ -706,9 +749,8 @@ __device__ __forceinline__ void item(const Params& p, const int r, const int g, 
                     uint2 pk;
                     pk.x = pack2_bf16(acc[ti][d][0] * inv, acc[ti][d][1] * inv);
                     pk.y = pack2_bf16(acc[ti][d][2] * inv, acc[ti][d][3] * inv);
-                    *(uint2*)(outp + orow * kDv + 16 * (kDbW * wave + d) + 4 * lq) = pk;
+                    *(uint2*)(outp + orow * kDv + 16 * (kDbW * vw + d) + 4 * lq) = pk;
                 }
-                if (a.lse && wave == 0 && lq == 0) a.lse[orow] = (M[ti] + log2f(L[ti])) * kLn2;
             }
         }
         return;
@@ -718,29 +760,22 @@ __device__ __forceinline__ void item(const Params& p, const int r, const int g, 
     for (int ti = 0; ti < kTilesPV; ++ti) {
         const int rr = 16 * ti + lr;
         if (row0 + rr < rows) {
-            if (wave == 0 && lq == 0) {
-                part[rr] = M[ti];
-                part[kRows + rr] = L[ti];
-            }
 #pragma unroll
             for (int d = 0; d < kDbW; ++d)
-                *(f32x4*)(part + 2 * kRows + rr * kDv + 16 * (kDbW * wave + d) + 4 * lq) = acc[ti][d];
+                *(f32x4*)(part + 2 * kRows + rr * kDv + 16 * (kDbW * vw + d) + 4 * lq) = acc[ti][d];
         }
     }
 }
 
-// Persistent workgroups: workgroup b serves queue b % 8 (its XCD), then the others.
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void mla_kernel(Params p) {
+// Persistent workgroups of eight waves: workgroup b serves queue b % 8 (its
+// XCD), then the others.  Each role runs its own item loop; the loops meet at
+// the same barriers.
+__global__ __launch_bounds__(kThreads) void mla_kernel(Params p) {
     __shared__ __align__(16) unsigned char lds[kRing * kTileB];
-    __shared__ int s_item;
-    __shared__ int s_flag;
     __shared__ Shared sh;
-    if (threadIdx.x == 0) s_flag = 0;
     uint32_t lds0 = (uint32_t)(uintptr_t)&lds[0];
     asm volatile("" : "+s"(lds0));
     const int home0 = blockIdx.x % kQueues;
-    // claim an item: the home queue first, then the others in turn
     auto claim_any = [&](int q_first) {
         for (int k = 0; k < kQueues; ++k) {
             const int q = (q_first + k) % kQueues;
@@ -749,24 +784,40 @@ void mla_kernel(Params p) {
         }
         return -1;
     };
-    if (threadIdx.x == 0) s_item = claim_any(home0);
+    if (threadIdx.x == 0) {
+        sh.flag = 0;
+        sh.item = claim_any(home0);
+    }
     __syncthreads();
-    int cur = __builtin_amdgcn_readfirstlane(s_item);
-    while (cur >= 0) {
-        const int q = cur >> 24;
-        const int it = p.head[kQueues + q] + (cur & 0xffffff);
-        const int4 e0 = p.list[2 * it];
-        const int4 e1 = p.list[2 * it + 1];
-        int nxt = 0;  // index claimed from queue q near the end of the item
-        item(p, e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w, lds0, q, nxt, s_flag, sh);
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            // the claim near the end came from queue q; past its end, look elsewhere
-            s_item = p.head[kQueues + q] + nxt < p.head[2 * kQueues + q] ? (q << 24) | nxt
-                                                                          : claim_any(q + 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    int cur = __builtin_amdgcn_readfirstlane(sh.item);
+    if (wave < kSW) {
+        while (cur >= 0) {
+            const int q = cur >> 24;
+            const int it = p.head[kQueues + q] + (cur & 0xffffff);
+            const int4 e0 = p.list[2 * it];
+            const int4 e1 = p.list[2 * it + 1];
+            int nxt = 0;  // index claimed from queue q near the end of the item (thread 0)
+            score_item(p, e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w, lds0, q, wave, nxt, sh);
+            __syncthreads();
+            if (threadIdx.x == 0) {
+                sh.item = p.head[kQueues + q] + nxt < p.head[2 * kQueues + q] ? (q << 24) | nxt
+                                                                               : claim_any(q + 1);
+            }
+            __syncthreads();
+            cur = __builtin_amdgcn_readfirstlane(sh.item);
         }
-        __syncthreads();
-        cur = __builtin_amdgcn_readfirstlane(s_item);
+    } else {
+        while (cur >= 0) {
+            const int q = cur >> 24;
+            const int it = p.head[kQueues + q] + (cur & 0xffffff);
+            const int4 e0 = p.list[2 * it];
+            const int4 e1 = p.list[2 * it + 1];
+            value_item(p, e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w, lds0, wave - kSW, sh);
+            __syncthreads();
+            __syncthreads();
+            cur = __builtin_amdgcn_readfirstlane(sh.item);
+        }
     }
 }
 
@@ -888,7 +939,7 @@ hipError_t launch_attn_mla(const AttnArgs& a, void* ws, hipStream_t s) {
     e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
-    // one workgroup per CU (114 KB of LDS, one wave per SIMD)
+    // one workgroup per CU (157 KB of LDS, eight waves: two per SIMD)
     const int64_t grid = std::min<int64_t>(cus, std::max<int64_t>(g.n_items, 1));
     hipLaunchKernelGGL(mla::mla_kernel, dim3((unsigned)grid), dim3(mla::kThreads), 0, s, p);
     e = hipGetLastError();
