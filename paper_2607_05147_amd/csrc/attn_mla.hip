@@ -69,7 +69,7 @@ constexpr int kTileChunks = kStep * kRowChunks;     // 2304
 constexpr int kTileB = kTileChunks * 16;            // 36864 bytes
 constexpr int kInstr = kTileChunks / 64;            // 36 wave copy instructions per step
 constexpr int kCopies = kInstr / kVW;               // 9 per value wave: 8 whole rows
-constexpr int kSplit = 4096;                        // keys per split (the last one holds the rest)
+constexpr int kSplit = 8192;                        // keys per split (the last one holds the rest)
 constexpr int kPageRegs = (kSplit / 64 + DSPARK_WAVE - 1) / DSPARK_WAVE;  // page-id registers per lane (pages >= 64 keys)
 constexpr int kKs = kDk / 32;                       // 18 slices of the score product
 constexpr int kDb = kDv / 16;                       // 32 blocks of output dims
@@ -411,7 +411,9 @@ __device__ __forceinline__ void score_item(const Params& p, const int r, const i
     lim_min = __reduce_min_sync(~0ull, lim_min);  // whole wave: a collective
     if (lane == 0) sh.lim[sw] = lim_min;          // read after the attempt's first barrier
 
-    float mref[kSTiles], mobs[kSTiles], lsum[kSTiles];
+    // mref: the row's fixed reference; mu: the same with -inf read as 0 (a row
+    // that sees no key of the split); mobs: this lane's running maximum
+    float mref[kSTiles], mu[kSTiles], mobs[kSTiles], lsum[kSTiles];
 #pragma unroll
     for (int j = 0; j < kSTiles; ++j) mref[j] = mobs[j] = -__builtin_huge_valf();
     bool over = false;
@@ -462,10 +464,17 @@ __device__ __forceinline__ void score_item(const Params& p, const int r, const i
                     if (!(key < end && key <= lim[j])) sv[j][e] = -__builtin_huge_valf();
                 }
             }
-            bm[j] = row_max4(vmax(vmax(sv[j][0], sv[j][1]), vmax(sv[j][2], sv[j][3]))) * p.scale2;
+            // lane-local maximum: the reference is fixed, so a step needs the
+            // row maximum across lanes only in the first step (and the
+            // observed maximum once per item, reduced at the rerun check)
+            bm[j] = vmax(vmax(sv[j][0], sv[j][1]), vmax(sv[j][2], sv[j][3])) * p.scale2;
             mobs[j] = vmax(mobs[j], bm[j]);
         }
         if (first_step) {
+            // a row that sees no key of the first step sees none of the split
+            // (its visible keys only grow), so its reference stays -inf
+#pragma unroll
+            for (int j = 0; j < kSTiles; ++j) bm[j] = row_max4(bm[j]);
             // the reference: the first step's maximum over both key blocks
             if (lq == 0) {
 #pragma unroll
@@ -473,17 +482,18 @@ __device__ __forceinline__ void score_item(const Params& p, const int r, const i
             }
             lds_barrier();  // X
 #pragma unroll
-            for (int j = 0; j < kSTiles; ++j) mref[j] = vmax(bm[j], sh.mx[partner][j][lr]);
+            for (int j = 0; j < kSTiles; ++j) {
+                mref[j] = vmax(bm[j], sh.mx[partner][j][lr]);
+                mu[j] = mref[j] == -__builtin_huge_valf() ? 0.0f : mref[j];
+            }
         }
         uint2* const pw = &sh.p[buf & 1][kSTiles * hs][kb][lane];
 #pragma unroll
         for (int j = 0; j < kSTiles; ++j) {
-            if (mref[j] == -__builtin_huge_valf()) mref[j] = bm[j];
             over |= bm[j] > mref[j] + kRange;
-            const float mu = mref[j] == -__builtin_huge_valf() ? 0.0f : mref[j];
             float pr[4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) pr[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[j][e], p.scale2, -mu));
+            for (int e = 0; e < 4; ++e) pr[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[j][e], p.scale2, -mu[j]));
             lsum[j] += (pr[0] + pr[1]) + (pr[2] + pr[3]);
             pw[j * 2 * DSPARK_WAVE] = uint2{cvt_pk_bf16(pr[0], pr[1]), cvt_pk_bf16(pr[2], pr[3])};
         }
@@ -510,6 +520,8 @@ __device__ __forceinline__ void score_item(const Params& p, const int r, const i
         // rerun check: did any row outgrow its reference?  (ballot on the whole wave)
         const bool any_over = __builtin_amdgcn_ballot_w64(over) != 0;
         if (lane == 0 && any_over) atomicOr(&sh.flag, 1);
+#pragma unroll
+        for (int j = 0; j < kSTiles; ++j) mobs[j] = row_max4(mobs[j]);
         if (lq == 0) {
 #pragma unroll
             for (int j = 0; j < kSTiles; ++j) sh.mx[sw][j][lr] = mobs[j];
@@ -523,7 +535,10 @@ __device__ __forceinline__ void score_item(const Params& p, const int r, const i
         if (!again) break;
         if (tid == 0) sh.flag = 0;
 #pragma unroll
-        for (int j = 0; j < kSTiles; ++j) mref[j] = mnext[j];
+        for (int j = 0; j < kSTiles; ++j) {
+            mref[j] = mnext[j];
+            mu[j] = mref[j] == -__builtin_huge_valf() ? 0.0f : mref[j];
+        }
         over = false;
     }
 

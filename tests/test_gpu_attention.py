@@ -310,8 +310,11 @@ def test_rows_outside_the_batch_left_unwritten(name):
     ("mid", 8, 8, [1, 2, 5], [1, 2, 5]),
     # contexts one key past a page, and one key past a 4096-key split
     ("mid", 32, 8, [1, 3, 17], [64, 65, 4097]),
-    # latent: a single key; one key past a split
+    # latent: a single key; 4097 keys (one split, a partial last step)
     ("mla", 128, 1, [1, 2], [1, 4097]),
+    # latent: one key past an 8192-key split, and a last split whose first key
+    # some verify rows cannot see (their partials are empty)
+    ("mla", 128, 1, [1, 6, 9], [8193, 16385, 8196]),
 ])
 def test_edge_context_lengths(name, Hq, Hkv, q_len, kv_len):
     w = synth.scaled(synth.WORKLOADS[name], R=len(q_len), Hq=Hq, Hkv=Hkv)
