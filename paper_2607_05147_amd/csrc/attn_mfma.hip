@@ -6,7 +6,7 @@
 // tiles of the chunk (64 * TPW rows) are dealt to them round-robin, and all
 // four share the key/value stream of the split through LDS:
 //
-//   * the split (at most ~2048 keys) is walked in 32-key steps; each step's
+//   * the split (at most 4096 keys) is walked in 32-key steps; each step's
 //     K and V rows (8 KB each) are copied from their page straight into LDS
 //     with global_load_lds_dwordx4 (no registers involved), into a ring of
 //     four buffers, three steps ahead of the one being computed; the waits

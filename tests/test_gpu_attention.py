@@ -191,6 +191,12 @@ def test_serving_full_size_sampled():
     _sampled_compare("serving", 0)
 
 
+def test_mid_full_size_sampled():
+    # the mid workload at its full size (32 requests, fp32 logits upstream,
+    # bf16 attention): every context fits one split
+    _sampled_compare("mid", 0, n_per_req=4)
+
+
 def test_highconc_full_size_sampled():
     _sampled_compare("highconc", 0, n_per_req=1)
 

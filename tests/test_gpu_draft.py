@@ -28,6 +28,10 @@ P_RTOL = 2e-4
 C_ATOL = 2e-5
 
 
+# requests of the full-size case that the oracle checks in full: 16 of 128,
+# spread over the batch (both ends included)
+FULL_SIZE_REQS = [int(x) for x in np.linspace(0, 127, 16).round()]
+
 def _run_gpu(w, case, rank, d, inv_temperature=1.0, anchor=None):
     inp = case.inp
     tok, p, conf = dspark.dspark_markov_draft(
@@ -120,9 +124,9 @@ def test_draft_invalid_anchor():
 
 def test_draft_full_size_sampled():
     # the serving shape: 128 requests, 16 positions, V = 129280, rank 256,
-    # 4096-wide hidden states; the oracle checks three requests in full
+    # 4096-wide hidden states; the oracle checks 16 requests spread over the batch in full
     w = synth.WORKLOADS["serving"]
-    case = guard.draft_case(w, 0, rank=256, d=4096, reqs=[0, 61, 127])
+    case = guard.draft_case(w, 0, rank=256, d=4096, reqs=FULL_SIZE_REQS)
     tok, p, conf = _run_gpu(w, case, 256, 4096)
     _compare(w, case, tok, p, conf, "full size")
     assert ((tok >= 0) & (tok < w.V)).all().item()
