@@ -45,8 +45,14 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kMfThreads = 256;
 constexpr int kMfWaves = 4;
+// Keys per split (the last split of a context holds the rest): kSplit, or a
+// smaller power of two down to kMinSplit when a batch's largest possible number
+// of work items at kSplit is below kTargetItems (three rounds of the 512
+// resident workgroups), so that a small batch still fills the part.
 constexpr int kSplit = 4096;
-static_assert(kSplit / 64 <= DSPARK_WAVE, "a split's page ids fit one per lane");   // keys per split (the last split of a context holds the rest)
+constexpr int kMinSplit = 512;
+constexpr int64_t kTargetItems = 1536;
+static_assert(kSplit / 64 <= DSPARK_WAVE, "a split's page ids fit one per lane");
 constexpr int kStepTok = 32;   // keys per step
 constexpr int kRing = 4;       // LDS buffers; copies run kRing - 1 steps ahead
 constexpr int kD = 128;
@@ -73,7 +79,7 @@ bool attn_mfma_supported(const AttnArgs& a) {
 }
 
 struct MfGeom {
-    int tpw, chunk_rows, group, max_splits, rc_max;
+    int tpw, chunk_rows, group, split, max_splits, rc_max;
     int64_t n_items;   // upper bound on attention work items
     int64_t n_merge;   // upper bound on merge items (8 rows each)
     size_t counter_bytes, list_bytes, mlist_bytes, slot_floats, part_bytes;
@@ -87,9 +93,12 @@ static MfGeom mf_geom(const AttnArgs& a) {
     g.chunk_rows = 16 * kMfWaves * g.tpw;
     g.group = a.Hq / a.Hkv;
     const int64_t max_kv = (int64_t)a.max_pages * a.page;
-    g.max_splits = (int)std::max<int64_t>(1, (max_kv + kSplit - 1) / kSplit);
     g.rc_max = (a.max_q * g.group + g.chunk_rows - 1) / g.chunk_rows;
     const int64_t slots = (int64_t)a.R * a.Hkv * g.rc_max;
+    g.split = kSplit;
+    while (g.split > kMinSplit && slots * ((max_kv + g.split - 1) / g.split) < kTargetItems)
+        g.split >>= 1;
+    g.max_splits = (int)std::max<int64_t>(1, (max_kv + g.split - 1) / g.split);
     g.n_items = slots * g.max_splits;
     g.n_merge = g.max_splits > 1 ? slots * (g.chunk_rows / kMergeRows) : 0;
     // [0] next item, [1] number of items, [2] number of merge items
@@ -108,7 +117,7 @@ size_t attn_mfma_workspace(const AttnArgs& a) {
 
 struct MfParams {
     AttnArgs a;
-    int group, max_splits, rc_max, chunk_rows;
+    int group, split, max_splits, rc_max, chunk_rows;  // split: keys per split
     int page_shift;                      // log2(page size)
     uint32_t ks0b, ks1b, ks2b, vs0b, vs1b, vs2b;  // KV strides in bytes
     float scale2;
@@ -118,14 +127,13 @@ struct MfParams {
     float* part;    // split partials: [slot][split] {m[rows], l[rows], o[rows][128]}
 };
 
-// Keys [start, end) of split s of a context of kv keys: whole kSplit-key
-// pieces, the last one holding the remainder.  The remainders spread item
+// Keys [start, end) of split s of a context of kv keys: whole pieces of
+// `split` keys, the last one holding the remainder.  The remainders spread item
 // lengths down to a single step, so the longest-first list ends with short
 // items and the persistent workgroups finish close together.
-__host__ __device__ __forceinline__ void split_range(int kv, int ns, int s, int& start, int& end) {
-    (void)ns;
-    start = s * kSplit;
-    end = min(kv, start + kSplit);
+__host__ __device__ __forceinline__ void split_range(int kv, int split, int s, int& start, int& end) {
+    start = s * split;
+    end = min(kv, start + split);
 }
 
 // Builds the work lists on the device from cu_q / kv_len (no host round trip).
@@ -158,13 +166,13 @@ __global__ __launch_bounds__(kPlanThreads) void mf_plan(MfParams p) {
         // the request's rows must lie inside the flattened batch the caller
         // sized: [0, min(cu_q[R], R * max_q))
         if (q0 < 0 || (int64_t)q0 + ql > total_rows) return false;
-        ns = (kv + kSplit - 1) / kSplit;
+        ns = (kv + p.split - 1) / p.split;
         nr = (ql * p.group + p.chunk_rows - 1) / p.chunk_rows;
         return true;
     };
     auto steps_of = [&](int kv, int ns, int sp) {
         int st, en;
-        split_range(kv, ns, sp, st, en);
+        split_range(kv, p.split, sp, st, en);
         return min((en - st + kStepTok - 1) / kStepTok, kBins - 1);
     };
     // histogram of item lengths (the request's lanes share its splits)
@@ -331,7 +339,7 @@ __device__ __forceinline__ void attn_item(const MfParams& p, const int r, const 
     const int rows = ql * p.group;
     const int row0 = rc * kChunkRows;
     int start, end;
-    split_range(kv, nsplit, s, start, end);
+    split_range(kv, p.split, s, start, end);
     const int nrows = min(kChunkRows, rows - row0);
     const int nt = (nrows + 15) >> 4;
 
@@ -727,6 +735,7 @@ hipError_t launch_attn_mfma(const AttnArgs& a, void* ws, hipStream_t s) {
     MfParams p;
     p.a = a;
     p.group = g.group;
+    p.split = g.split;
     p.max_splits = g.max_splits;
     p.rc_max = g.rc_max;
     p.chunk_rows = g.chunk_rows;
