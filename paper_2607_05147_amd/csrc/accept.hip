@@ -268,35 +268,30 @@ __global__ __launch_bounds__(kBlk) void acc_rowpass(
     auto load = [&](int i, WaveChunk<BF16>& c) {
         if (VEC) wc_load<BF16>(row_of(i), (i % nch) * kChunk, V, lane, c);
     };
-    auto process = [&](int i, const WaveChunk<BF16>& c) {
-        const int v0 = (i % nch) * kChunk;
-        const int v1 = min(V, v0 + kChunk);
-        float x[kLanePer];
-        if (VEC) {
-            wc_unpack<BF16>(c, x);
-            if (v1 < v0 + kChunk) wc_mask<BF16>(x, v0, v1, lane, -__builtin_huge_valf());
-        } else {
-            wc_load_slow<BF16>(row_of(i), v0, v1, lane, -__builtin_huge_valf(), x);
-        }
-        chunk_stat<BF16, GREEDY>(x, v0, lane, scale2, stats + i);
-        if (!GREEDY && lane == 0 && v0 == 0) rows[i / nch] = RowInfo{0.0f, 0.0f, -1, -1};
-    };
     // each wave walks a contiguous range of (row, chunk) items, i.e. whole
-    // stretches of logit rows, with the next chunk's loads in flight (two
-    // register buffers) while it reduces the current one
+    // stretches of logit rows.  One register buffer: a chunk's words are
+    // unpacked into x as soon as they land, and the buffer is refilled with
+    // the next chunk right away, so its loads are in flight while this chunk
+    // is reduced (fewer registers than two buffers, so more waves per SIMD)
     const int nwv = gridDim.x * kWaves;
     const int per = (items + nwv - 1) / nwv;
     int it = (blockIdx.x * kWaves + wave_id()) * per;
     const int end = min(items, it + per);
-    WaveChunk<BF16> A, B;
+    WaveChunk<BF16> A;
     if (it < end) load(it, A);
-    while (it < end) {
-        if (it + 1 < end) load(it + 1, B);
-        process(it, A);
-        if (++it >= end) break;
-        if (it + 1 < end) load(it + 1, A);
-        process(it, B);
-        ++it;
+    for (; it < end; ++it) {
+        const int v0 = (it % nch) * kChunk;
+        const int v1 = min(V, v0 + kChunk);
+        float x[kLanePer];
+        if (VEC) {
+            wc_unpack<BF16>(A, x);
+            if (it + 1 < end) load(it + 1, A);
+            if (v1 < v0 + kChunk) wc_mask<BF16>(x, v0, v1, lane, -__builtin_huge_valf());
+        } else {
+            wc_load_slow<BF16>(row_of(it), v0, v1, lane, -__builtin_huge_valf(), x);
+        }
+        chunk_stat<BF16, GREEDY>(x, v0, lane, scale2, stats + it);
+        if (!GREEDY && lane == 0 && v0 == 0) rows[it / nch] = RowInfo{0.0f, 0.0f, -1, -1};
     }
 }
 
