@@ -114,10 +114,10 @@ ATTN_PATHS = {
     "generic": {"src": "attn_generic.hip", "kernels": ("attn_generic_kernel", "attn_generic_merge"),
                 "bound": "hbm"},
     # not attention: the draft blocks' launches
-    "draft": {"src": "markov.hip", "kernels": ("md_hidden", "md_first", "md_tile", "md_stats"),
+    "draft": {"src": "markov.hip", "kernels": ("md_hidden", "md_first", "md_tile", "md_stats", "md_norm"),
               "bound": "hbm"},
     "rnn_draft": {"src": "markov.hip", "kernels": ("md_hidden", "rnn_hproj", "md_first", "rnn_state",
-                                                   "md_tile", "md_stats"),
+                                                   "md_tile", "md_stats", "md_norm"),
                   "bound": "hbm"},
     # not attention: the acceptance launches of one dspark_accept call (the
     # resolve kernel runs once per call)
@@ -681,9 +681,9 @@ def draft_bench(args):
     head = "RNN-head" if rnn else "Markov-head"
     log(f"{head} draft block: {ms.mean() * 1e3:.1f} us per call ({ms.mean() * 1e3 / w.K:.1f} us per "
         f"position), {gbps:.0f} GB/s = {gbps / HBM_PEAK_GBPS:.1%} of HBM peak")
-    kernels = ("dspark_rnn_draft: md_hidden + rnn_hproj + md_first, then rnn_state + md_tile<0> + "
-               "md_stats + md_tile<1> per position" if rnn else
-               "dspark_markov_draft: md_hidden + md_first, then md_tile<0> + md_stats + md_tile<1> "
+    kernels = ("dspark_rnn_draft: md_hidden + rnn_hproj + md_first, then rnn_state + md_tile + "
+               "md_stats + md_norm per position" if rnn else
+               "dspark_markov_draft: md_hidden + md_first, then md_tile + md_stats + md_norm "
                "per position")
     result = {
         "metric": f"draft tokens/s and achieved HBM GB/s (% of peak), {head} draft block on 1 MI355X",

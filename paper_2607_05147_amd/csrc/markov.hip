@@ -9,22 +9,25 @@
 //   x_k = inverse CDF of p_k at u[r, k-1];   c_k = sigmoid(w . [h_k; e_k] / T_k).
 // Launches, all on one stream: md_hidden (the backbone part w_h . h_k of every
 // confidence logit, once) and md_first (e_1 and c_1), then per position k:
-//   md_tile<0>  one workgroup per 128 vocabulary entries: W2^T e for every
-//               request on v_mfma_f32_16x16x32_bf16 (the tile's W2t rows stay
-//               in registers as A operands, the embeddings stream through LDS
-//               in chunks of 32 requests as B operands), plus the base logits;
-//               then the tile's softmax statistics (max, sum of exp) per request;
-//   md_stats    one wave per request: the row's max and total and the tile in
-//               which the running mass passes u * total (fp64 prefix over the
-//               tiles in vocabulary order);
-//   md_tile<1>  the same product again, writing p_k = exp(z - max) / total; the
-//               workgroup whose tile holds a request's draw makes it (fp64
-//               prefix of that tile's masses), writes x_k, gathers e_{k+1} into
-//               the other embedding buffer and writes c_{k+1}.
-// The product is recomputed rather than stored: the second pass reads W2t
-// again (66 MB at V = 129280, rank 256, which the 256 MB last-level cache can
-// hold) instead of writing and re-reading fp32 logits.  The positions of a
-// block are sequential by definition (x_k feeds position k + 1).
+//   md_tile   one workgroup per 128 vocabulary entries: W2^T e for every
+//             request on v_mfma_f32_16x16x32_bf16 (the tile's W2t rows stay in
+//             registers as A operands, the embeddings stream through LDS in
+//             chunks of 32 requests as B operands), plus the base logits; z is
+//             written to draft_p in fp32, with the tile's softmax statistics
+//             (max, sum of exp) per request;
+//   md_stats  one wave per request: the row's max and total and the tile in
+//             which the running mass passes u * total (fp64 prefix over the
+//             tiles in vocabulary order);
+//   md_norm   a streaming pass over draft_p that turns z into
+//             p_k = exp(z - max) / total in place; the workgroup whose segment
+//             holds a request's draw makes it (fp64 prefix of that tile's
+//             masses), writes x_k, gathers e_{k+1} into the other embedding
+//             buffer and writes c_{k+1}.
+// The product runs once per position: the projection and the base logits are
+// read once, and z makes one round trip through draft_p (66 MB per position
+// at R = 128, V = 129280, small enough for the 256 MB last-level cache to
+// serve the re-read).  The positions of a block are sequential by definition
+// (x_k feeds position k + 1).
 #include <algorithm>
 #include <math.h>
 
@@ -78,7 +81,7 @@ __device__ __forceinline__ float quad_sum(float v) {
     return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
-// Per-request state of a position between the two tile passes.
+// Per-request state of a position, from the tile statistics to the normalisation.
 struct RowInfo {
     float M;     // row maximum of z (base-2 units: z * log2 e)
     float S;     // sum over the row of exp(z - M)
@@ -145,14 +148,11 @@ __global__ __launch_bounds__(kThreads) void md_first(MarkovArgs a, const float* 
 
 // z for (request, vocabulary entry) pairs of one 128-entry tile:
 // C[v, r] = sum_j W2t[v, j] E[r, j] on MFMA (A: the tile's W2t rows, kept in
-// registers; B: the embeddings, 64 requests at a time through LDS), then
+// registers; B: the embeddings, 32 requests at a time through LDS), then
 // z = inv_temp * (U + C), kept in base-2 units (z * log2 e, so that exp(z - m)
-// is one v_exp_f32 of the difference).
-// PASS 0: per-tile statistics stats[r * ntiles + tile] = (max z, sum 2^(z - max)).
-// PASS 1: draft_p = 2^(z - M) / S with (M, S) of the request's RowInfo; for
-//   every request whose draw falls in this tile, the draw itself (fp64 prefix
-//   of the tile's masses in vocabulary order), and for position k < K the next
-//   embedding E_next[r] = W1[x_k] and the confidence c_{k+1}.
+// is one v_exp_f32 of the difference).  z goes to the request's draft_p row
+// (md_norm turns it into p in place), and the per-tile statistics to
+// stats[r * ntiles + tile] = (max z, sum 2^(z - max)).
 // VEC: 4 consecutive entries per lane are loaded / stored as one vector
 // (V, ld multiples of 4, aligned rows).
 // NT: bf16 terms of the B operand per request (1: the embedding itself; 3:
@@ -162,19 +162,16 @@ __global__ __launch_bounds__(kThreads) void md_first(MarkovArgs a, const float* 
 // BF16: the base logits' type.  Their loads are branch-free (clamped
 // indices; entries past V are masked with the rest of the tile), so they issue
 // back to back and stay in flight during the products.  Occupancy: three
-// waves per SIMD for the one-term statistics pass; two for the pass that
-// draws and writes p, and for three terms (three times the staged embedding
-// loads), which leaves their loads room without spilling (measured faster).
-template <int KS, int NT, int PASS, bool VEC, bool BF16>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 1 && PASS == 0 ? 3 : 2, 4))) void md_tile(MarkovArgs a, const uint16_t* E,
-                                                    float2* stats, const RowInfo* info,
-                                                    uint16_t* E_next, const float* sh,
-                                                    int ntiles, int k) {
+// waves per SIMD for one term; two for three terms (three times the staged
+// embedding loads), which leaves their loads room without spilling (measured
+// faster).
+template <int KS, int NT, bool VEC, bool BF16>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 1 ? 3 : 2, 4))) void md_tile(
+    MarkovArgs a, const uint16_t* E, float2* stats, int ntiles, int k) {
     constexpr int kNch = 4 * KS;  // 16-byte chunks per embedding row
     constexpr int kRank = 32 * KS;
     __shared__ __align__(16) uint16_t se[NT * kChunkR * kRank];
     __shared__ float2 sst[kWaves][kChunkR];
-    __shared__ float smass[kTileV];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -242,13 +239,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 
                 }
             }
         }
-        // (drawing pass) the chunk's row statistics, needed only after the
-        // products, are in flight with the other loads
-        RowInfo ri_c[PASS == 1 ? kRT : 1];
-        if (PASS == 1) {
-#pragma unroll
-            for (int rt = 0; rt < kRT; ++rt) ri_c[rt] = info[min(c0 + 16 * rt + lr, a.R - 1)];
-        }
         lds_barrier();  // the previous chunk's LDS reads are done (global loads stay in flight)
         // (no guard when the copy divides evenly: a branch here would make the
         // stores wait for the base logits as well)
@@ -299,110 +289,48 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 
                     for (int e = 0; e < 4; ++e)
                         if (!(rok && v0 + 16 * vt + 4 * lq + e < a.V)) z[vt][e] = -__builtin_huge_valf();
             }
-            if (PASS == 0) {
-                float m = -__builtin_huge_valf();
+            if (rok) {  // z itself, normalised in place by md_norm
+                float* out = a.draft_p + ((int64_t)r * a.K + (k - 1)) * a.V;
 #pragma unroll
-                for (int vt = 0; vt < kVT; ++vt)
+                for (int vt = 0; vt < kVT; ++vt) {
+                    const int vb = v0 + 16 * vt + 4 * lq;
+                    if (VEC && vb + 3 < a.V) {
+                        *(float4*)(out + vb) = float4{z[vt][0], z[vt][1], z[vt][2], z[vt][3]};
+                    } else {
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) m = fmaxf(m, z[vt][e]);
-                m = quad_max(m);
-                float s = 0.0f;
-                if (m > -__builtin_huge_valf()) {
-#pragma unroll
-                    for (int vt = 0; vt < kVT; ++vt)
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) s += __builtin_amdgcn_exp2f(z[vt][e] - m);
-                }
-                s = quad_sum(s);
-                if (lq == 0) sst[wave][16 * rt + lr] = float2{m, s};
-            } else {
-                const RowInfo ri = ri_c[PASS == 1 ? rt : 0];
-                const float inv = 1.0f / ri.S;
-                float q[kVT][4];
-#pragma unroll
-                for (int vt = 0; vt < kVT; ++vt)
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) q[vt][e] = __builtin_amdgcn_exp2f(z[vt][e] - ri.M);
-                if (rok) {
-                    float* out = a.draft_p + ((int64_t)r * a.K + (k - 1)) * a.V;
-#pragma unroll
-                    for (int vt = 0; vt < kVT; ++vt) {
-                        const int vb = v0 + 16 * vt + 4 * lq;
-                        if (VEC && vb + 3 < a.V) {
-                            *(float4*)(out + vb) = float4{q[vt][0] * inv, q[vt][1] * inv, q[vt][2] * inv,
-                                                          q[vt][3] * inv};
-                        } else {
-#pragma unroll
-                            for (int e = 0; e < 4; ++e)
-                                if (vb + e < a.V) out[vb + e] = q[vt][e] * inv;
-                        }
+                        for (int e = 0; e < 4; ++e)
+                            if (vb + e < a.V) out[vb + e] = z[vt][e];
                     }
-                }
-                // draws that fall in this tile (the same set in every wave)
-                uint64_t bits = __builtin_amdgcn_ballot_w64(rok && lq == 0 && ri.tile == tile);
-                while (bits) {
-                    const int j = __builtin_ctzll(bits);
-                    bits &= bits - 1;
-                    if (lr == j) {
-#pragma unroll
-                        for (int vt = 0; vt < kVT; ++vt)
-#pragma unroll
-                            for (int e = 0; e < 4; ++e) smass[wave * kWaveV + 16 * vt + 4 * lq + e] = q[vt][e];
-                    }
-                    lds_barrier();
-                    if (wave == 0) {
-                        const int rr = c0 + 16 * rt + j;
-                        const int64_t row = (int64_t)rr * a.K + (k - 1);
-                        const double thr = info[rr].thr;
-                        const double m0 = smass[2 * lane], m1 = smass[2 * lane + 1];
-                        double incl = m0 + m1;
-#pragma unroll
-                        for (int o = 1; o < DSPARK_WAVE; o <<= 1) {
-                            const double t = __shfl_up(incl, o, DSPARK_WAVE);
-                            if (lane >= o) incl += t;
-                        }
-                        const double c0m = incl - (m0 + m1);  // mass before entry 2 * lane
-                        // first entry whose running mass passes thr (zero masses are never drawn)
-                        const int cand = c0m + m0 > thr && m0 > 0.0 ? 2 * lane
-                                         : incl > thr && m1 > 0.0   ? 2 * lane + 1
-                                                                    : kTileV;
-                        int first = cand;
-#pragma unroll
-                        for (int o = 32; o > 0; o >>= 1) first = min(first, __shfl_xor(first, o, DSPARK_WAVE));
-                        // rounding: the tile's last entry with mass
-                        int last = m1 > 0.0 ? 2 * lane + 1 : m0 > 0.0 ? 2 * lane : -1;
-#pragma unroll
-                        for (int o = 32; o > 0; o >>= 1) last = max(last, __shfl_xor(last, o, DSPARK_WAVE));
-                        const int pick = first < kTileV ? first : max(last, 0);
-                        const int x = tile * kTileV + pick;
-                        const bool ok = prev_token(a, rr, k) >= 0;
-                        if (lane == 0) a.draft_tok[row] = ok ? x : -1;
-                        if (k < a.K) {
-                            const uint16_t* w1 = a.W1 + (int64_t)(ok ? x : 0) * a.rank;
-                            for (int q8 = lane * 8; q8 < a.rank; q8 += DSPARK_WAVE * 8)
-                                *(uint4*)(E_next + (int64_t)rr * a.rank + q8) = *(const uint4*)(w1 + q8);
-                            const float sc = embed_dot(a, w1, lane) + (sh ? sh[row + 1] : 0.0f);
-                            if (lane == 0) a.conf[row + 1] = ok ? confidence(a, sc, k + 1) : __builtin_nanf("");
-                        }
-                    }
-                    lds_barrier();
                 }
             }
+            float m = -__builtin_huge_valf();
+#pragma unroll
+            for (int vt = 0; vt < kVT; ++vt)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) m = fmaxf(m, z[vt][e]);
+            m = quad_max(m);
+            float s = 0.0f;
+            if (m > -__builtin_huge_valf()) {
+#pragma unroll
+                for (int vt = 0; vt < kVT; ++vt)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) s += __builtin_amdgcn_exp2f(z[vt][e] - m);
+            }
+            s = quad_sum(s);
+            if (lq == 0) sst[wave][16 * rt + lr] = float2{m, s};
         }
-        if (PASS == 0) {
-            lds_barrier();
-            if (tid < kChunkR && c0 + tid < a.R) {
-                float M = -__builtin_huge_valf();
+        lds_barrier();
+        if (tid < kChunkR && c0 + tid < a.R) {
+            float M = -__builtin_huge_valf();
 #pragma unroll
-                for (int w = 0; w < kWaves; ++w) M = fmaxf(M, sst[w][tid].x);
-                float S = 0.0f;
-                if (M > -__builtin_huge_valf()) {
+            for (int w = 0; w < kWaves; ++w) M = fmaxf(M, sst[w][tid].x);
+            float S = 0.0f;
+            if (M > -__builtin_huge_valf()) {
 #pragma unroll
-                    for (int w = 0; w < kWaves; ++w)
-                        if (sst[w][tid].x > -__builtin_huge_valf()) S += sst[w][tid].y * exp2f(sst[w][tid].x - M);
-                }
-                stats[(int64_t)(c0 + tid) * ntiles + tile] = float2{M, S};
+                for (int w = 0; w < kWaves; ++w)
+                    if (sst[w][tid].x > -__builtin_huge_valf()) S += sst[w][tid].y * exp2f(sst[w][tid].x - M);
             }
+            stats[(int64_t)(c0 + tid) * ntiles + tile] = float2{M, S};
         }
     }
 }
@@ -499,16 +427,121 @@ inline void stats_pass(const MarkovArgs& a, const float2* stats, RowInfo* info, 
         hipLaunchKernelGGL(md_stats<kStatsMaxPer>, dim3(a.R), dim3(DSPARK_WAVE), 0, s, a, stats, info, ntiles, k);
 }
 
-// One launch of md_tile over every vocabulary tile, instantiated for the
-// base logits' type and vector access.
-template <int KS, int NT, int PASS>
-void tile_pass(const MarkovArgs& a, const uint16_t* E, float2* stats, const RowInfo* info,
-               uint16_t* En, const float* shp, int ntiles, int k, bool vec, hipStream_t s) {
+// ----------------------------------------------------------------- md_norm
+
+// One workgroup per (request, 8192-entry segment of the vocabulary).  The
+// request's draft_p row holds z in base-2 units (written by md_tile); it
+// becomes p = 2^(z - M) / S in place, every load of the thread issued before
+// its first store.  In the workgroup whose segment holds the request's draw
+// tile, wave 0 takes that tile's 128 entries itself: their masses 2^(z - M)
+// in fp32, the draw (fp64 prefix in vocabulary order; the first entry whose
+// running mass passes thr, or the tile's last entry with mass), their p, then
+// x_k, and for k < K the next embedding E_next[r] = W1[x_k] and the
+// confidence c_{k+1}.  The other threads skip that tile, so nothing else
+// writes it.
+constexpr int kNormV = 8192;
+constexpr int kNormIt = kNormV / (4 * kThreads);  // float4 groups per thread
+static_assert(kNormV % kTileV == 0, "a tile lies inside one segment");
+
+template <bool VEC>
+__global__ __launch_bounds__(kThreads) void md_norm(MarkovArgs a, const RowInfo* info, uint16_t* E_next,
+                                                    const float* sh, int k) {
+    const int r = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int s0 = blockIdx.y * kNormV;
+    const int s1 = min(a.V, s0 + kNormV);
+    const int64_t row = (int64_t)r * a.K + (k - 1);
+    float* p = a.draft_p + row * a.V;
+    const RowInfo ri = info[r];
+    const float inv = 1.0f / ri.S;
+    const int tb = ri.tile * kTileV;
+    const bool draws = tb >= s0 && tb < s1;  // the same in the whole workgroup
+    const int skip0 = draws ? tb : s1, skip1 = draws ? tb + kTileV : s1;
+    const bool drawer = draws && tid < DSPARK_WAVE;
+    float dz[2];
+    if (drawer) {
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const int v = tb + 2 * lane + e;
+            dz[e] = v < a.V ? p[v] : -__builtin_huge_valf();
+        }
+    }
+    if (VEC) {
+        // V % 4 == 0: groups start at multiples of 4, so a group is wholly
+        // inside or outside the draw tile and the row
+        float4 zv[kNormIt];
+#pragma unroll
+        for (int i = 0; i < kNormIt; ++i)
+            zv[i] = *(const float4*)(p + min(s0 + 4 * (tid + i * kThreads), s1 - 4));
+#pragma unroll
+        for (int i = 0; i < kNormIt; ++i) {
+            const int v = s0 + 4 * (tid + i * kThreads);
+            if (v < s1 && (v < skip0 || v >= skip1))
+                *(float4*)(p + v) = float4{__builtin_amdgcn_exp2f(zv[i].x - ri.M) * inv,
+                                           __builtin_amdgcn_exp2f(zv[i].y - ri.M) * inv,
+                                           __builtin_amdgcn_exp2f(zv[i].z - ri.M) * inv,
+                                           __builtin_amdgcn_exp2f(zv[i].w - ri.M) * inv};
+        }
+    } else {
+        float zs[4 * kNormIt];
+#pragma unroll
+        for (int i = 0; i < 4 * kNormIt; ++i) zs[i] = p[min(s0 + tid + i * kThreads, s1 - 1)];
+#pragma unroll
+        for (int i = 0; i < 4 * kNormIt; ++i) {
+            const int v = s0 + tid + i * kThreads;
+            if (v < s1 && (v < skip0 || v >= skip1)) p[v] = __builtin_amdgcn_exp2f(zs[i] - ri.M) * inv;
+        }
+    }
+    if (!drawer) return;
+    const float q0 = __builtin_amdgcn_exp2f(dz[0] - ri.M), q1 = __builtin_amdgcn_exp2f(dz[1] - ri.M);
+    if (tb + 2 * lane < a.V) p[tb + 2 * lane] = q0 * inv;
+    if (tb + 2 * lane + 1 < a.V) p[tb + 2 * lane + 1] = q1 * inv;
+    const double m0 = q0, m1 = q1;
+    double incl = m0 + m1;
+#pragma unroll
+    for (int o = 1; o < DSPARK_WAVE; o <<= 1) {
+        const double t = __shfl_up(incl, o, DSPARK_WAVE);
+        if (lane >= o) incl += t;
+    }
+    const double before = incl - (m0 + m1);  // mass before entry 2 * lane
+    // first entry whose running mass passes thr (zero masses are never drawn)
+    const int cand = before + m0 > ri.thr && m0 > 0.0 ? 2 * lane
+                     : incl > ri.thr && m1 > 0.0    ? 2 * lane + 1
+                                                    : kTileV;
+    int first = cand;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) first = min(first, __shfl_xor(first, o, DSPARK_WAVE));
+    // rounding: the tile's last entry with mass
+    int last = m1 > 0.0 ? 2 * lane + 1 : m0 > 0.0 ? 2 * lane : -1;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) last = max(last, __shfl_xor(last, o, DSPARK_WAVE));
+    const int x = tb + (first < kTileV ? first : max(last, 0));
+    const bool ok = prev_token(a, r, k) >= 0;
+    if (lane == 0) a.draft_tok[row] = ok ? x : -1;
+    if (k < a.K) {
+        const uint16_t* w1 = a.W1 + (int64_t)(ok ? x : 0) * a.rank;
+        for (int q8 = lane * 8; q8 < a.rank; q8 += DSPARK_WAVE * 8)
+            *(uint4*)(E_next + (int64_t)r * a.rank + q8) = *(const uint4*)(w1 + q8);
+        const float sc = embed_dot(a, w1, lane) + (sh ? sh[row + 1] : 0.0f);
+        if (lane == 0) a.conf[row + 1] = ok ? confidence(a, sc, k + 1) : __builtin_nanf("");
+    }
+}
+
+// One position after the embeddings E are in place: md_tile over every
+// vocabulary tile (z and the tile statistics), md_stats, then md_norm, which
+// draws x_k and gathers the next embedding into En.
+template <int KS, int NT>
+void position(const MarkovArgs& a, const uint16_t* E, float2* stats, RowInfo* info, uint16_t* En,
+              const float* shp, int ntiles, int k, bool vec, hipStream_t s) {
     const dim3 g(ntiles), b(kThreads);
-    if (vec && a.base_bf16) hipLaunchKernelGGL((md_tile<KS, NT, PASS, true, true>), g, b, 0, s, a, E, stats, info, En, shp, ntiles, k);
-    else if (vec) hipLaunchKernelGGL((md_tile<KS, NT, PASS, true, false>), g, b, 0, s, a, E, stats, info, En, shp, ntiles, k);
-    else if (a.base_bf16) hipLaunchKernelGGL((md_tile<KS, NT, PASS, false, true>), g, b, 0, s, a, E, stats, info, En, shp, ntiles, k);
-    else hipLaunchKernelGGL((md_tile<KS, NT, PASS, false, false>), g, b, 0, s, a, E, stats, info, En, shp, ntiles, k);
+    if (vec && a.base_bf16) hipLaunchKernelGGL((md_tile<KS, NT, true, true>), g, b, 0, s, a, E, stats, ntiles, k);
+    else if (vec) hipLaunchKernelGGL((md_tile<KS, NT, true, false>), g, b, 0, s, a, E, stats, ntiles, k);
+    else if (a.base_bf16) hipLaunchKernelGGL((md_tile<KS, NT, false, true>), g, b, 0, s, a, E, stats, ntiles, k);
+    else hipLaunchKernelGGL((md_tile<KS, NT, false, false>), g, b, 0, s, a, E, stats, ntiles, k);
+    stats_pass(a, stats, info, ntiles, k, s);
+    const dim3 gn(a.R, ceil_div(a.V, kNormV));
+    if (vec) hipLaunchKernelGGL(md_norm<true>, gn, b, 0, s, a, (const RowInfo*)info, En, shp, k);
+    else hipLaunchKernelGGL(md_norm<false>, gn, b, 0, s, a, (const RowInfo*)info, En, shp, k);
 }
 
 // ------------------------------------------------------------ RNN head
@@ -730,10 +763,8 @@ hipError_t launch_rnn_ks(const MarkovArgs& a, uint16_t* Ee, uint16_t* E3, float*
         uint16_t* tn = (k & 1) ? T0 : T1;
         hipLaunchKernelGGL(rnn_state, dim3(a.rank / kStJ, ceil_div(a.R, kStR)), dim3(kThreads), 0, s, a, hpp,
                            sp, tp, sn, tn, (const uint16_t*)Ee, E3, k);
-        tile_pass<KS, 3, 0>(a, E3, stats, info, Ee, shp, ntiles, k, vec, s);
-        stats_pass(a, stats, info, ntiles, k, s);
         // the draw gathers W1[x_k] into Ee: the embedding input of position k + 1
-        tile_pass<KS, 3, 1>(a, E3, stats, info, Ee, shp, ntiles, k, vec, s);
+        position<KS, 3>(a, E3, stats, info, Ee, shp, ntiles, k, vec, s);
     }
     return hipGetLastError();
 }
@@ -748,9 +779,7 @@ hipError_t launch_ks(const MarkovArgs& a, uint16_t* E0, uint16_t* E1, float2* st
     for (int k = 1; k <= a.K; ++k) {
         uint16_t* Ek = (k & 1) ? E0 : E1;
         uint16_t* En = (k & 1) ? E1 : E0;
-        tile_pass<KS, 1, 0>(a, Ek, stats, info, En, shp, ntiles, k, vec, s);
-        stats_pass(a, stats, info, ntiles, k, s);
-        tile_pass<KS, 1, 1>(a, Ek, stats, info, En, shp, ntiles, k, vec, s);
+        position<KS, 1>(a, Ek, stats, info, En, shp, ntiles, k, vec, s);
     }
     return hipGetLastError();
 }
