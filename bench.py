@@ -114,7 +114,8 @@ ATTN_PATHS = {
     "generic": {"src": "attn_generic.hip", "kernels": ("attn_generic_kernel", "attn_generic_merge"),
                 "bound": "hbm"},
     # not attention: the draft blocks' launches
-    "draft": {"src": "markov.hip", "kernels": ("md_hidden", "md_first", "md_tile", "md_stats", "md_norm"),
+    "draft": {"src": "markov.hip", "kernels": ("md_hidden", "md_first", "md_coop", "md_check", "md_tile",
+                                              "md_stats", "md_norm"),
               "bound": "hbm"},
     "rnn_draft": {"src": "markov.hip", "kernels": ("md_hidden", "rnn_hproj", "md_first", "rnn_state",
                                                    "md_tile", "md_stats", "md_norm"),
@@ -683,8 +684,7 @@ def draft_bench(args):
         f"position), {gbps:.0f} GB/s = {gbps / HBM_PEAK_GBPS:.1%} of HBM peak")
     kernels = ("dspark_rnn_draft: md_hidden + rnn_hproj + md_first, then rnn_state + md_tile + "
                "md_stats + md_norm per position" if rnn else
-               "dspark_markov_draft: md_hidden + md_first, then md_tile + md_stats + md_norm "
-               "per position")
+               "dspark_markov_draft: md_hidden + md_first, then md_coop per position, md_check")
     result = {
         "metric": f"draft tokens/s and achieved HBM GB/s (% of peak), {head} draft block on 1 MI355X",
         "value": w.R * w.K / (ms_per / 1e3),

@@ -8,7 +8,12 @@
 //   e_k = W1[x_{k-1}];   z_k = inv_temp * (U_k + W2^T e_k);   p_k = softmax(z_k);
 //   x_k = inverse CDF of p_k at u[r, k-1];   c_k = sigmoid(w . [h_k; e_k] / T_k).
 // Launches, all on one stream: md_hidden (the backbone part w_h . h_k of every
-// confidence logit, once) and md_first (e_1 and c_1), then per position k:
+// confidence logit, once) and md_first (e_1 and c_1), then per position k
+// either one md_coop launch per group of up to 128 requests (Markov head,
+// bf16 base logits, V % 4 == 0, a grid the device holds at once; md_check
+// after the block), which keeps z in registers across two grid-wide
+// exchanges so that the projection and the base logits are read once and p
+// is written once, or the three launches:
 //   md_tile   one workgroup per 128 vocabulary entries: W2^T e for every
 //             request on v_mfma_f32_16x16x32_bf16 (the tile's W2t rows stay in
 //             registers as A operands, the embeddings stream through LDS in
@@ -23,11 +28,8 @@
 //             holds a request's draw makes it (fp64 prefix of that tile's
 //             masses), writes x_k, gathers e_{k+1} into the other embedding
 //             buffer and writes c_{k+1}.
-// The product runs once per position: the projection and the base logits are
-// read once, and z makes one round trip through draft_p (66 MB per position
-// at R = 128, V = 129280, small enough for the 256 MB last-level cache to
-// serve the re-read).  The positions of a block are sequential by definition
-// (x_k feeds position k + 1).
+// The positions of a block are sequential by definition (x_k feeds position
+// k + 1).
 #include <algorithm>
 #include <math.h>
 
@@ -49,6 +51,14 @@ constexpr int kChunkR = 32;              // requests per LDS chunk
 constexpr int kRT = kChunkR / 16;        // 16-request blocks per chunk
 
 __host__ __device__ constexpr int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// md_coop's grid barrier: arrival groups of workgroups (blockIdx % 8) and its
+// words in the workspace, 128 bytes apart: [0] arrivals of the groups' last
+// workgroups, [1] timeout, [stride * (1 + x)] arrivals of group x,
+// [stride * (1 + groups + x)] flag of group x
+constexpr int kCoGroups = 8;
+constexpr int kSyncStride = 32;
+constexpr int kSyncWords = kSyncStride * (1 + 2 * kCoGroups);
 
 // Slot of 16-byte chunk c in row t of the embedding chunk (nch chunks per row,
 // a power of two).  The XOR (bits of t in the order 0, 2, 1, 3) puts the 16
@@ -131,8 +141,11 @@ __global__ __launch_bounds__(kThreads) void md_hidden(MarkovArgs a, float* sh) {
 // ---------------------------------------------------------------- md_first
 
 // Position 1: e_1 = W1[x_0] into the first embedding buffer, and c_1.  One wave per request.
-__global__ __launch_bounds__(kThreads) void md_first(MarkovArgs a, const float* sh, uint16_t* E0) {
+// Also zeroes md_coop's barrier words (when given).
+__global__ __launch_bounds__(kThreads) void md_first(MarkovArgs a, const float* sh, uint16_t* E0, unsigned* sync) {
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    if (sync && blockIdx.x == 0)
+        for (int i = threadIdx.x; i < kSyncWords; i += kThreads) sync[i] = 0u;
     const int r = blockIdx.x * kWaves + wave;
     if (r >= a.R) return;  // whole wave
     const int x0 = a.anchor[r];
@@ -343,11 +356,52 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 
 // contiguous run of tiles l * per .. l * per + per - 1, so the lane order is
 // the vocabulary order; the reductions are lane shuffles, with no barrier.
 constexpr int kStatsMaxPer = 32;  // tiles per lane (up to 2048 tiles: V <= 262144)
-template <int P>
-__global__ __launch_bounds__(DSPARK_WAVE) void md_stats(MarkovArgs a, const float2* stats, RowInfo* info,
-                                                        int ntiles, int k) {
-    const int r = blockIdx.x;
-    const int lane = threadIdx.x;
+// Device-coherent 64-bit access (agent scope, relaxed): it bypasses the
+// per-XCD L2, for data that the workgroups of one cooperative launch exchange
+// across a grid barrier.
+__device__ __forceinline__ uint64_t ld_dev64(const void* p) {
+    return __hip_atomic_load((uint64_t*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev64(void* p, uint64_t v) {
+    __hip_atomic_store((uint64_t*)p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <bool SC>
+__device__ __forceinline__ float2 ld_f2(const float2* p) {
+    if (!SC) return *p;
+    const uint64_t v = ld_dev64(p);
+    return float2{__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32))};
+}
+template <bool SC>
+__device__ __forceinline__ void st_f2(float2* p, float2 v) {
+    if (!SC) {
+        *p = v;
+        return;
+    }
+    st_dev64(p, (uint64_t)__float_as_uint(v.x) | ((uint64_t)__float_as_uint(v.y) << 32));
+}
+static_assert(sizeof(RowInfo) == 24, "RowInfo moves as three 64-bit words");
+template <bool SC>
+__device__ __forceinline__ void st_info(RowInfo* p, const RowInfo& v) {
+    if (!SC) {
+        *p = v;
+        return;
+    }
+    const uint64_t* w = (const uint64_t*)&v;
+    for (int i = 0; i < 3; ++i) st_dev64((uint64_t*)p + i, w[i]);
+}
+template <bool SC>
+__device__ __forceinline__ RowInfo ld_info(const RowInfo* p) {
+    if (!SC) return *p;
+    RowInfo v;
+    uint64_t* w = (uint64_t*)&v;
+    for (int i = 0; i < 3; ++i) w[i] = ld_dev64((const uint64_t*)p + i);
+    return v;
+}
+
+// SC: the statistics are read and the row's RowInfo written device-coherently.
+template <int P, bool SC>
+__device__ __forceinline__ void row_stats(const MarkovArgs& a, const float2* stats, RowInfo* info, int ntiles,
+                                          int k, int r, int lane) {
     const float2* st = stats + (int64_t)r * ntiles;
     const int per = ceil_div(ntiles, DSPARK_WAVE);
     const int t0 = lane * per;
@@ -356,7 +410,7 @@ __global__ __launch_bounds__(DSPARK_WAVE) void md_stats(MarkovArgs a, const floa
     const float uu = a.u[(int64_t)r * a.K + (k - 1)];
     float2 x[P];
 #pragma unroll
-    for (int i = 0; i < P; ++i) x[i] = st[min(t0 + i, ntiles - 1)];
+    for (int i = 0; i < P; ++i) x[i] = ld_f2<SC>(st + min(t0 + i, ntiles - 1));
     float m = -__builtin_huge_valf();
 #pragma unroll
     for (int i = 0; i < P; ++i) {
@@ -409,14 +463,20 @@ __global__ __launch_bounds__(DSPARK_WAVE) void md_stats(MarkovArgs a, const floa
                 ri.tile = lastpos;
                 ri.thr = __builtin_huge_val();
             }
-            info[r] = ri;
+            st_info<SC>(info + r, ri);
         }
     } else if (lane == 0) {
         // rounding pushed u * total past the end: the row's last tile with mass
         ri.tile = max(last, 0);
         ri.thr = __builtin_huge_val();
-        info[r] = ri;
+        st_info<SC>(info + r, ri);
     }
+}
+
+template <int P>
+__global__ __launch_bounds__(DSPARK_WAVE) void md_stats(MarkovArgs a, const float2* stats, RowInfo* info,
+                                                        int ntiles, int k) {
+    row_stats<P, false>(a, stats, info, ntiles, k, blockIdx.x, threadIdx.x);
 }
 
 inline void stats_pass(const MarkovArgs& a, const float2* stats, RowInfo* info, int ntiles, int k,
@@ -542,6 +602,338 @@ void position(const MarkovArgs& a, const uint16_t* E, float2* stats, RowInfo* in
     const dim3 gn(a.R, ceil_div(a.V, kNormV));
     if (vec) hipLaunchKernelGGL(md_norm<true>, gn, b, 0, s, a, (const RowInfo*)info, En, shp, k);
     else hipLaunchKernelGGL(md_norm<false>, gn, b, 0, s, a, (const RowInfo*)info, En, shp, k);
+}
+
+// ----------------------------------------------------------------- md_coop
+
+// One position of the Markov head (bf16 base logits, V % 4 == 0, at most 1024
+// tiles) for a group of up to 128 requests in one launch whose workgroups are
+// all resident at once (the grid is at most what the device holds, one
+// workgroup per CU), with z held in registers from the product to the
+// normalisation, so that it never goes through memory: the projection and
+// the base logits are read once and p is written once.
+//   A  workgroup g owns the tiles 4g .. 4g + 3 (8 waves, 16 vocabulary entries
+//      of a tile each, the group's requests as 8 blocks of 16): the group's
+//      embeddings go to LDS, then per tile z = inv_temp * (U + W2^T e) on
+//      v_mfma_f32_16x16x32_bf16, with the next tile's W2t rows and base
+//      logits loaded during the current tile's products; z stays in the
+//      accumulators (128 AGPRs per lane), and the per-tile statistics (max,
+//      sum of 2^(z - max)) go to memory;
+//   -  grid barrier;
+//   B  one wave per request: row maximum, total and draw tile (the md_stats
+//      computation);
+//   -  grid barrier;
+//   C  every workgroup writes p = 2^(z - M) / S for its tiles from the
+//      registers; the draws of the requests whose draw tile it owns are made
+//      eight at a time, one per wave: the tile's masses go through LDS, then
+//      the fp64 prefix in vocabulary order, x_k, and for k < K the gather of
+//      e_{k+1} and c_{k+1}.
+// The statistics and row records cross the barriers as device-coherent
+// (agent-scope) 64-bit stores and loads, which bypass the per-XCD L2, so the
+// barrier needs no L2 write-back or invalidation: a thread's stores are
+// complete (s_waitcnt) before its workgroup arrives.  Arrivals are counted per
+// group of workgroups (blockIdx % 8) and the last arrival of the last group
+// raises every group's flag, which that group's workgroups poll.  Barrier b
+// (b = 2L + 1, 2L + 2 for launch L of the block) completes when a group's
+// count reaches its size times b; md_first zeroes the counts and flags.
+// Residency: the grid never exceeds the workgroups the device holds at once,
+// so on an otherwise idle device every workgroup starts at once; if other
+// work holds CUs, the missing workgroups start when it ends.  A wait longer
+// than kSyncTimeout (2 s) gives up and sets the timeout word, after which
+// every barrier of the block returns at once and md_check marks the block's
+// outputs invalid (draft tokens -1, confidences NaN): the kernels always
+// finish.
+constexpr int kCoThreads = 512;
+constexpr int kCoWaves = kCoThreads / DSPARK_WAVE;  // 8: 16 entries of a tile each
+constexpr int kCoTiles = 4;                         // tiles per workgroup
+constexpr int kCoRows = 128;                        // requests per group
+constexpr int kCoRT = kCoRows / 16;
+constexpr uint64_t kSyncTimeout = 200000000ull;     // wall-clock ticks (100 MHz): 2 s
+static_assert(kCoWaves * 16 == kTileV, "the waves of a workgroup cover one tile");
+
+struct CoopArgs {
+    MarkovArgs a;
+    const uint16_t* E;  // embeddings of position k, row r at E + r * rank
+    uint16_t* E_next;   // embeddings of position k + 1
+    float2* stats;      // [R, ntiles]
+    RowInfo* info;      // [R]
+    const float* sh;    // w_h . h per (r, k), or null
+    unsigned* sync;     // kSyncWords barrier words
+    int ntiles, k, g0, ng;
+    unsigned launch;    // index L of this launch in the block
+};
+
+// Keeps a value in accumulation registers (AGPRs) at this point: z lives
+// there from the products to the normalisation, leaving the vector registers
+// to the loads and the row statistics.
+__device__ __forceinline__ void pin_acc(f32x4& v) { asm volatile("" : "+a"(v)); }
+
+__device__ __forceinline__ void grid_barrier(unsigned* sync, unsigned b) {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0);  // this thread's stores are complete
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const unsigned G = gridDim.x, x = blockIdx.x % kCoGroups;
+        const unsigned nx = (G - x + kCoGroups - 1) / kCoGroups, ngrp = min(G, (unsigned)kCoGroups);
+        if (__hip_atomic_fetch_add(sync + kSyncStride * (1 + x), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) +
+                    1u == nx * b &&
+            __hip_atomic_fetch_add(sync, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1u == ngrp * b) {
+            for (unsigned y = 0; y < ngrp; ++y)
+                __hip_atomic_store(sync + kSyncStride * (1 + kCoGroups + y), b, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+        }
+        unsigned* flag = sync + kSyncStride * (1 + kCoGroups + x);
+        const uint64_t t0 = wall_clock64();
+        while (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < b &&
+               __hip_atomic_load(sync + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u) {
+            __builtin_amdgcn_s_sleep(8);
+            if (wall_clock64() - t0 > kSyncTimeout)
+                __hip_atomic_store(sync + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+    __syncthreads();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+template <int KS>
+__global__ __launch_bounds__(kCoThreads) void md_coop(CoopArgs c) {
+    const MarkovArgs& a = c.a;
+    constexpr int kNch = 4 * KS;  // 16-byte chunks per embedding row
+    constexpr int kRank = 32 * KS;
+    constexpr int kECopy = kCoRows * kNch / kCoThreads;  // embedding chunks per thread
+    static_assert(kCoRows * kNch % kCoThreads == 0, "the embedding copy divides evenly");
+    __shared__ __align__(16) uint16_t se[kCoRows * kRank];
+    __shared__ float2 sst[kCoTiles][kCoWaves][kCoRows];
+    __shared__ RowInfo sinfo[kCoRows];
+    __shared__ float smass[kCoWaves][kTileV];
+    __shared__ int sdraw[kCoRows];
+    __shared__ int ndraw;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int lr = lane & 15;
+    const int lq = lane >> 4;
+    const int k = c.k, g0 = c.g0;
+    const int t0 = blockIdx.x * kCoTiles;
+    const int nt = min(kCoTiles, c.ntiles - t0);  // >= 1: the grid is ceil(ntiles / 4)
+    const unsigned G = gridDim.x;
+    const int R = c.ng;
+    const int nrt = (R + 15) >> 4;
+    constexpr float kLog2e = 1.4426950408889634f;
+    const float scale2 = a.inv_temp * kLog2e;
+
+    // A fragments of tile i (W2t rows, clamped into the vocabulary) and its
+    // base logits at position k for the group at g0 (entries 4 lq .. 4 lq + 3
+    // of this wave's 16, rows 16 rt + lr, 4 bf16 each)
+    bf16x8 af[2][KS];
+    uint2 ub[2][kCoRT];
+    auto load_tile = [&](int i, bf16x8 (&A)[KS], uint2 (&U)[kCoRT]) {
+        const int vt = (t0 + i) * kTileV + 16 * wave;
+        const uint16_t* src = a.W2t + (int64_t)min(vt + lr, a.V - 1) * kRank + 8 * lq;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) A[ks] = *(const bf16x8*)(src + 32 * ks);
+        const int vc = min(vt + 4 * lq, a.V - 4);  // V % 4 == 0
+#pragma unroll
+        for (int rt = 0; rt < kCoRT; ++rt) {
+            const int r = g0 + min(16 * rt + lr, R - 1);
+            U[rt] = *(const uint2*)((const uint16_t*)a.base + ((int64_t)r * a.K + (k - 1)) * a.ld + vc);
+        }
+    };
+    // the group's embeddings (rows past the group are zero), then the
+    // first tile, which stays in flight past the LDS stores
+    uint64_t ev[kECopy][2];
+#pragma unroll
+    for (int j = 0; j < kECopy; ++j) {
+        const int idx = tid + j * kCoThreads, t = idx / kNch, ch = idx % kNch;
+        const uint4 v = *(const uint4*)(c.E + (int64_t)(g0 + min(t, R - 1)) * kRank + 8 * ch);
+        ev[j][0] = t < R ? (uint64_t)v.x | ((uint64_t)v.y << 32) : 0u;
+        ev[j][1] = t < R ? (uint64_t)v.z | ((uint64_t)v.w << 32) : 0u;
+    }
+    load_tile(0, af[0], ub[0]);
+#pragma unroll
+    for (int j = 0; j < kECopy; ++j) {
+        const int idx = tid + j * kCoThreads, t = idx / kNch, ch = idx % kNch;
+        uint64_t* dst = (uint64_t*)(se + (t * kNch + eslot(t, ch, kNch)) * 8);
+        dst[0] = ev[j][0];
+        dst[1] = ev[j][1];
+    }
+    lds_barrier();
+
+    // ---- A: products, z in the accumulators, tile statistics
+    f32x4 acc[kCoTiles][kCoRT];
+#pragma unroll
+    for (int i = 0; i < kCoTiles; ++i) {
+        if (i + 1 < nt) load_tile(i + 1, af[(i + 1) & 1], ub[(i + 1) & 1]);
+#pragma unroll
+        for (int rt = 0; rt < kCoRT; ++rt) {
+            acc[i][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+            pin_acc(acc[i][rt]);
+        }
+        if (i < nt) {
+#pragma unroll
+            for (int rt = 0; rt < kCoRT; ++rt) {
+                if (rt < nrt) {
+                    const int t = 16 * rt + lr;
+#pragma unroll
+                    for (int ks = 0; ks < KS; ++ks) {
+                        const bf16x8 b = *(const bf16x8*)(se + (t * kNch + eslot(t, 4 * ks + lq, kNch)) * 8);
+                        acc[i][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i & 1][ks], b, acc[i][rt], 0, 0, 0);
+                    }
+                }
+            }
+            const int vb = (t0 + i) * kTileV + 16 * wave + 4 * lq;
+#pragma unroll
+            for (int rt = 0; rt < kCoRT; ++rt) {
+                const bool ok = vb < a.V && 16 * rt + lr < R;
+                const uint2 w = ub[i & 1][rt];
+                const float u[4] = {__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u),
+                                    __uint_as_float(w.y << 16), __uint_as_float(w.y & 0xffff0000u)};
+                float m = -__builtin_huge_valf();
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float z = ok ? scale2 * (u[e] + acc[i][rt][e]) : -__builtin_huge_valf();
+                    acc[i][rt][e] = z;
+                    m = fmaxf(m, z);
+                }
+                m = quad_max(m);
+                float s = 0.0f;
+                if (m > -__builtin_huge_valf()) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) s += __builtin_amdgcn_exp2f(acc[i][rt][e] - m);
+                }
+                s = quad_sum(s);
+                if (lq == 0) sst[i][wave][16 * rt + lr] = float2{m, s};
+                pin_acc(acc[i][rt]);
+            }
+        }
+    }
+    lds_barrier();
+    {
+        const int i = tid / kCoRows, r = tid % kCoRows;  // 512 threads: every (tile, request)
+        if (i < nt && r < R) {
+            float M = -__builtin_huge_valf();
+#pragma unroll
+            for (int w = 0; w < kCoWaves; ++w) M = fmaxf(M, sst[i][w][r].x);
+            float S = 0.0f;
+            if (M > -__builtin_huge_valf()) {
+#pragma unroll
+                for (int w = 0; w < kCoWaves; ++w)
+                    if (sst[i][w][r].x > -__builtin_huge_valf())
+                        S += sst[i][w][r].y * exp2f(sst[i][w][r].x - M);
+            }
+            st_f2<true>(c.stats + (int64_t)(g0 + r) * c.ntiles + t0 + i, float2{M, S});
+        }
+    }
+    grid_barrier(c.sync, 2u * c.launch + 1u);
+
+    // ---- B: row statistics, one wave per request
+    for (int r = blockIdx.x + (int)G * wave; r < R; r += (int)G * kCoWaves)
+        row_stats<16, true>(a, c.stats, c.info, c.ntiles, k, g0 + r, lane);
+    grid_barrier(c.sync, 2u * c.launch + 2u);
+#pragma unroll
+    for (int i = 0; i < kCoTiles; ++i)
+#pragma unroll
+        for (int rt = 0; rt < kCoRT; ++rt) pin_acc(acc[i][rt]);
+
+    // ---- C: p from the registers, then the draws of the tiles owned here
+    if (tid == 0) ndraw = 0;
+    if (tid < R) sinfo[tid] = ld_info<true>(c.info + g0 + tid);
+    lds_barrier();
+    if (tid < R) {
+        const int ti = sinfo[tid].tile - t0;
+        if (ti >= 0 && ti < nt) sdraw[atomicAdd(&ndraw, 1)] = tid;
+    }
+    float rm[kCoRT], rinv[kCoRT];
+#pragma unroll
+    for (int rt = 0; rt < kCoRT; ++rt) {
+        const RowInfo ri = sinfo[min(16 * rt + lr, R - 1)];
+        rm[rt] = ri.M;
+        rinv[rt] = 1.0f / ri.S;
+    }
+#pragma unroll
+    for (int i = 0; i < kCoTiles; ++i) {
+        const int vb = (t0 + i) * kTileV + 16 * wave + 4 * lq;
+        if (i < nt && vb < a.V) {
+#pragma unroll
+            for (int rt = 0; rt < kCoRT; ++rt) {
+                const int r = 16 * rt + lr;
+                if (r < R) {
+                    float* out = a.draft_p + ((int64_t)(g0 + r) * a.K + (k - 1)) * a.V + vb;
+                    *(float4*)out = float4{__builtin_amdgcn_exp2f(acc[i][rt][0] - rm[rt]) * rinv[rt],
+                                           __builtin_amdgcn_exp2f(acc[i][rt][1] - rm[rt]) * rinv[rt],
+                                           __builtin_amdgcn_exp2f(acc[i][rt][2] - rm[rt]) * rinv[rt],
+                                           __builtin_amdgcn_exp2f(acc[i][rt][3] - rm[rt]) * rinv[rt]};
+                }
+            }
+        }
+    }
+    lds_barrier();  // the draw list is complete (the p stores drain meanwhile)
+    const int nd = ndraw;
+    for (int j0 = 0; j0 < nd; j0 += kCoWaves) {
+        // every wave puts its 16 entries of each draw tile of this round into LDS
+        for (int j = j0; j < min(nd, j0 + kCoWaves); ++j) {
+            const int rl = sdraw[j];
+            const int ti = sinfo[rl].tile - t0;
+            const float M = sinfo[rl].M;
+#pragma unroll
+            for (int i = 0; i < kCoTiles; ++i)
+#pragma unroll
+                for (int rt = 0; rt < kCoRT; ++rt)
+                    if (i == ti && 16 * rt + lr == rl) {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            smass[j - j0][16 * wave + 4 * lq + e] = __builtin_amdgcn_exp2f(acc[i][rt][e] - M);
+                    }
+        }
+        lds_barrier();
+        if (j0 + wave < nd) {  // wave w makes draw j0 + w
+            const int rl = sdraw[j0 + wave];
+            const RowInfo ri = sinfo[rl];
+            const int r = g0 + rl;
+            const int64_t row = (int64_t)r * a.K + (k - 1);
+            const double m0 = smass[wave][2 * lane], m1 = smass[wave][2 * lane + 1];
+            double incl = m0 + m1;
+#pragma unroll
+            for (int o = 1; o < DSPARK_WAVE; o <<= 1) {
+                const double t = __shfl_up(incl, o, DSPARK_WAVE);
+                if (lane >= o) incl += t;
+            }
+            const double before = incl - (m0 + m1);  // mass before entry 2 * lane
+            // first entry whose running mass passes thr (zero masses are never drawn)
+            const int cand = before + m0 > ri.thr && m0 > 0.0 ? 2 * lane
+                             : incl > ri.thr && m1 > 0.0    ? 2 * lane + 1
+                                                            : kTileV;
+            int first = cand;
+#pragma unroll
+            for (int o = 32; o > 0; o >>= 1) first = min(first, __shfl_xor(first, o, DSPARK_WAVE));
+            // rounding: the tile's last entry with mass
+            int last = m1 > 0.0 ? 2 * lane + 1 : m0 > 0.0 ? 2 * lane : -1;
+#pragma unroll
+            for (int o = 32; o > 0; o >>= 1) last = max(last, __shfl_xor(last, o, DSPARK_WAVE));
+            const int x = ri.tile * kTileV + (first < kTileV ? first : max(last, 0));
+            const bool ok = prev_token(a, r, k) >= 0;
+            if (lane == 0) a.draft_tok[row] = ok ? x : -1;
+            if (k < a.K) {
+                const uint16_t* w1 = a.W1 + (int64_t)(ok ? x : 0) * a.rank;
+                for (int q8 = lane * 8; q8 < a.rank; q8 += DSPARK_WAVE * 8)
+                    *(uint4*)(c.E_next + (int64_t)r * a.rank + q8) = *(const uint4*)(w1 + q8);
+                const float sc = embed_dot(a, w1, lane) + (c.sh ? c.sh[row + 1] : 0.0f);
+                if (lane == 0) a.conf[row + 1] = ok ? confidence(a, sc, k + 1) : __builtin_nanf("");
+            }
+        }
+        lds_barrier();
+    }
+}
+
+// After the block's md_coop launches: when one of their barriers gave up
+// waiting, no output of the block is valid (draft tokens -1, confidences NaN).
+__global__ __launch_bounds__(kThreads) void md_check(MarkovArgs a, const unsigned* sync) {
+    if (sync[1] == 0u) return;
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i < (int64_t)a.R * a.K) {
+        a.draft_tok[i] = -1;
+        a.conf[i] = __builtin_nanf("");
+    }
 }
 
 // ------------------------------------------------------------ RNN head
@@ -754,7 +1146,7 @@ hipError_t launch_rnn_ks(const MarkovArgs& a, uint16_t* Ee, uint16_t* E3, float*
     }
     const float* shp = a.d > 0 ? sh : nullptr;
     const float* hpp = a.d > 0 ? Hp : nullptr;
-    hipLaunchKernelGGL(md_first, dim3(ceil_div(a.R, kWaves)), dim3(kThreads), 0, s, a, shp, Ee);
+    hipLaunchKernelGGL(md_first, dim3(ceil_div(a.R, kWaves)), dim3(kThreads), 0, s, a, shp, Ee, (unsigned*)nullptr);
     for (int k = 1; k <= a.K; ++k) {
         // s_{k-1} in fp32 and as three terms (unread at k = 1), and where s_k goes
         const float* sp = (k & 1) ? S1 : S0;
@@ -769,18 +1161,62 @@ hipError_t launch_rnn_ks(const MarkovArgs& a, uint16_t* Ee, uint16_t* E3, float*
     return hipGetLastError();
 }
 
+// Workgroups of md_coop<KS> that the current device holds at once (0 when
+// it cannot tell); computed once per device.
+template <int KS>
+int coop_grid_limit() {
+    constexpr int kMaxDevices = 64;
+    static int cache[kMaxDevices];  // 0: not yet asked, -1: none
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
+    if (cache[dev] == 0) {
+        int cus = 0, nb = 0;
+        const bool ok = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+                        hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, md_coop<KS>, kCoThreads, 0) == hipSuccess;
+        cache[dev] = ok && nb * cus > 0 ? nb * cus : -1;
+    }
+    return cache[dev] > 0 ? cache[dev] : 0;
+}
+
 template <int KS>
 hipError_t launch_ks(const MarkovArgs& a, uint16_t* E0, uint16_t* E1, float2* stats, RowInfo* info,
-                     float* sh, int ntiles, bool vec, hipStream_t s) {
+                     float* sh, unsigned* sync, int ntiles, bool vec, hipStream_t s) {
     const int64_t rows = (int64_t)a.R * a.K;
     if (a.d > 0) hipLaunchKernelGGL(md_hidden, dim3((unsigned)ceil_div((int)rows, kWaves)), dim3(kThreads), 0, s, a, sh);
     const float* shp = a.d > 0 ? sh : nullptr;
-    hipLaunchKernelGGL(md_first, dim3(ceil_div(a.R, kWaves)), dim3(kThreads), 0, s, a, shp, E0);
+    hipLaunchKernelGGL(md_first, dim3(ceil_div(a.R, kWaves)), dim3(kThreads), 0, s, a, shp, E0, sync);
+    // one md_coop launch per position and group of 128 requests where its
+    // grid fits the device at once; three launches per position otherwise
+    const int G = ceil_div(ntiles, kCoTiles);
+    const bool coop = vec && a.base_bf16 && ntiles <= DSPARK_WAVE * 16 && G <= coop_grid_limit<KS>();
+    unsigned launch = 0;
     for (int k = 1; k <= a.K; ++k) {
         uint16_t* Ek = (k & 1) ? E0 : E1;
         uint16_t* En = (k & 1) ? E1 : E0;
-        position<KS, 1>(a, Ek, stats, info, En, shp, ntiles, k, vec, s);
+        if (!coop) {
+            position<KS, 1>(a, Ek, stats, info, En, shp, ntiles, k, vec, s);
+            continue;
+        }
+        for (int g0 = 0; g0 < a.R; g0 += kCoRows) {
+            CoopArgs c;
+            c.a = a;
+            c.E = Ek;
+            c.E_next = En;
+            c.stats = stats;
+            c.info = info;
+            c.sh = shp;
+            c.sync = sync;
+            c.ntiles = ntiles;
+            c.k = k;
+            c.g0 = g0;
+            c.ng = std::min(kCoRows, a.R - g0);
+            c.launch = launch++;
+            hipLaunchKernelGGL(md_coop<KS>, dim3(G), dim3(kCoThreads), 0, s, c);
+        }
     }
+    if (coop)
+        hipLaunchKernelGGL(md_check, dim3((unsigned)ceil_div((int)rows, kThreads)), dim3(kThreads), 0, s, a,
+                           (const unsigned*)sync);
     return hipGetLastError();
 }
 
@@ -790,7 +1226,7 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 namespace {
 struct WsLayout {
-    size_t e, stats, info, sh, total;
+    size_t e, stats, info, sh, sync, total;
 };
 WsLayout ws_layout(int R, int K, int V, int rank) {
     const int ntiles = mkd::ceil_div(V, mkd::kTileV);
@@ -799,7 +1235,8 @@ WsLayout ws_layout(int R, int K, int V, int rank) {
     l.stats = align256((size_t)R * ntiles * sizeof(float2));
     l.info = align256((size_t)R * sizeof(mkd::RowInfo));
     l.sh = align256((size_t)R * K * sizeof(float));
-    l.total = 2 * l.e + l.stats + l.info + l.sh;
+    l.sync = align256(mkd::kSyncWords * sizeof(unsigned));  // md_coop's barrier words
+    l.total = 2 * l.e + l.stats + l.info + l.sh + l.sync;
     return l;
 }
 }  // namespace
@@ -868,14 +1305,15 @@ hipError_t launch_markov(const MarkovArgs& a, void* ws, hipStream_t s) {
     float2* stats = (float2*)(p + 2 * l.e);
     mkd::RowInfo* info = (mkd::RowInfo*)(p + 2 * l.e + l.stats);
     float* sh = (float*)(p + 2 * l.e + l.stats + l.info);
+    unsigned* sync = (unsigned*)(p + 2 * l.e + l.stats + l.info + l.sh);
     const size_t eb = a.base_bf16 ? 2 : 4;
     const bool vec = a.V % 4 == 0 && a.ld % 4 == 0 && ((uintptr_t)a.base % (4 * eb)) == 0 &&
                      ((uintptr_t)a.draft_p % 16) == 0;
     switch (a.rank) {
-        case 32: return mkd::launch_ks<1>(a, E0, E1, stats, info, sh, ntiles, vec, s);
-        case 64: return mkd::launch_ks<2>(a, E0, E1, stats, info, sh, ntiles, vec, s);
-        case 128: return mkd::launch_ks<4>(a, E0, E1, stats, info, sh, ntiles, vec, s);
-        default: return mkd::launch_ks<8>(a, E0, E1, stats, info, sh, ntiles, vec, s);
+        case 32: return mkd::launch_ks<1>(a, E0, E1, stats, info, sh, sync, ntiles, vec, s);
+        case 64: return mkd::launch_ks<2>(a, E0, E1, stats, info, sh, sync, ntiles, vec, s);
+        case 128: return mkd::launch_ks<4>(a, E0, E1, stats, info, sh, sync, ntiles, vec, s);
+        default: return mkd::launch_ks<8>(a, E0, E1, stats, info, sh, sync, ntiles, vec, s);
     }
 }
 

@@ -105,6 +105,15 @@ def test_draft_wide_vocabulary():
     _compare(w, case, tok, p, conf, "wide vocabulary")
 
 
+def test_draft_wide_aligned_vocabulary():
+    # bf16 base logits and V % 4 == 0 but 1094 tiles: more than one
+    # cooperative grid holds, so each position takes the three-launch form
+    w = synth.scaled(synth.WORKLOADS["serving"], R=5, K=2, V=140000)
+    case = guard.draft_case(w, 10, rank=128, d=16)
+    tok, p, conf = _run_gpu(w, case, 128, 16)
+    _compare(w, case, tok, p, conf, "wide aligned vocabulary")
+
+
 def test_draft_invalid_anchor():
     # anchors outside [0, V) mark their requests: tokens -1, confidences NaN;
     # the other requests are unaffected
