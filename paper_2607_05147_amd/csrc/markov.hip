@@ -612,8 +612,10 @@ void position(const MarkovArgs& a, const uint16_t* E, float2* stats, RowInfo* in
 // workgroup per CU), with z held in registers from the product to the
 // normalisation, so that it never goes through memory: the projection and
 // the base logits are read once and p is written once.
-//   A  workgroup g owns the tiles 4g .. 4g + 3 (8 waves, 16 vocabulary entries
-//      of a tile each, the group's requests as 8 blocks of 16): the group's
+//   A  workgroup g owns the tiles g, g + G, g + 2G, g + 3G (G workgroups; 8
+//      waves, 16 vocabulary entries of a tile each, the group's requests as 8
+//      blocks of 16), so that at each step the grid reads one contiguous
+//      stretch of W2t and of every base-logit row: the group's
 //      embeddings go to LDS, then per tile z = inv_temp * (U + W2^T e) on
 //      v_mfma_f32_16x16x32_bf16, with the next tile's W2t rows and base
 //      logits loaded during the current tile's products; z stays in the
@@ -714,8 +716,11 @@ __global__ __launch_bounds__(kCoThreads) void md_coop(CoopArgs c) {
     const int lr = lane & 15;
     const int lq = lane >> 4;
     const int k = c.k, g0 = c.g0;
-    const int t0 = blockIdx.x * kCoTiles;
-    const int nt = min(kCoTiles, c.ntiles - t0);  // >= 1: the grid is ceil(ntiles / 4)
+    // tiles g, g + G, g + 2G, g + 3G: at each step the grid reads one
+    // contiguous stretch of every base-logit row and of W2t
+    const int Gt = gridDim.x;
+    const int nt = min(kCoTiles, (c.ntiles - (int)blockIdx.x + Gt - 1) / Gt);  // >= 1
+    auto tile_of = [&](int i) { return (int)blockIdx.x + i * Gt; };
     const unsigned G = gridDim.x;
     const int R = c.ng;
     const int nrt = (R + 15) >> 4;
@@ -728,7 +733,7 @@ __global__ __launch_bounds__(kCoThreads) void md_coop(CoopArgs c) {
     bf16x8 af[2][KS];
     uint2 ub[2][kCoRT];
     auto load_tile = [&](int i, bf16x8 (&A)[KS], uint2 (&U)[kCoRT]) {
-        const int vt = (t0 + i) * kTileV + 16 * wave;
+        const int vt = tile_of(i) * kTileV + 16 * wave;
         const uint16_t* src = a.W2t + (int64_t)min(vt + lr, a.V - 1) * kRank + 8 * lq;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) A[ks] = *(const bf16x8*)(src + 32 * ks);
@@ -781,7 +786,7 @@ __global__ __launch_bounds__(kCoThreads) void md_coop(CoopArgs c) {
                     }
                 }
             }
-            const int vb = (t0 + i) * kTileV + 16 * wave + 4 * lq;
+            const int vb = tile_of(i) * kTileV + 16 * wave + 4 * lq;
 #pragma unroll
             for (int rt = 0; rt < kCoRT; ++rt) {
                 const bool ok = vb < a.V && 16 * rt + lr < R;
@@ -821,7 +826,7 @@ __global__ __launch_bounds__(kCoThreads) void md_coop(CoopArgs c) {
                     if (sst[i][w][r].x > -__builtin_huge_valf())
                         S += sst[i][w][r].y * exp2f(sst[i][w][r].x - M);
             }
-            st_f2<true>(c.stats + (int64_t)(g0 + r) * c.ntiles + t0 + i, float2{M, S});
+            st_f2<true>(c.stats + (int64_t)(g0 + r) * c.ntiles + tile_of(i), float2{M, S});
         }
     }
     grid_barrier(c.sync, 2u * c.launch + 1u);
@@ -835,45 +840,23 @@ __global__ __launch_bounds__(kCoThreads) void md_coop(CoopArgs c) {
 #pragma unroll
         for (int rt = 0; rt < kCoRT; ++rt) pin_acc(acc[i][rt]);
 
-    // ---- C: p from the registers, then the draws of the tiles owned here
+    // ---- C: the draws of the tiles owned here, then p from the registers
+    // (the draws first: a load waits for every store issued before it, and
+    // the draw's gathers would queue behind the p stores)
     if (tid == 0) ndraw = 0;
     if (tid < R) sinfo[tid] = ld_info<true>(c.info + g0 + tid);
     lds_barrier();
     if (tid < R) {
-        const int ti = sinfo[tid].tile - t0;
-        if (ti >= 0 && ti < nt) sdraw[atomicAdd(&ndraw, 1)] = tid;
+        const int d = sinfo[tid].tile - (int)blockIdx.x;
+        if (d >= 0 && d % Gt == 0 && d / Gt < nt) sdraw[atomicAdd(&ndraw, 1)] = tid;
     }
-    float rm[kCoRT], rinv[kCoRT];
-#pragma unroll
-    for (int rt = 0; rt < kCoRT; ++rt) {
-        const RowInfo ri = sinfo[min(16 * rt + lr, R - 1)];
-        rm[rt] = ri.M;
-        rinv[rt] = 1.0f / ri.S;
-    }
-#pragma unroll
-    for (int i = 0; i < kCoTiles; ++i) {
-        const int vb = (t0 + i) * kTileV + 16 * wave + 4 * lq;
-        if (i < nt && vb < a.V) {
-#pragma unroll
-            for (int rt = 0; rt < kCoRT; ++rt) {
-                const int r = 16 * rt + lr;
-                if (r < R) {
-                    float* out = a.draft_p + ((int64_t)(g0 + r) * a.K + (k - 1)) * a.V + vb;
-                    *(float4*)out = float4{__builtin_amdgcn_exp2f(acc[i][rt][0] - rm[rt]) * rinv[rt],
-                                           __builtin_amdgcn_exp2f(acc[i][rt][1] - rm[rt]) * rinv[rt],
-                                           __builtin_amdgcn_exp2f(acc[i][rt][2] - rm[rt]) * rinv[rt],
-                                           __builtin_amdgcn_exp2f(acc[i][rt][3] - rm[rt]) * rinv[rt]};
-                }
-            }
-        }
-    }
-    lds_barrier();  // the draw list is complete (the p stores drain meanwhile)
+    lds_barrier();  // the draw list is complete
     const int nd = ndraw;
     for (int j0 = 0; j0 < nd; j0 += kCoWaves) {
         // every wave puts its 16 entries of each draw tile of this round into LDS
         for (int j = j0; j < min(nd, j0 + kCoWaves); ++j) {
             const int rl = sdraw[j];
-            const int ti = sinfo[rl].tile - t0;
+            const int ti = (sinfo[rl].tile - (int)blockIdx.x) / Gt;
             const float M = sinfo[rl].M;
 #pragma unroll
             for (int i = 0; i < kCoTiles; ++i)
@@ -921,7 +904,32 @@ __global__ __launch_bounds__(kCoThreads) void md_coop(CoopArgs c) {
                 if (lane == 0) a.conf[row + 1] = ok ? confidence(a, sc, k + 1) : __builtin_nanf("");
             }
         }
-        lds_barrier();
+        // (after the last round the other waves go on to the p stores)
+        if (j0 + kCoWaves < nd) lds_barrier();
+    }
+    float rm[kCoRT], rinv[kCoRT];
+#pragma unroll
+    for (int rt = 0; rt < kCoRT; ++rt) {
+        const RowInfo ri = sinfo[min(16 * rt + lr, R - 1)];
+        rm[rt] = ri.M;
+        rinv[rt] = 1.0f / ri.S;
+    }
+#pragma unroll
+    for (int i = 0; i < kCoTiles; ++i) {
+        const int vb = tile_of(i) * kTileV + 16 * wave + 4 * lq;
+        if (i < nt && vb < a.V) {
+#pragma unroll
+            for (int rt = 0; rt < kCoRT; ++rt) {
+                const int r = 16 * rt + lr;
+                if (r < R) {
+                    float* out = a.draft_p + ((int64_t)(g0 + r) * a.K + (k - 1)) * a.V + vb;
+                    *(float4*)out = float4{__builtin_amdgcn_exp2f(acc[i][rt][0] - rm[rt]) * rinv[rt],
+                                           __builtin_amdgcn_exp2f(acc[i][rt][1] - rm[rt]) * rinv[rt],
+                                           __builtin_amdgcn_exp2f(acc[i][rt][2] - rm[rt]) * rinv[rt],
+                                           __builtin_amdgcn_exp2f(acc[i][rt][3] - rm[rt]) * rinv[rt]};
+                }
+            }
+        }
     }
 }
 
