@@ -337,6 +337,48 @@ dspark_status dspark_rnn_draft(const int32_t* anchor, const void* base_logits,
                                int R, int K, int V, int32_t* draft_tok, float* draft_p,
                                float* conf, void* ws, size_t ws_bytes, dspark_stream stream);
 
+/* ------------------------------------------------------------------------
+ * Input checks: the device-side values of a call, looked at before it.
+ *
+ * The stages clamp the values that live in device memory so that no access
+ * leaves the buffers described above, and skip the requests that break a
+ * rule; two kinds of value cannot be caught that way.  A block-table entry
+ * names a page of a cache whose size dspark_verify_attn is not told, so an
+ * entry past the cache is read as if it were a page; and a uniform or a
+ * confidence outside its range changes the result without any access going
+ * astray.  Each check enqueues one small kernel on `stream` (nothing is
+ * synchronised) that writes the first rule broken -- the smallest request
+ * index, then the rule order below -- to `report`, a device int32[4]:
+ *   {code, request, index, value}, code 0 = every rule holds.
+ * The caller reads it once the stream has run the check, before the call it
+ * guards.  Bad sizes or pointers -> EINVAL with nothing enqueued.
+ *
+ * dspark_check_verify_inputs (dspark_verify_attn's block_table, max_pages,
+ * kv_len, cu_q, R, max_q, page_size, and num_pages, the number of pages of
+ * the cache): code 1 rows cu_q[r] .. cu_q[r+1]-1 not inside
+ * [0, min(cu_q[R], R*max_q)) or cu_q decreasing (index 0: value cu_q[r];
+ * 1: cu_q[r+1]); 2 q_len_r above max_q (value q_len_r); 3 kv_len_r outside
+ * [q_len_r, max_pages*page_size] (value kv_len_r); 4 a block-table entry of a
+ * page the request reads outside [0, num_pages) (index: logical page, value:
+ * the entry).
+ * dspark_check_accept_inputs (dspark_accept's cu_q, u (nullable), R, K):
+ * code 1 rows as above with R*(K+1); 2 len_r = q_len_r - 1 outside [0, K];
+ * 3 u[r, t] (t = 0 .. K) outside [0, 1) or NaN (index t, value: the float's
+ * bits).
+ * dspark_check_schedule_inputs (dspark_schedule's conf, R, K): code 1
+ * conf[r, j] outside [0, 1] or NaN (index j, value: the float's bits).
+ * ---------------------------------------------------------------------- */
+dspark_status dspark_check_verify_inputs(const int32_t* block_table, int max_pages,
+                                         const int32_t* kv_len, const int32_t* cu_q, int R,
+                                         int max_q, int page_size, int num_pages, int32_t* report,
+                                         dspark_stream stream);
+
+dspark_status dspark_check_accept_inputs(const int32_t* cu_q, const float* u, int R, int K,
+                                         int32_t* report, dspark_stream stream);
+
+dspark_status dspark_check_schedule_inputs(const float* conf, int R, int K, int32_t* report,
+                                           dspark_stream stream);
+
 #ifdef __cplusplus
 }
 #endif

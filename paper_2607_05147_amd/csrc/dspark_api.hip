@@ -522,4 +522,43 @@ dspark_status dspark_rnn_draft(const int32_t* anchor, const void* base_logits,
     return hip_status(dspark::launch_rnn(a, ws, (hipStream_t)stream), "dspark_rnn_draft");
 }
 
+// ---- input checks ---------------------------------------------------------------
+
+dspark_status dspark_check_verify_inputs(const int32_t* block_table, int max_pages, const int32_t* kv_len,
+                                         const int32_t* cu_q, int R, int max_q, int page_size, int num_pages,
+                                         int32_t* report, dspark_stream stream) {
+    if (R < 1 || R > kMaxR) return fail(DSPARK_EINVAL, "R=%d outside [1, %d]", R, kMaxR);
+    if (max_q < 1 || max_pages < 1 || page_size < 1 || num_pages < 1)
+        return fail(DSPARK_EINVAL, "max_q=%d max_pages=%d page_size=%d num_pages=%d", max_q, max_pages,
+                    page_size, num_pages);
+    if ((int64_t)max_pages * page_size > INT32_MAX)
+        return fail(DSPARK_EUNSUPPORTED, "context bound max_pages*page_size too large");
+    if (!block_table || !kv_len || !cu_q || !report) return fail(DSPARK_EINVAL, "null argument");
+    if (!aligned(block_table, 4) || !aligned(kv_len, 4) || !aligned(cu_q, 4) || !aligned(report, 4))
+        return fail(DSPARK_EINVAL, "misaligned pointer");
+    return hip_status(dspark::launch_check_verify(block_table, max_pages, kv_len, cu_q, R, max_q, page_size,
+                                                  num_pages, report, (hipStream_t)stream),
+                      "dspark_check_verify_inputs");
+}
+
+dspark_status dspark_check_accept_inputs(const int32_t* cu_q, const float* u, int R, int K, int32_t* report,
+                                         dspark_stream stream) {
+    if (R < 1 || R > kMaxR) return fail(DSPARK_EINVAL, "R=%d outside [1, %d]", R, kMaxR);
+    if (K < 0 || K > kMaxK) return fail(DSPARK_EINVAL, "K=%d outside [0, %d]", K, kMaxK);
+    if (!cu_q || !report) return fail(DSPARK_EINVAL, "null argument");
+    if (!aligned(cu_q, 4) || !aligned(u, 4) || !aligned(report, 4)) return fail(DSPARK_EINVAL, "misaligned pointer");
+    return hip_status(dspark::launch_check_accept(cu_q, u, R, K, report, (hipStream_t)stream),
+                      "dspark_check_accept_inputs");
+}
+
+dspark_status dspark_check_schedule_inputs(const float* conf, int R, int K, int32_t* report,
+                                           dspark_stream stream) {
+    if (R < 1 || R > kMaxR) return fail(DSPARK_EINVAL, "R=%d outside [1, %d]", R, kMaxR);
+    if (K < 0 || K > kMaxK) return fail(DSPARK_EINVAL, "K=%d outside [0, %d]", K, kMaxK);
+    if ((K > 0 && !conf) || !report) return fail(DSPARK_EINVAL, "null argument");
+    if (!aligned(conf, 4) || !aligned(report, 4)) return fail(DSPARK_EINVAL, "misaligned pointer");
+    return hip_status(dspark::launch_check_schedule(conf, R, K, report, (hipStream_t)stream),
+                      "dspark_check_schedule_inputs");
+}
+
 }  // extern "C"

@@ -93,4 +93,12 @@ bool markov_rank_supported(int rank);
 int markov_max_vocab();  // per-tile statistics of one request fit one workgroup
 hipError_t launch_markov(const MarkovArgs& a, void* ws, hipStream_t s);
 
+// ---- input checks (device-side values) -------------------------------------------
+hipError_t launch_check_verify(const int32_t* block_table, int max_pages, const int32_t* kv_len,
+                               const int32_t* cu_q, int R, int max_q, int page_size, int num_pages,
+                               int32_t* report, hipStream_t s);
+hipError_t launch_check_accept(const int32_t* cu_q, const float* u, int R, int K, int32_t* report,
+                               hipStream_t s);
+hipError_t launch_check_schedule(const float* conf, int R, int K, int32_t* report, hipStream_t s);
+
 }  // namespace dspark

@@ -79,6 +79,12 @@ def lib():
         L.dspark_rnn_draft.restype = i32
         L.dspark_rnn_draft.argtypes = [p, p, i32, i64, p, p, p, i32, p, p, i32, p, p, f32, i32, i32,
                                        i32, p, p, p, p, sz, p]
+        L.dspark_check_verify_inputs.restype = i32
+        L.dspark_check_verify_inputs.argtypes = [p, i32, p, p, i32, i32, i32, i32, p, p]
+        L.dspark_check_accept_inputs.restype = i32
+        L.dspark_check_accept_inputs.argtypes = [p, p, i32, i32, p, p]
+        L.dspark_check_schedule_inputs.restype = i32
+        L.dspark_check_schedule_inputs.argtypes = [p, i32, i32, p, p]
         _lib = L
     return _lib
 
@@ -139,6 +145,79 @@ def dspark_schedule_workspace_size(R: int, K: int) -> int:
     return int(lib().dspark_schedule_workspace_size(R, K))
 
 
+# ---------------------------------------------------------------- input checks
+
+CHECK_RULES = {
+    "verify": {1: "rows of the request outside the batch (or cu_q decreasing)", 2: "q_len above max_q",
+               3: "kv_len outside [q_len, max_pages * page_size]", 4: "block-table entry outside the cache"},
+    "accept": {1: "rows of the request outside the batch (or cu_q decreasing)", 2: "len = q_len - 1 outside [0, K]",
+               3: "uniform outside [0, 1)"},
+    "schedule": {1: "confidence outside [0, 1]"},
+}
+
+
+def debug_checks() -> bool:
+    """DSPARK_DEBUG=1: the stage wrappers check their device-side inputs
+    first and raise on the first rule broken (each call then waits for its
+    check)."""
+    return os.environ.get("DSPARK_DEBUG", "0") not in ("", "0")
+
+
+def _report(report: torch.Tensor, kind: str, stream) -> Optional[tuple]:
+    (torch.cuda.current_stream(report.device) if stream is None else stream).synchronize()
+    code, r, i, v = (int(x) for x in report.cpu().tolist())
+    return None if code == 0 else (code, r, i, v, CHECK_RULES[kind].get(code, "?"))
+
+
+def check_verify_inputs(block_table: torch.Tensor, kv_len: torch.Tensor, cu_q: torch.Tensor, max_q: int,
+                        page_size: int, num_pages: int, stream=None) -> Optional[tuple]:
+    """First broken rule of dspark_verify_attn's device-side inputs as
+    (code, request, index, value, rule) or None; waits for the check."""
+    _dev(block_table, "block_table", torch.int32)
+    R, max_pages = block_table.shape
+    _dev(kv_len, "kv_len", torch.int32, (R,))
+    _dev(cu_q, "cu_q", torch.int32, (R + 1,))
+    report = torch.empty(4, dtype=torch.int32, device=cu_q.device)
+    st = lib().dspark_check_verify_inputs(_p(block_table), max_pages, _p(kv_len), _p(cu_q), R, max_q,
+                                          page_size, num_pages, _p(report), _stream(stream))
+    _raise(st, "dspark_check_verify_inputs")
+    return _report(report, "verify", stream)
+
+
+def check_accept_inputs(cu_q: torch.Tensor, u: Optional[torch.Tensor], K: int, stream=None) -> Optional[tuple]:
+    _dev(cu_q, "cu_q", torch.int32)
+    R = cu_q.numel() - 1
+    _dev(u, "u", torch.float32, (R, K + 1), optional=True)
+    report = torch.empty(4, dtype=torch.int32, device=cu_q.device)
+    st = lib().dspark_check_accept_inputs(_p(cu_q), _p(u), R, K, _p(report), _stream(stream))
+    _raise(st, "dspark_check_accept_inputs")
+    return _report(report, "accept", stream)
+
+
+def check_schedule_inputs(conf: torch.Tensor, stream=None) -> Optional[tuple]:
+    _dev(conf, "conf", torch.float32)
+    R, K = conf.shape
+    report = torch.empty(4, dtype=torch.int32, device=conf.device)
+    st = lib().dspark_check_schedule_inputs(_p(conf), R, K, _p(report), _stream(stream))
+    _raise(st, "dspark_check_schedule_inputs")
+    return _report(report, "schedule", stream)
+
+
+def _cache_pages(cache: torch.Tensor, strides: Sequence[int], heads: int, page_size: int, dim: int) -> int:
+    """Pages a flat cache holds: page p is readable when its last element,
+    p * s0 + (heads - 1) * s1 + (page_size - 1) * s2 + dim - 1, is inside."""
+    s0, s1, s2 = (int(x) for x in strides)
+    span = (heads - 1) * s1 + (page_size - 1) * s2 + dim
+    return max(0, (cache.numel() - span) // s0 + 1) if s0 > 0 else 0
+
+
+def _debug_raise(found: Optional[tuple], what: str) -> None:
+    if found is not None:
+        code, r, i, v, rule = found
+        raise DSparkError(f"{what}: input check failed: request {r}: {rule} (code {code}, index {i}, "
+                          f"value {v})", 1)
+
+
 def dspark_schedule(conf: torch.Tensor, sps: torch.Tensor, mode: int = 0,
                     len_out: Optional[torch.Tensor] = None, cu_q: Optional[torch.Tensor] = None,
                     tok_req: Optional[torch.Tensor] = None, want_tok_req: bool = False,
@@ -160,6 +239,8 @@ def dspark_schedule(conf: torch.Tensor, sps: torch.Tensor, mode: int = 0,
     _dev(cu_q, "cu_q", torch.int32, (R + 1,))
     _dev(tok_req, "tok_req", torch.int32, (R * (K + 1),), optional=True)
     ws, ws_bytes = _workspace(dspark_schedule_workspace_size(R, K), dev, ws)
+    if debug_checks() and K > 0:
+        _debug_raise(check_schedule_inputs(conf, stream), "dspark_schedule")
     st = lib().dspark_schedule(_p(conf), R, K, _p(sps), sps.numel(), mode, _p(len_out), _p(cu_q),
                                _p(tok_req), _p(ws), ws_bytes, _stream(stream))
     _raise(st, "dspark_schedule")
@@ -272,6 +353,11 @@ def dspark_verify_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Te
     need = dspark_verify_attn_workspace_size(R, max_q, Hq, Hkv, Dqk, Dv, max_pages, page_size,
                                              q.dtype)
     ws, ws_bytes = _workspace(need, q.device, ws)
+    if debug_checks():
+        num_pages = min(_cache_pages(k_cache, k_strides, Hkv, page_size, Dqk),
+                        _cache_pages(v_cache, v_strides, Hkv, page_size, Dv))
+        _debug_raise(check_verify_inputs(block_table, kv_len, cu_q, max_q, page_size, max(num_pages, 1),
+                                         stream), "dspark_verify_attn")
     ks = (C.c_int64 * 3)(*[int(x) for x in k_strides])
     vs = (C.c_int64 * 3)(*[int(x) for x in v_strides])
     st = lib().dspark_verify_attn(_p(q), _p(k_cache), _p(v_cache), ks, vs, _p(block_table),
@@ -321,6 +407,8 @@ def dspark_accept(draft_tok: torch.Tensor, logits: torch.Tensor, cu_q: torch.Ten
     _dev(accept_rate, "accept_rate", torch.float32, optional=True)
     need = dspark_accept_workspace_size(R, K, V)
     ws, ws_bytes = _workspace(need, dev, ws)
+    if debug_checks():
+        _debug_raise(check_accept_inputs(cu_q, u, K, stream), "dspark_accept")
     st = lib().dspark_accept(_p(draft_tok), _p(draft_p), C.c_void_p(logits.data_ptr()),
                              _DT[logits.dtype], ld, _p(u), _p(cu_q), R, K, V,
                              float(inv_temperature), _p(accepted_len), _p(next_tok),

@@ -203,6 +203,40 @@ def test_accept_validation(L):
     assert _acc(L, logits=C.c_void_p((1 << 20) + 1)) == EINVAL
 
 
+def test_input_check_validation(L):
+    def cv(bt=FAKE, mp=8, kv=FAKE, cu=FAKE, R=4, mq=9, ps=16, n=100, rep=FAKE):
+        return L.dspark_check_verify_inputs(bt, mp, kv, cu, R, mq, ps, n, rep, None)
+
+    assert cv(R=0) == EINVAL
+    assert cv(R=8193) == EINVAL
+    assert cv(mq=0) == EINVAL
+    assert cv(n=0) == EINVAL
+    assert cv(ps=0) == EINVAL
+    assert cv(mp=1 << 20, ps=1 << 12) == EUNSUPPORTED  # context bound past int32
+    assert cv(bt=None) == EINVAL
+    assert cv(rep=None) == EINVAL
+    assert cv(kv=C.c_void_p((1 << 20) + 2)) == EINVAL
+
+    def ca(cu=FAKE, u=FAKE, R=4, K=8, rep=FAKE):
+        return L.dspark_check_accept_inputs(cu, u, R, K, rep, None)
+
+    assert ca(R=0) == EINVAL
+    assert ca(K=-1) == EINVAL
+    assert ca(K=65) == EINVAL
+    assert ca(cu=None) == EINVAL
+    assert ca(rep=None) == EINVAL
+    assert ca(u=C.c_void_p((1 << 20) + 1)) == EINVAL
+
+    def cs(conf=FAKE, R=4, K=8, rep=FAKE):
+        return L.dspark_check_schedule_inputs(conf, R, K, rep, None)
+
+    assert cs(conf=None) == EINVAL  # conf is needed when K > 0
+    assert cs(R=8193) == EINVAL
+    assert cs(K=65) == EINVAL
+    assert cs(rep=None) == EINVAL
+    assert cs(rep=C.c_void_p((1 << 20) + 3)) == EINVAL
+
+
 def test_accept_workspace_size(L):
     assert L.dspark_accept_workspace_size(128, 16, 129280) > 0
     assert L.dspark_accept_workspace_size(0, 16, 129280) == 0
