@@ -118,7 +118,7 @@ ATTN_PATHS = {
                                               "md_stats", "md_norm"),
               "bound": "hbm"},
     "rnn_draft": {"src": "markov.hip", "kernels": ("md_hidden", "rnn_hproj", "md_first", "rnn_state",
-                                                   "md_tile", "md_stats", "md_norm"),
+                                                   "md_coop", "md_check", "md_tile", "md_stats", "md_norm"),
                   "bound": "hbm"},
     # not attention: the acceptance launches of one dspark_accept call (the
     # resolve kernel runs once per call)
@@ -682,8 +682,8 @@ def draft_bench(args):
     head = "RNN-head" if rnn else "Markov-head"
     log(f"{head} draft block: {ms.mean() * 1e3:.1f} us per call ({ms.mean() * 1e3 / w.K:.1f} us per "
         f"position), {gbps:.0f} GB/s = {gbps / HBM_PEAK_GBPS:.1%} of HBM peak")
-    kernels = ("dspark_rnn_draft: md_hidden + rnn_hproj + md_first, then rnn_state + md_tile + "
-               "md_stats + md_norm per position" if rnn else
+    kernels = ("dspark_rnn_draft: md_hidden + rnn_hproj + md_first, then rnn_state + md_coop per "
+               "position, md_check" if rnn else
                "dspark_markov_draft: md_hidden + md_first, then md_coop per position, md_check")
     result = {
         "metric": f"draft tokens/s and achieved HBM GB/s (% of peak), {head} draft block on 1 MI355X",

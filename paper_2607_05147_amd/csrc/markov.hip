@@ -9,9 +9,9 @@
 //   x_k = inverse CDF of p_k at u[r, k-1];   c_k = sigmoid(w . [h_k; e_k] / T_k).
 // Launches, all on one stream: md_hidden (the backbone part w_h . h_k of every
 // confidence logit, once) and md_first (e_1 and c_1), then per position k
-// either one md_coop launch per group of up to 128 requests (Markov head,
-// bf16 base logits, V % 4 == 0, a grid the device holds at once; md_check
-// after the block), which keeps z in registers across two grid-wide
+// either one md_coop launch per group of up to 128 requests (bf16 base
+// logits, V % 4 == 0, a grid the device holds at once; md_check after the
+// block), which keeps z in registers across two grid-wide
 // exchanges so that the projection and the base logits are read once and p
 // is written once, or the three launches:
 //   md_tile   one workgroup per 128 vocabulary entries: W2^T e for every
@@ -168,16 +168,16 @@ __global__ __launch_bounds__(kThreads) void md_first(MarkovArgs a, const float* 
 // stats[r * ntiles + tile] = (max z, sum 2^(z - max)).
 // VEC: 4 consecutive entries per lane are loaded / stored as one vector
 // (V, ld multiples of 4, aligned rows).
-// NT: bf16 terms of the B operand per request (1: the embedding itself; 3:
-// an fp32 vector split as hi + mid + lo, each term a bf16 rounding of what the
-// previous ones leave, so the products reproduce the fp32 vector's to fp32
-// accuracy); E row r holds the NT terms one after the other.
+// NT: bf16 terms of the B operand per request (1: the embedding itself; 2:
+// the RNN head's fp32 output split as hi + mid, the second term the bf16
+// rounding of what the first leaves, so the products see the fp32 vector to
+// within 2^-16 of each entry); E row r holds the NT terms one after the other.
 // BF16: the base logits' type.  Their loads are branch-free (clamped
 // indices; entries past V are masked with the rest of the tile), so they issue
 // back to back and stay in flight during the products.  Occupancy: three
-// waves per SIMD for one term; two for three terms (three times the staged
-// embedding loads), which leaves their loads room without spilling (measured
-// faster).
+// waves per SIMD for one term; two for more terms (more staged embedding
+// loads), which leaves their loads room without spilling (measured faster
+// with three terms).
 template <int KS, int NT, bool VEC, bool BF16>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 1 ? 3 : 2, 4))) void md_tile(
     MarkovArgs a, const uint16_t* E, float2* stats, int ntiles, int k) {
@@ -211,7 +211,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 
         // below wait only for the embeddings (loads complete in order), and the
         // base logits stay in flight during the products
         // (measured: this guarded form schedules better than clamped, unguarded
-        // loads, by 1.4x on the three-term product)
+        // loads, by 1.4x on a three-term product)
         constexpr int kCopy = ceil_div(NT * kChunkR * kNch, kThreads);
         uint4 ev[kCopy];
 #pragma unroll
@@ -606,8 +606,10 @@ void position(const MarkovArgs& a, const uint16_t* E, float2* stats, RowInfo* in
 
 // ----------------------------------------------------------------- md_coop
 
-// One position of the Markov head (bf16 base logits, V % 4 == 0, at most 1024
-// tiles) for a group of up to 128 requests in one launch whose workgroups are
+// One position of either head (bf16 base logits, V % 4 == 0, at most 1024
+// tiles; NT B terms per request: the Markov head's embedding, or the RNN
+// head's output as two terms, whose products add up in the accumulators) for
+// a group of up to 128 requests in one launch whose workgroups are
 // all resident at once (the grid is at most what the device holds, one
 // workgroup per CU), with z held in registers from the product to the
 // normalisation, so that it never goes through memory: the projection and
@@ -625,11 +627,11 @@ void position(const MarkovArgs& a, const uint16_t* E, float2* stats, RowInfo* in
 //   B  one wave per request: row maximum, total and draw tile (the md_stats
 //      computation);
 //   -  grid barrier;
-//   C  every workgroup writes p = 2^(z - M) / S for its tiles from the
-//      registers; the draws of the requests whose draw tile it owns are made
-//      eight at a time, one per wave: the tile's masses go through LDS, then
-//      the fp64 prefix in vocabulary order, x_k, and for k < K the gather of
-//      e_{k+1} and c_{k+1}.
+//   C  the draws of the requests whose draw tile a workgroup owns, eight at
+//      a time, one per wave: the tile's masses go through LDS, then the fp64
+//      prefix in vocabulary order, x_k, and for k < K the gather of e_{k+1}
+//      and c_{k+1}; then every workgroup writes p = 2^(z - M) / S for its
+//      tiles from the registers.
 // The statistics and row records cross the barriers as device-coherent
 // (agent-scope) 64-bit stores and loads, which bypass the per-XCD L2, so the
 // barrier needs no L2 write-back or invalidation: a thread's stores are
@@ -651,11 +653,12 @@ constexpr int kCoTiles = 4;                         // tiles per workgroup
 constexpr int kCoRows = 128;                        // requests per group
 constexpr int kCoRT = kCoRows / 16;
 constexpr uint64_t kSyncTimeout = 200000000ull;     // wall-clock ticks (100 MHz): 2 s
+constexpr int kCoLds = 160 * 1024;                  // LDS of one workgroup (and CU)
 static_assert(kCoWaves * 16 == kTileV, "the waves of a workgroup cover one tile");
 
 struct CoopArgs {
     MarkovArgs a;
-    const uint16_t* E;  // embeddings of position k, row r at E + r * rank
+    const uint16_t* E;  // B operand of position k: row r at E + r * NT * rank (NT bf16 terms)
     uint16_t* E_next;   // embeddings of position k + 1
     float2* stats;      // [R, ntiles]
     RowInfo* info;      // [R]
@@ -697,19 +700,31 @@ __device__ __forceinline__ void grid_barrier(unsigned* sync, unsigned b) {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
-template <int KS>
+template <int KS, int NT>
 __global__ __launch_bounds__(kCoThreads) void md_coop(CoopArgs c) {
     const MarkovArgs& a = c.a;
     constexpr int kNch = 4 * KS;  // 16-byte chunks per embedding row
     constexpr int kRank = 32 * KS;
-    constexpr int kECopy = kCoRows * kNch / kCoThreads;  // embedding chunks per thread
-    static_assert(kCoRows * kNch % kCoThreads == 0, "the embedding copy divides evenly");
-    __shared__ __align__(16) uint16_t se[kCoRows * kRank];
-    __shared__ float2 sst[kCoTiles][kCoWaves][kCoRows];
-    __shared__ RowInfo sinfo[kCoRows];
-    __shared__ float smass[kCoWaves][kTileV];
-    __shared__ int sdraw[kCoRows];
-    __shared__ int ndraw;
+    constexpr int kECopy = NT * kCoRows * kNch / kCoThreads;  // embedding chunks per thread
+    static_assert(NT * kCoRows * kNch % kCoThreads == 0, "the embedding copy divides evenly");
+    // LDS: the group's embeddings (NT terms per request), the per-wave tile
+    // statistics, and phase C's draw records, which take the embeddings'
+    // place when the three do not fit side by side (the embeddings are no
+    // longer read by then)
+    constexpr int kSeBytes = NT * kCoRows * kRank * 2;
+    constexpr int kSstBytes = kCoTiles * kCoWaves * kCoRows * (int)sizeof(float2);
+    constexpr int kInfoBytes = kCoRows * (int)sizeof(RowInfo), kMassBytes = kCoWaves * kTileV * 4;
+    constexpr int kDrawBytes = kInfoBytes + kMassBytes + (kCoRows + 4) * 4;
+    constexpr bool kShare = kSeBytes + kSstBytes + kDrawBytes > kCoLds;
+    static_assert(kSeBytes + kSstBytes <= kCoLds && kDrawBytes <= kSeBytes, "md_coop's LDS fits");
+    __shared__ __align__(16) unsigned char smem[kSeBytes + kSstBytes + (kShare ? 0 : kDrawBytes)];
+    uint16_t* const se = (uint16_t*)smem;
+    float2(*const sst)[kCoWaves][kCoRows] = (float2(*)[kCoWaves][kCoRows])(smem + kSeBytes);
+    unsigned char* const sdr = smem + (kShare ? 0 : kSeBytes + kSstBytes);
+    RowInfo* const sinfo = (RowInfo*)sdr;
+    float(*const smass)[kTileV] = (float(*)[kTileV])(sdr + kInfoBytes);
+    int* const sdraw = (int*)(sdr + kInfoBytes + kMassBytes);
+    int& ndraw = sdraw[kCoRows];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -749,16 +764,17 @@ __global__ __launch_bounds__(kCoThreads) void md_coop(CoopArgs c) {
     uint64_t ev[kECopy][2];
 #pragma unroll
     for (int j = 0; j < kECopy; ++j) {
-        const int idx = tid + j * kCoThreads, t = idx / kNch, ch = idx % kNch;
-        const uint4 v = *(const uint4*)(c.E + (int64_t)(g0 + min(t, R - 1)) * kRank + 8 * ch);
+        const int idx = tid + j * kCoThreads, t = idx / (NT * kNch), q = idx % (NT * kNch);
+        const uint4 v = *(const uint4*)(c.E + (int64_t)(g0 + min(t, R - 1)) * (NT * kRank) + 8 * q);
         ev[j][0] = t < R ? (uint64_t)v.x | ((uint64_t)v.y << 32) : 0u;
         ev[j][1] = t < R ? (uint64_t)v.z | ((uint64_t)v.w << 32) : 0u;
     }
     load_tile(0, af[0], ub[0]);
 #pragma unroll
     for (int j = 0; j < kECopy; ++j) {
-        const int idx = tid + j * kCoThreads, t = idx / kNch, ch = idx % kNch;
-        uint64_t* dst = (uint64_t*)(se + (t * kNch + eslot(t, ch, kNch)) * 8);
+        const int idx = tid + j * kCoThreads, t = idx / (NT * kNch), q = idx % (NT * kNch);
+        const int nt = q / kNch, ch = q % kNch;
+        uint64_t* dst = (uint64_t*)(se + ((nt * kCoRows + t) * kNch + eslot(t, ch, kNch)) * 8);
         dst[0] = ev[j][0];
         dst[1] = ev[j][1];
     }
@@ -780,10 +796,14 @@ __global__ __launch_bounds__(kCoThreads) void md_coop(CoopArgs c) {
                 if (rt < nrt) {
                     const int t = 16 * rt + lr;
 #pragma unroll
-                    for (int ks = 0; ks < KS; ++ks) {
-                        const bf16x8 b = *(const bf16x8*)(se + (t * kNch + eslot(t, 4 * ks + lq, kNch)) * 8);
-                        acc[i][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i & 1][ks], b, acc[i][rt], 0, 0, 0);
-                    }
+                    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+                        for (int ks = 0; ks < KS; ++ks) {
+                            const bf16x8 b =
+                                *(const bf16x8*)(se + ((nt * kCoRows + t) * kNch + eslot(t, 4 * ks + lq, kNch)) * 8);
+                            acc[i][rt] =
+                                __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i & 1][ks], b, acc[i][rt], 0, 0, 0);
+                        }
                 }
             }
             const int vb = tile_of(i) * kTileV + 16 * wave + 4 * lq;
@@ -944,6 +964,55 @@ __global__ __launch_bounds__(kThreads) void md_check(MarkovArgs a, const unsigne
     }
 }
 
+// Workgroups of md_coop<KS, NT> that the current device holds at once (0 when
+// it cannot tell); computed once per device.
+template <int KS, int NT>
+int coop_grid_limit() {
+    constexpr int kMaxDevices = 64;
+    static int cache[kMaxDevices];  // 0: not yet asked, -1: none
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
+    if (cache[dev] == 0) {
+        int cus = 0, nb = 0;
+        const bool ok = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+                        hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, md_coop<KS, NT>, kCoThreads, 0) == hipSuccess;
+        cache[dev] = ok && nb * cus > 0 ? nb * cus : -1;
+    }
+    return cache[dev] > 0 ? cache[dev] : 0;
+}
+
+// One position as md_coop launches, one per group of up to 128 requests
+// (launch counts the block's launches: it numbers their barriers).
+template <int KS, int NT>
+void coop_position(const MarkovArgs& a, const uint16_t* E, uint16_t* En, float2* stats, RowInfo* info,
+                   const float* shp, unsigned* sync, int ntiles, int k, unsigned& launch, hipStream_t s) {
+    const int G = ceil_div(ntiles, kCoTiles);
+    for (int g0 = 0; g0 < a.R; g0 += kCoRows) {
+        CoopArgs c;
+        c.a = a;
+        c.E = E;
+        c.E_next = En;
+        c.stats = stats;
+        c.info = info;
+        c.sh = shp;
+        c.sync = sync;
+        c.ntiles = ntiles;
+        c.k = k;
+        c.g0 = g0;
+        c.ng = std::min(kCoRows, a.R - g0);
+        c.launch = launch++;
+        hipLaunchKernelGGL((md_coop<KS, NT>), dim3(G), dim3(kCoThreads), 0, s, c);
+    }
+}
+
+// md_coop applies: bf16 base logits, V % 4 == 0 (vec), at most 1024 tiles
+// (the row statistics' 16 tiles per lane), and a grid the device holds at once.
+template <int KS, int NT>
+bool coop_applies(const MarkovArgs& a, int ntiles, bool vec) {
+    return vec && a.base_bf16 && ntiles <= DSPARK_WAVE * 16 &&
+           ceil_div(ntiles, kCoTiles) <= coop_grid_limit<KS, NT>();
+}
+
 // ------------------------------------------------------------ RNN head
 
 // The backbone part of the RNN head's projection (eq. rnn), once for every
@@ -1030,8 +1099,13 @@ __global__ __launch_bounds__(kThreads) void rnn_hproj(MarkovArgs a, float* Hp) {
     }
 }
 
-// hi + mid + lo: each term the bf16 rounding of what the previous ones leave,
-// so that their sum is v to fp32 accuracy
+// hi + mid (+ lo): each term the bf16 rounding of what the previous ones
+// leave; hi + mid is v to within 2^-16 |v|, hi + mid + lo to fp32 accuracy
+__device__ __forceinline__ void split2(float v, uint16_t* dst, int stride) {
+    const uint16_t hi = f32_to_bf16(v);
+    dst[0] = hi;
+    dst[stride] = f32_to_bf16(v - bf16_to_f32(hi));
+}
 __device__ __forceinline__ void split3(float v, uint16_t* dst, int stride) {
     const uint16_t hi = f32_to_bf16(v);
     const float r1 = v - bf16_to_f32(hi);
@@ -1050,7 +1124,8 @@ __device__ __forceinline__ void split3(float v, uint16_t* dst, int stride) {
 // 16 state dims, so a lane holds all three pre-activations of one (request,
 // dim) and applies the gated update in registers: s_k = g s_{k-1} + (1 - g)
 // tanh(a_c) with g = sigmoid(a_g), written in fp32 and as three terms, and the
-// head's output o_k = tanh(a_o) as three terms for md_tile.  A workgroup owns
+// head's output o_k = tanh(a_o) as two terms (hi, mid) for the vocabulary
+// product.  A workgroup owns
 // 16 dims x 16 requests; its four waves take every fourth 32-input step (both
 // operands straight from memory, kStDepth steps ahead) and wave 0 adds the
 // four partial products in wave order.  The state is double-buffered (others
@@ -1059,7 +1134,7 @@ constexpr int kStJ = 16, kStR = 16, kStDepth = 4;
 __global__ __launch_bounds__(kThreads) void rnn_state(MarkovArgs a, const float* Hp,
                                                       const float* s_prev, const uint16_t* S3_prev,
                                                       float* s_next, uint16_t* S3_next,
-                                                      const uint16_t* Ee, uint16_t* E3, int k) {
+                                                      const uint16_t* Ee, uint16_t* E2, int k) {
     __shared__ f32x4 part[kWaves - 1][3][DSPARK_WAVE];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int lr = lane & 15, lq = lane >> 4;
@@ -1138,14 +1213,14 @@ __global__ __launch_bounds__(kThreads) void rnn_state(MarkovArgs a, const float*
         const float sn = g * sp + (1.0f - g) * tanhf(ac);
         s_next[(int64_t)r * rank + j] = sn;
         split3(sn, S3_next + (int64_t)r * 3 * rank + j, rank);
-        split3(tanhf(ao), E3 + (int64_t)r * 3 * rank + j, rank);
+        split2(tanhf(ao), E2 + (int64_t)r * 2 * rank + j, rank);
     }
 }
 
 template <int KS>
-hipError_t launch_rnn_ks(const MarkovArgs& a, uint16_t* Ee, uint16_t* E3, float* S0, float* S1,
+hipError_t launch_rnn_ks(const MarkovArgs& a, uint16_t* Ee, uint16_t* E2, float* S0, float* S1,
                          uint16_t* T0, uint16_t* T1, float* Hp, float2* stats, RowInfo* info,
-                         float* sh, int ntiles, bool vec, hipStream_t s) {
+                         float* sh, unsigned* sync, int ntiles, bool vec, hipStream_t s) {
     const int64_t rows = (int64_t)a.R * a.K;
     if (a.d > 0) {
         hipLaunchKernelGGL(md_hidden, dim3((unsigned)ceil_div((int)rows, kWaves)), dim3(kThreads), 0, s, a, sh);
@@ -1154,7 +1229,11 @@ hipError_t launch_rnn_ks(const MarkovArgs& a, uint16_t* Ee, uint16_t* E3, float*
     }
     const float* shp = a.d > 0 ? sh : nullptr;
     const float* hpp = a.d > 0 ? Hp : nullptr;
-    hipLaunchKernelGGL(md_first, dim3(ceil_div(a.R, kWaves)), dim3(kThreads), 0, s, a, shp, Ee, (unsigned*)nullptr);
+    hipLaunchKernelGGL(md_first, dim3(ceil_div(a.R, kWaves)), dim3(kThreads), 0, s, a, shp, Ee, sync);
+    // the vocabulary product with the output's two terms: md_coop where it
+    // applies, else md_tile, md_stats and md_norm
+    const bool coop = coop_applies<KS, 2>(a, ntiles, vec);
+    unsigned launch = 0;
     for (int k = 1; k <= a.K; ++k) {
         // s_{k-1} in fp32 and as three terms (unread at k = 1), and where s_k goes
         const float* sp = (k & 1) ? S1 : S0;
@@ -1162,28 +1241,15 @@ hipError_t launch_rnn_ks(const MarkovArgs& a, uint16_t* Ee, uint16_t* E3, float*
         const uint16_t* tp = (k & 1) ? T1 : T0;
         uint16_t* tn = (k & 1) ? T0 : T1;
         hipLaunchKernelGGL(rnn_state, dim3(a.rank / kStJ, ceil_div(a.R, kStR)), dim3(kThreads), 0, s, a, hpp,
-                           sp, tp, sn, tn, (const uint16_t*)Ee, E3, k);
+                           sp, tp, sn, tn, (const uint16_t*)Ee, E2, k);
         // the draw gathers W1[x_k] into Ee: the embedding input of position k + 1
-        position<KS, 3>(a, E3, stats, info, Ee, shp, ntiles, k, vec, s);
+        if (coop) coop_position<KS, 2>(a, E2, Ee, stats, info, shp, sync, ntiles, k, launch, s);
+        else position<KS, 2>(a, E2, stats, info, Ee, shp, ntiles, k, vec, s);
     }
+    if (coop)
+        hipLaunchKernelGGL(md_check, dim3((unsigned)ceil_div((int)rows, kThreads)), dim3(kThreads), 0, s, a,
+                           (const unsigned*)sync);
     return hipGetLastError();
-}
-
-// Workgroups of md_coop<KS> that the current device holds at once (0 when
-// it cannot tell); computed once per device.
-template <int KS>
-int coop_grid_limit() {
-    constexpr int kMaxDevices = 64;
-    static int cache[kMaxDevices];  // 0: not yet asked, -1: none
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
-    if (cache[dev] == 0) {
-        int cus = 0, nb = 0;
-        const bool ok = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-                        hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, md_coop<KS>, kCoThreads, 0) == hipSuccess;
-        cache[dev] = ok && nb * cus > 0 ? nb * cus : -1;
-    }
-    return cache[dev] > 0 ? cache[dev] : 0;
 }
 
 template <int KS>
@@ -1193,34 +1259,15 @@ hipError_t launch_ks(const MarkovArgs& a, uint16_t* E0, uint16_t* E1, float2* st
     if (a.d > 0) hipLaunchKernelGGL(md_hidden, dim3((unsigned)ceil_div((int)rows, kWaves)), dim3(kThreads), 0, s, a, sh);
     const float* shp = a.d > 0 ? sh : nullptr;
     hipLaunchKernelGGL(md_first, dim3(ceil_div(a.R, kWaves)), dim3(kThreads), 0, s, a, shp, E0, sync);
-    // one md_coop launch per position and group of 128 requests where its
-    // grid fits the device at once; three launches per position otherwise
-    const int G = ceil_div(ntiles, kCoTiles);
-    const bool coop = vec && a.base_bf16 && ntiles <= DSPARK_WAVE * 16 && G <= coop_grid_limit<KS>();
+    // one md_coop launch per position and group of 128 requests where it
+    // applies; three launches per position otherwise
+    const bool coop = coop_applies<KS, 1>(a, ntiles, vec);
     unsigned launch = 0;
     for (int k = 1; k <= a.K; ++k) {
         uint16_t* Ek = (k & 1) ? E0 : E1;
         uint16_t* En = (k & 1) ? E1 : E0;
-        if (!coop) {
-            position<KS, 1>(a, Ek, stats, info, En, shp, ntiles, k, vec, s);
-            continue;
-        }
-        for (int g0 = 0; g0 < a.R; g0 += kCoRows) {
-            CoopArgs c;
-            c.a = a;
-            c.E = Ek;
-            c.E_next = En;
-            c.stats = stats;
-            c.info = info;
-            c.sh = shp;
-            c.sync = sync;
-            c.ntiles = ntiles;
-            c.k = k;
-            c.g0 = g0;
-            c.ng = std::min(kCoRows, a.R - g0);
-            c.launch = launch++;
-            hipLaunchKernelGGL(md_coop<KS>, dim3(G), dim3(kCoThreads), 0, s, c);
-        }
+        if (coop) coop_position<KS, 1>(a, Ek, En, stats, info, shp, sync, ntiles, k, launch, s);
+        else position<KS, 1>(a, Ek, stats, info, En, shp, ntiles, k, vec, s);
     }
     if (coop)
         hipLaunchKernelGGL(md_check, dim3((unsigned)ceil_div((int)rows, kThreads)), dim3(kThreads), 0, s, a,
@@ -1252,23 +1299,25 @@ WsLayout ws_layout(int R, int K, int V, int rank) {
 size_t markov_workspace(int R, int K, int V, int rank) { return ws_layout(R, K, V, rank).total; }
 
 namespace {
-// RNN head: the embedding input Ee, the three-term output E3, two state
-// buffers, the backbone part of the projection, then what the Markov head uses
+// RNN head: the embedding input Ee, the two-term output E2, two state
+// buffers (fp32 and three terms), the backbone part of the projection, then
+// what the Markov head uses
 struct RnnLayout {
-    size_t ee, e3, st, st3, hp, stats, info, sh, total;
+    size_t ee, e2, st, st3, hp, stats, info, sh, sync, total;
 };
 RnnLayout rnn_layout(int R, int K, int V, int rank) {
     const int ntiles = mkd::ceil_div(V, mkd::kTileV);
     RnnLayout l;
     l.ee = align256((size_t)R * rank * 2);
-    l.e3 = align256((size_t)R * 3 * rank * 2);
+    l.e2 = align256((size_t)R * 2 * rank * 2);
     l.st = align256((size_t)R * rank * 4);
     l.st3 = align256((size_t)R * 3 * rank * 2);
     l.hp = align256((size_t)R * K * 3 * rank * 4);
     l.stats = align256((size_t)R * ntiles * sizeof(float2));
     l.info = align256((size_t)R * sizeof(mkd::RowInfo));
     l.sh = align256((size_t)R * K * sizeof(float));
-    l.total = l.ee + l.e3 + 2 * l.st + 2 * l.st3 + l.hp + l.stats + l.info + l.sh;
+    l.sync = align256(mkd::kSyncWords * sizeof(unsigned));
+    l.total = l.ee + l.e2 + 2 * l.st + 2 * l.st3 + l.hp + l.stats + l.info + l.sh + l.sync;
     return l;
 }
 }  // namespace
@@ -1280,7 +1329,7 @@ hipError_t launch_rnn(const MarkovArgs& a, void* ws, hipStream_t s) {
     const RnnLayout l = rnn_layout(a.R, a.K, a.V, a.rank);
     char* p = (char*)ws;
     uint16_t* Ee = (uint16_t*)p;                 p += l.ee;
-    uint16_t* E3 = (uint16_t*)p;                 p += l.e3;
+    uint16_t* E2 = (uint16_t*)p;                 p += l.e2;
     float* S0 = (float*)p;                       p += l.st;
     float* S1 = (float*)p;                       p += l.st;
     uint16_t* T0 = (uint16_t*)p;                 p += l.st3;
@@ -1288,15 +1337,16 @@ hipError_t launch_rnn(const MarkovArgs& a, void* ws, hipStream_t s) {
     float* Hp = (float*)p;                       p += l.hp;
     float2* stats = (float2*)p;                  p += l.stats;
     mkd::RowInfo* info = (mkd::RowInfo*)p;       p += l.info;
-    float* sh = (float*)p;
+    float* sh = (float*)p;                       p += l.sh;
+    unsigned* sync = (unsigned*)p;
     const size_t eb = a.base_bf16 ? 2 : 4;
     const bool vec = a.V % 4 == 0 && a.ld % 4 == 0 && ((uintptr_t)a.base % (4 * eb)) == 0 &&
                      ((uintptr_t)a.draft_p % 16) == 0;
     switch (a.rank) {
-        case 32: return mkd::launch_rnn_ks<1>(a, Ee, E3, S0, S1, T0, T1, Hp, stats, info, sh, ntiles, vec, s);
-        case 64: return mkd::launch_rnn_ks<2>(a, Ee, E3, S0, S1, T0, T1, Hp, stats, info, sh, ntiles, vec, s);
-        case 128: return mkd::launch_rnn_ks<4>(a, Ee, E3, S0, S1, T0, T1, Hp, stats, info, sh, ntiles, vec, s);
-        default: return mkd::launch_rnn_ks<8>(a, Ee, E3, S0, S1, T0, T1, Hp, stats, info, sh, ntiles, vec, s);
+        case 32: return mkd::launch_rnn_ks<1>(a, Ee, E2, S0, S1, T0, T1, Hp, stats, info, sh, sync, ntiles, vec, s);
+        case 64: return mkd::launch_rnn_ks<2>(a, Ee, E2, S0, S1, T0, T1, Hp, stats, info, sh, sync, ntiles, vec, s);
+        case 128: return mkd::launch_rnn_ks<4>(a, Ee, E2, S0, S1, T0, T1, Hp, stats, info, sh, sync, ntiles, vec, s);
+        default: return mkd::launch_rnn_ks<8>(a, Ee, E2, S0, S1, T0, T1, Hp, stats, info, sh, sync, ntiles, vec, s);
     }
 }
 

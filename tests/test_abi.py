@@ -312,7 +312,7 @@ def test_rnn_draft_validation(L):
 
 def test_rnn_draft_workspace_size(L):
     n = L.dspark_rnn_draft_workspace_size(128, 16, 129280, 256)
-    # the Markov head's buffers plus the three-term output, two states and the
+    # the Markov head's buffers plus the two-term output, two states and the
     # hidden part of the projection for every position
     assert n >= L.dspark_markov_draft_workspace_size(128, 16, 129280, 256) + 128 * 16 * 768 * 4
     assert L.dspark_rnn_draft_workspace_size(128, 16, 129280, 96) == 0

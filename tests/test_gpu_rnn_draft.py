@@ -9,12 +9,15 @@ cores), so each carries a relative error of a few 2^-24 per term in the
 worst case and ~sqrt(n) 2^-24 typically; tanh and sigmoid add a few ulp, and
 the state recursion carries the error from position to position without
 amplifying it (|ds_k/ds_{k-1}| <= max g < 1 plus the candidate's bounded
-slope).  The output enters the vocabulary product as three bf16 terms whose
-sum is its fp32 value, so the bias W2^T o has the Markov head's error
-(rank 2^-24 sum_j |W2[j, v] o_j|) plus that of o, ~1e-5 relative at
-rank 256, d 4096.  Entries of p are compared at P_RTOL = 2e-4 relative, the
-Markov head's bound; confidences at C_ATOL = 2e-5 (their path is the Markov
-head's).
+slope).  The output enters the vocabulary product as two bf16 terms, hi +
+mid, whose sum is o_j to within 2^-16 |o_j|, so the bias W2^T o has the
+Markov head's error (rank 2^-24 sum_j |W2[j, v] o_j|) plus that of o, ~1e-5
+relative at rank 256, d 4096, plus sum_j W2[j, v] r_j for the residuals r_j
+of the split: rounding residuals of independent entries, which add up like
+a random walk, 1-2e-5 relative at the serving shape (2^-16 sum_j |W2[j, v]
+o_j| ~ 3e-4 only if every residual had the sign of its weight).  Entries of p
+are compared at P_RTOL = 2e-4 relative, the Markov head's bound; confidences
+at C_ATOL = 2e-5 (their path is the Markov head's).
 """
 import numpy as np
 import pytest
