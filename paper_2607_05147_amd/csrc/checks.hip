@@ -68,7 +68,7 @@ __global__ __launch_bounds__(kChkThreads) void chk_verify(const int32_t* block_t
             } else if (kv < ql || (int64_t)kv > (int64_t)max_pages * page_size) {
                 f = Finding{3, r, 0, kv};
             } else {
-                const int np = (kv + page_size - 1) / page_size;
+                const int np = (int)(((int64_t)kv + page_size - 1) / page_size);
                 for (int p = 0; p < np; ++p) {
                     const int e = block_table[(int64_t)r * max_pages + p];
                     if (e < 0 || e >= num_pages) {
