@@ -14,6 +14,10 @@
  *                            background section): greedy match or stochastic
  *                            rejection sampling, emitting the accepted length
  *                            and the corrected / bonus token per request.
+ * Upstream of them, the drafter's sequential stage (dspark_markov_draft,
+ * dspark_rnn_draft) produces the draft tokens, distributions and confidences
+ * they consume; dspark_check_*_inputs look at a call's device-side values
+ * before it.
  *
  * Conventions shared by every entry point
  *   - All array arguments are DEVICE pointers unless marked "host".  Arrays are
@@ -27,7 +31,9 @@
  *     dspark_last_error() then describes it (thread-local).  Values that live
  *     in device memory (lengths, tokens) cannot be checked on the host; the
  *     kernels clamp them into range as documented per call, so no access
- *     leaves the buffers described here.
+ *     leaves the buffers described here -- except through block-table
+ *     entries, which name pages of a cache whose size dspark_verify_attn is
+ *     not told (dspark_check_verify_inputs checks them).
  *   - A workspace must not be shared by two calls that may run concurrently.
  */
 #ifndef DSPARK_H
@@ -40,7 +46,7 @@
 extern "C" {
 #endif
 
-#define DSPARK_ABI_VERSION 2
+#define DSPARK_ABI_VERSION 3
 
 typedef enum {
     DSPARK_OK = 0,
