@@ -88,12 +88,15 @@ def test_draft_other_ranks(rank):
     _compare(w, case, tok, p, conf, f"rank {rank}")
 
 
-def test_draft_several_request_chunks():
-    # 150 requests: the embeddings stream through LDS in five chunks of 32
-    w = synth.scaled(synth.WORKLOADS["serving"], R=150, K=2, V=1024)
+@pytest.mark.parametrize("R,K", [(150, 2), (300, 3)])
+def test_draft_several_request_chunks(R, K):
+    # more requests than one cooperative launch takes: groups of 128 (the last
+    # partial), one launch per group and position, their grid barriers
+    # numbered across the block (three groups x three positions: nine launches)
+    w = synth.scaled(synth.WORKLOADS["serving"], R=R, K=K, V=1024)
     case = guard.draft_case(w, 4, rank=64, d=8)
     tok, p, conf = _run_gpu(w, case, 64, 8)
-    _compare(w, case, tok, p, conf, "150 requests")
+    _compare(w, case, tok, p, conf, f"{R} requests")
 
 
 def test_draft_wide_vocabulary():

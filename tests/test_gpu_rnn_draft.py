@@ -94,14 +94,16 @@ def test_rnn_draft_other_ranks(rank):
     _compare(w, case, tok, p, conf, f"rank {rank}")
 
 
-def test_rnn_draft_several_request_blocks():
-    # 150 requests: ten state blocks (the last one partial), five LDS chunks
-    # of the vocabulary product, 150 * 2 = 300 hidden rows (a partial 64-row
-    # block of the projection)
-    w = synth.scaled(synth.WORKLOADS["serving"], R=150, K=2, V=1024)
+@pytest.mark.parametrize("R,K", [(150, 2), (300, 3)])
+def test_rnn_draft_several_request_blocks(R, K):
+    # 150 requests: ten state blocks (the last one partial), two groups of the
+    # cooperative vocabulary product (128 + 22), 150 * 2 = 300 hidden rows (a
+    # partial 64-row block of the projection); 300 requests: three groups over
+    # three positions (nine launches, their barriers numbered across the block)
+    w = synth.scaled(synth.WORKLOADS["serving"], R=R, K=K, V=1024)
     case = guard.draft_case(w, 4, rank=64, d=8, head="rnn")
     tok, p, conf = _run_gpu(w, case, 8)
-    _compare(w, case, tok, p, conf, "150 requests")
+    _compare(w, case, tok, p, conf, f"{R} requests")
 
 
 def test_rnn_draft_long_block():
