@@ -373,6 +373,10 @@ dspark_status dspark_rnn_draft(const int32_t* anchor, const void* base_logits,
  * bits).
  * dspark_check_schedule_inputs (dspark_schedule's conf, R, K): code 1
  * conf[r, j] outside [0, 1] or NaN (index j, value: the float's bits).
+ * dspark_check_draft_inputs (dspark_markov_draft's and dspark_rnn_draft's u,
+ * sts_temp (nullable), R, K): code 1 a temperature sts_temp[k] not finite and
+ * positive (request -1, index k, value: the float's bits); 2 u[r, k] outside
+ * [0, 1) or NaN (index k, value: the float's bits).
  * ---------------------------------------------------------------------- */
 dspark_status dspark_check_verify_inputs(const int32_t* block_table, int max_pages,
                                          const int32_t* kv_len, const int32_t* cu_q, int R,
@@ -384,6 +388,9 @@ dspark_status dspark_check_accept_inputs(const int32_t* cu_q, const float* u, in
 
 dspark_status dspark_check_schedule_inputs(const float* conf, int R, int K, int32_t* report,
                                            dspark_stream stream);
+
+dspark_status dspark_check_draft_inputs(const float* u, const float* sts_temp, int R, int K,
+                                        int32_t* report, dspark_stream stream);
 
 #ifdef __cplusplus
 }

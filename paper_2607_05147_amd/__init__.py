@@ -15,7 +15,7 @@ _BINDING_NAMES = (
     "dspark_accept_workspace_size", "dspark_schedule_noalloc", "dspark_schedule_capacity",
     "dspark_schedule_topk", "dspark_markov_draft", "dspark_markov_draft_workspace_size",
     "dspark_rnn_draft", "dspark_rnn_draft_workspace_size", "check_verify_inputs",
-    "check_accept_inputs", "check_schedule_inputs", "debug_checks", "DSparkError",
+    "check_accept_inputs", "check_schedule_inputs", "check_draft_inputs", "debug_checks", "DSparkError",
 )
 
 

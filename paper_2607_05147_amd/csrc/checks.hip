@@ -136,6 +136,52 @@ __global__ __launch_bounds__(kChkThreads) void chk_schedule(const float* conf, i
     if (!done && threadIdx.x == 0) report[0] = report[1] = report[2] = report[3] = 0;
 }
 
+// Drafter inputs: 1 a per-position temperature T_k outside (0, inf) or NaN
+// (request -1, index k, value: its bits); 2 a uniform u[r, k] outside [0, 1)
+// or NaN (index k, value: its bits).
+__global__ __launch_bounds__(kChkThreads) void chk_draft(const float* u, const float* sts_temp, int R, int K,
+                                                         int32_t* report) {
+    __shared__ int s_temp;  // first bad temperature (K if none)
+    if (threadIdx.x == 0) s_temp = K;
+    __syncthreads();
+    if (sts_temp && (int)threadIdx.x < K) {
+        const float t = sts_temp[threadIdx.x];
+        if (!(t > 0.0f && t < __builtin_huge_valf())) atomicMin(&s_temp, (int)threadIdx.x);
+    }
+    __syncthreads();
+    if (s_temp < K) {
+        if (threadIdx.x == 0) {
+            report[0] = 1;
+            report[1] = -1;
+            report[2] = s_temp;
+            report[3] = (int)__float_as_uint(sts_temp[s_temp]);
+        }
+        return;
+    }
+    bool done = false;
+    for (int base = 0; base < R && !done; base += kChkThreads) {
+        const int r = base + (int)threadIdx.x;
+        Finding f{0, r, 0, 0};
+        if (r < R) {
+            for (int k = 0; k < K; ++k) {
+                const float x = u[(int64_t)r * K + k];
+                if (!(x >= 0.0f && x < 1.0f)) {
+                    f = Finding{2, r, k, (int)__float_as_uint(x)};
+                    break;
+                }
+            }
+        }
+        report_first(f, report, done);
+    }
+    if (!done && threadIdx.x == 0) report[0] = report[1] = report[2] = report[3] = 0;
+}
+
+hipError_t launch_check_draft(const float* u, const float* sts_temp, int R, int K, int32_t* report,
+                              hipStream_t s) {
+    hipLaunchKernelGGL(chk_draft, dim3(1), dim3(kChkThreads), 0, s, u, sts_temp, R, K, report);
+    return hipGetLastError();
+}
+
 hipError_t launch_check_verify(const int32_t* block_table, int max_pages, const int32_t* kv_len,
                                const int32_t* cu_q, int R, int max_q, int page_size, int num_pages,
                                int32_t* report, hipStream_t s) {

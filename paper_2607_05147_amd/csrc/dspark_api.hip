@@ -561,4 +561,15 @@ dspark_status dspark_check_schedule_inputs(const float* conf, int R, int K, int3
                       "dspark_check_schedule_inputs");
 }
 
+dspark_status dspark_check_draft_inputs(const float* u, const float* sts_temp, int R, int K, int32_t* report,
+                                        dspark_stream stream) {
+    if (R < 1 || R > kMaxR) return fail(DSPARK_EINVAL, "R=%d outside [1, %d]", R, kMaxR);
+    if (K < 1 || K > kMaxK) return fail(DSPARK_EINVAL, "K=%d outside [1, %d]", K, kMaxK);
+    if (!u || !report) return fail(DSPARK_EINVAL, "null argument");
+    if (!aligned(u, 4) || !aligned(sts_temp, 4) || !aligned(report, 4))
+        return fail(DSPARK_EINVAL, "misaligned pointer");
+    return hip_status(dspark::launch_check_draft(u, sts_temp, R, K, report, (hipStream_t)stream),
+                      "dspark_check_draft_inputs");
+}
+
 }  // extern "C"

@@ -100,5 +100,7 @@ hipError_t launch_check_verify(const int32_t* block_table, int max_pages, const 
 hipError_t launch_check_accept(const int32_t* cu_q, const float* u, int R, int K, int32_t* report,
                                hipStream_t s);
 hipError_t launch_check_schedule(const float* conf, int R, int K, int32_t* report, hipStream_t s);
+hipError_t launch_check_draft(const float* u, const float* sts_temp, int R, int K, int32_t* report,
+                              hipStream_t s);
 
 }  // namespace dspark

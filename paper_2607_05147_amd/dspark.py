@@ -85,6 +85,8 @@ def lib():
         L.dspark_check_accept_inputs.argtypes = [p, p, i32, i32, p, p]
         L.dspark_check_schedule_inputs.restype = i32
         L.dspark_check_schedule_inputs.argtypes = [p, i32, i32, p, p]
+        L.dspark_check_draft_inputs.restype = i32
+        L.dspark_check_draft_inputs.argtypes = [p, p, i32, i32, p, p]
         _lib = L
     return _lib
 
@@ -153,6 +155,7 @@ CHECK_RULES = {
     "accept": {1: "rows of the request outside the batch (or cu_q decreasing)", 2: "len = q_len - 1 outside [0, K]",
                3: "uniform outside [0, 1)"},
     "schedule": {1: "confidence outside [0, 1]"},
+    "draft": {1: "temperature not finite and positive", 2: "uniform outside [0, 1)"},
 }
 
 
@@ -201,6 +204,20 @@ def check_schedule_inputs(conf: torch.Tensor, stream=None) -> Optional[tuple]:
     st = lib().dspark_check_schedule_inputs(_p(conf), R, K, _p(report), _stream(stream))
     _raise(st, "dspark_check_schedule_inputs")
     return _report(report, "schedule", stream)
+
+
+def check_draft_inputs(u: torch.Tensor, sts_temp: Optional[torch.Tensor] = None,
+                       stream=None) -> Optional[tuple]:
+    """First broken rule of a draft block's uniforms [R, K] and per-position
+    temperatures [K] (request -1) as (code, request, index, value, rule) or
+    None; waits for the check."""
+    _dev(u, "u", torch.float32)
+    R, K = u.shape
+    _dev(sts_temp, "sts_temp", torch.float32, (K,), optional=True)
+    report = torch.empty(4, dtype=torch.int32, device=u.device)
+    st = lib().dspark_check_draft_inputs(_p(u), _p(sts_temp), R, K, _p(report), _stream(stream))
+    _raise(st, "dspark_check_draft_inputs")
+    return _report(report, "draft", stream)
 
 
 def _cache_pages(cache: torch.Tensor, strides: Sequence[int], heads: int, page_size: int, dim: int) -> int:
@@ -464,6 +481,8 @@ def dspark_markov_draft(anchor: torch.Tensor, base_logits: torch.Tensor, W1: tor
     if need == 0:
         raise DSparkError(f"unsupported shape: R={R} V={V} rank={rank}")
     ws, ws_bytes = _workspace(need, dev, ws)
+    if debug_checks():
+        _debug_raise(check_draft_inputs(u, sts_temp, stream), "dspark_markov_draft")
     st = lib().dspark_markov_draft(_p(anchor), C.c_void_p(base_logits.data_ptr()),
                                    _DT[base_logits.dtype], ld, _p(W1), _p(W2t), rank, _p(hidden),
                                    _p(w_conf), d, _p(sts_temp), _p(u), float(inv_temperature), R,
@@ -520,6 +539,8 @@ def dspark_rnn_draft(anchor: torch.Tensor, base_logits: torch.Tensor, W1: torch.
     if need == 0:
         raise DSparkError(f"unsupported shape: R={R} V={V} rank={rank}")
     ws, ws_bytes = _workspace(need, dev, ws)
+    if debug_checks():
+        _debug_raise(check_draft_inputs(u, sts_temp, stream), "dspark_rnn_draft")
     st = lib().dspark_rnn_draft(_p(anchor), C.c_void_p(base_logits.data_ptr()),
                                 _DT[base_logits.dtype], ld, _p(W1), _p(W2t), _p(Wrnn), rank,
                                 _p(hidden), _p(w_conf), d, _p(sts_temp), _p(u),

@@ -236,6 +236,15 @@ def test_input_check_validation(L):
     assert cs(rep=None) == EINVAL
     assert cs(rep=C.c_void_p((1 << 20) + 3)) == EINVAL
 
+    def cd(u=FAKE, t=FAKE, R=4, K=8, rep=FAKE):
+        return L.dspark_check_draft_inputs(u, t, R, K, rep, None)
+
+    assert cd(u=None) == EINVAL
+    assert cd(K=0) == EINVAL  # a draft block has at least one position
+    assert cd(R=0) == EINVAL
+    assert cd(rep=None) == EINVAL
+    assert cd(t=C.c_void_p((1 << 20) + 2)) == EINVAL
+
 
 def test_accept_workspace_size(L):
     assert L.dspark_accept_workspace_size(128, 16, 129280) > 0

@@ -259,3 +259,31 @@ def test_debug_mode_raises_before_accept_and_schedule(monkeypatch):
     conf[1, 2] = -0.5
     with pytest.raises(dspark.DSparkError, match="confidence outside"):
         dspark.dspark_schedule(to_dev(conf), to_dev(synth.sps_table(w)))
+
+
+def test_draft_uniforms_and_temperatures():
+    rng = np.random.default_rng(9)
+    R, K = 600, 16
+    u = rng.random((R, K), dtype=np.float32)
+    temp = (1.0 + 0.05 * np.arange(1, K + 1)).astype(np.float32)
+    assert dspark.check_draft_inputs(to_dev(u), to_dev(temp)) is None
+    assert dspark.check_draft_inputs(to_dev(u)) is None  # no temperatures: all 1
+    u[431, 15] = 1.0
+    assert dspark.check_draft_inputs(to_dev(u), to_dev(temp))[:4] == (2, 431, 15, _bits(1.0))
+    u[17, 3] = np.float32("inf")
+    assert dspark.check_draft_inputs(to_dev(u), to_dev(temp))[:4] == (2, 17, 3, _bits(np.inf))
+    temp[6] = 0.0  # a temperature is reported before any uniform
+    assert dspark.check_draft_inputs(to_dev(u), to_dev(temp))[:4] == (1, -1, 6, _bits(0.0))
+
+
+def test_debug_mode_raises_before_the_draft_block(monkeypatch):
+    monkeypatch.setenv("DSPARK_DEBUG", "1")
+    w = synth.scaled(synth.WORKLOADS["serving"], R=3, K=2, V=256)
+    inp = synth.markov_inputs(w, 0, rank=32, d=8)
+    args = [to_dev(inp.anchor), to_dev(inp.base), to_dev(inp.W1), to_dev(inp.W2t), to_dev(inp.w_conf)]
+    u = to_dev(inp.u)
+    dspark.dspark_markov_draft(*args, u, w.K, hidden=to_dev(inp.hidden), sts_temp=to_dev(inp.sts_temp))
+    torch.cuda.synchronize()
+    u[2, 1] = -0.5
+    with pytest.raises(dspark.DSparkError, match="uniform outside"):
+        dspark.dspark_markov_draft(*args, u, w.K, hidden=to_dev(inp.hidden), sts_temp=to_dev(inp.sts_temp))
