@@ -1,11 +1,12 @@
-// Input checks for the device-side values of the three stages.
+// Input checks for the device-side values of the three stages and the draft
+// block.
 //
 // The stages clamp what lives in device memory (row offsets, context
 // lengths, tokens) so that no access leaves the caller's buffers, and skip
 // requests whose values break the documented rules.  Two things cannot be
 // clamped: a block-table entry names a page of a cache whose size the call is
-// not told, and a uniform or confidence outside its range silently changes
-// the result.  These kernels look at the values before a call and report the
+// not told, and a uniform, confidence or temperature outside its range
+// silently changes the result.  These kernels look at the values before a call and report the
 // first rule broken (smallest request, then the rule's order below) as four
 // int32 {code, request, index, value bits}; code 0 means none.  One
 // workgroup walks the requests 256 at a time; it reads only the arrays and
